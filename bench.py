@@ -1,0 +1,199 @@
+"""Benchmark of the composed-prefill hot path on one MI355X.
+
+A step is one attention layer of one batch: compose (gather + RoPE
+re-rotation of cached units) -> append + causal GQA prefill attention of the
+computed rows (main stream), with retention of computed units running
+concurrently on a side stream and joined at the end of the step.  Steps
+rotate over --layers distinct layer buffer sets (pool, request KV, inputs),
+as consecutive model layers would, so one layer's data is not served from
+the previous step's caches.
+
+Prints one JSON line.  `value` is prompt tokens per second per layer.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0
+PEAK_MFMA_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def kv_elem_bytes(dtype):
+    return {"f32": 4, "bf16": 2, "e4m3": 1}[dtype]
+
+
+def cpu_baseline(wl, n_req):
+    """Time the CPU oracle on the first n_req requests of the same batch."""
+    import threadpoolctl
+    from oracle import pipeline as PL
+    from oracle.compose import retained_pages
+    info = threadpoolctl.threadpool_info()
+    cores = max([i.get("num_threads", 1) for i in info] + [1])
+    t0 = time.perf_counter()
+    toks = 0
+    for r in range(n_req):
+        PL.run_request(wl, r)
+        toks += wl.requests[r].prompt_len
+    sub = type(wl)(**{**vars(wl), "requests": wl.requests[:n_req]})
+    retained_pages(sub)
+    dt = time.perf_counter() - t0
+    return {"value": toks / dt, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"requests 0..{n_req - 1} of the batch ({toks} prompt tokens): "
+                      f"compose + append + attention (all heads, fp64) + retain; "
+                      f"{dt:.1f} s on {cores} BLAS threads (os.cpu_count()={os.cpu_count()})"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=40)
+    ap.add_argument("--warmup", type=int, default=8)
+    ap.add_argument("--workload", default="rag8b")
+    ap.add_argument("--layers", type=int, default=8)
+    ap.add_argument("--cpu-requests", type=int, default=2)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the path "
+              "shards by request or KV head with no exchange, see DESIGN.md", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import workloads
+    from paper_2609_32999_amd import staging
+    from paper_2609_32999_amd.session import Session
+
+    wl = workloads.generate(args.workload)
+    m = wl.model
+    L = args.layers
+    log(f"[bench] workload={wl.name} layers={L} prompt_tokens={wl.prompt_tokens}")
+    sess = Session(m, wl.n_pool_pages, wl.n_req_pages, n_layers=L)
+    staging.upload_pool(sess, wl, layer=0)
+    for l in range(1, L):
+        sess.pool_k[l].copy_(sess.pool_k[0])
+        sess.pool_v[l].copy_(sess.pool_v[0])
+    plan = sess.plan(wl.requests)
+    q, k, v = staging.fresh_inputs(sess, wl, plan)
+    qs = [q] + [q.clone() for _ in range(L - 1)]
+    ks = [k] + [k.clone() for _ in range(L - 1)]
+    vs = [v] + [v.clone() for _ in range(L - 1)]
+    out, lse = sess.new_outputs(plan, with_lse=True)
+    pos, _ = plan.compute_positions()
+    T = plan.num_compute_tokens
+    torch.cuda.synchronize()
+    log(f"[bench] plan T={T} gather={plan.num_gather_tokens} retain={plan.num_retain_tokens} "
+        f"items={plan.num_attn_items}")
+
+    main_s = torch.cuda.current_stream()
+    side = torch.cuda.Stream()
+    E = lambda: torch.cuda.Event(enable_timing=True)
+    n_ev = args.steps
+    evs = [[E() for _ in range(4)] for _ in range(n_ev)]
+    evr = [[E(), E()] for _ in range(n_ev)]
+
+    def step(i, rec=None, recr=None):
+        l = i % L
+        if rec:
+            rec[0].record(main_s)
+        side.wait_stream(main_s)
+        with torch.cuda.stream(side):
+            if recr:
+                recr[0].record(side)
+            sess.retain(plan, ks[l], vs[l], layer=l, stream=side)
+            if recr:
+                recr[1].record(side)
+        sess.compose(plan, layer=l, stream=main_s)
+        if rec:
+            rec[1].record(main_s)
+        sess.append(plan, ks[l], vs[l], layer=l, stream=main_s)
+        if rec:
+            rec[2].record(main_s)
+        sess.attn(plan, qs[l], out, lse, layer=l, stream=main_s)
+        if rec:
+            rec[3].record(main_s)
+        main_s.wait_stream(side)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    log(f"[bench] warmup done ({args.warmup} steps)")
+    t_start, t_end = E(), E()
+    w0 = time.perf_counter()
+    t_start.record(main_s)
+    for i in range(args.steps):
+        step(i, evs[i], evr[i])
+    t_end.record(main_s)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+    total_ms = t_start.elapsed_time(t_end)
+    ms = total_ms / args.steps
+    compose_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
+    append_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
+    attn_ms = float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))
+    retain_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evr]))
+    log(f"[bench] timed {args.steps} steps: {ms:.3f} ms/step (wall {wall * 1e3 / args.steps:.3f}); "
+        f"compose {compose_ms * 1e3:.1f} us, append {append_ms * 1e3:.1f} us, "
+        f"attn {attn_ms * 1e3:.1f} us, retain {retain_ms * 1e3:.1f} us")
+
+    w = kv_elem_bytes(m.kv_dtype)
+    row_bytes = 2 * m.n_kv_heads * m.head_dim * w           # K + V of one token
+    gather_bytes = 2 * plan.num_gather_tokens * row_bytes   # read + write
+    append_bytes = 2 * T * row_bytes
+    retain_bytes = 2 * plan.num_retain_tokens * row_bytes
+    visible = int((pos.astype(np.int64) + 1).sum())
+    attn_flops = 4.0 * m.head_dim * m.n_q_heads * visible
+    attn_tflops = attn_flops / (attn_ms * 1e-3) / 1e12
+    compose_gbs = gather_bytes / (compose_ms * 1e-3) / 1e9
+    peak = PEAK_MFMA_TFLOPS[m.act_dtype]
+    value = wl.prompt_tokens / (ms * 1e-3)
+
+    rec = {
+        "metric": "composed-prefill tokens/s per layer",
+        "value": value,
+        "unit": "tokens/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": m.act_dtype, "data": "synthetic",
+        "config": {
+            "workload": f"{wl.name}: {wl.cfg.description}",
+            "requests": len(wl.requests), "prompt_tokens": wl.prompt_tokens,
+            "computed_tokens": T, "gathered_tokens": plan.num_gather_tokens,
+            "retained_tokens": plan.num_retain_tokens, "layer_buffer_sets": L,
+            "seed": wl.seed,
+        },
+        "computed_tokens_per_s": T / (ms * 1e-3),
+        "assembly_hbm_gbps": compose_gbs,
+        "attention_tflops": attn_tflops,
+        "kernel_us": {"compose": compose_ms * 1e3, "append": append_ms * 1e3,
+                      "attention": attn_ms * 1e3, "retain_side_stream": retain_ms * 1e3},
+        "roofline": {"bound": "mfma", "achieved": attn_tflops, "peak": peak,
+                     "unit": "TFLOP/s", "frac": attn_tflops / peak, "traffic": None,
+                     "kernel": "attn_mfma_kernel", "flops_per_launch": attn_flops},
+        "roofline_compose": {"bound": "hbm", "achieved": compose_gbs, "peak": PEAK_HBM_GBS,
+                             "unit": "GB/s", "frac": compose_gbs / PEAK_HBM_GBS,
+                             "bytes_per_launch": gather_bytes},
+        "append_gbps": append_bytes / (append_ms * 1e-3) / 1e9,
+        "retain_gbps": retain_bytes / (retain_ms * 1e-3) / 1e9 if retain_ms > 0 else None,
+    }
+    if not args.no_cpu_baseline:
+        log("[bench] timing the CPU oracle baseline")
+        rec["cpu_baseline"] = cpu_baseline(wl, min(args.cpu_requests, len(wl.requests)))
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

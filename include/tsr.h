@@ -1,0 +1,254 @@
+/*
+ * tsr.h -- C ABI of the composed-prefill hot path (libtsr.so, gfx950).
+ *
+ * The library composes a request's prefill from per-context-unit KV states,
+ * one attention layer at a time (Tessera, Sections 5.1, 5.3 and 5.4):
+ *
+ *   tsr_compose_kv    cached hits: gather unit KV pages from the pool into
+ *                     the request's pages, re-rotating keys cached before
+ *                     RoPE to the unit's new prompt positions;
+ *   tsr_prefill_attn  the final extend pass: rotate the computed tokens'
+ *                     queries and keys at their positions, append their K/V
+ *                     to the request pages, and run causal GQA attention of
+ *                     those tokens over the whole assembled KV;
+ *   tsr_retain_kv     write newly computed units' reusable form (keys before
+ *                     RoPE, values) into their pool pages.
+ *
+ * Conventions
+ *   - Every pointer named dev_* or documented as "device" is a HIP device
+ *     pointer; every other pointer is host memory.  `stream` is a
+ *     hipStream_t passed as void*.  NULL selects the default stream.
+ *   - The caller owns every buffer, including the plan workspace and the
+ *     RoPE table; the library never allocates device memory.  Host memory
+ *     the library allocates lives inside the plan object.
+ *   - Inputs are borrowed until the work enqueued on `stream` completes.
+ *   - No function throws, aborts or exits.  On failure a status other than
+ *     TSR_OK is returned, nothing is enqueued, and tsr_last_error() (a
+ *     thread-local string) says why.
+ *   - Thread safety: plans are immutable after creation and may be used
+ *     from several threads and streams at once.
+ *
+ * KV page layout (pool and request pages alike), one layer:
+ *     [n_pages][n_kv_heads][page_size][head_dim]   (head-major within a page)
+ * Token j of a unit lives in its block j / B at slot j % B (Section 5.1);
+ * prompt position p of a request lives in request page block_table[p / B]
+ * at slot p % B.
+ *
+ * Row order ("plan order") of the computed tokens: requests in the order
+ * given, and within a request the computed tokens by increasing prompt
+ * position.  q/k/v inputs and attention outputs use this row order.
+ */
+#ifndef TSR_H
+#define TSR_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define TSR_ABI_VERSION 1
+
+typedef enum {
+  TSR_OK = 0,
+  TSR_ERR_INVALID_ARG = 1,   /* malformed request, null pointer, bad size */
+  TSR_ERR_UNSUPPORTED = 2,   /* valid but not implemented (dtype, shape)  */
+  TSR_ERR_OUT_OF_RANGE = 3,  /* page id, position or arena bound exceeded */
+  TSR_ERR_DEVICE = 4         /* a HIP call failed (message in last error) */
+} tsr_status;
+
+typedef enum { TSR_F32 = 0, TSR_BF16 = 1, TSR_E4M3 = 2 } tsr_dtype;
+
+/* Preparation of a unit (Section 5.1, per-unit plan): a state used from a
+ * cache tier is a HIT; a state computed from text is a MISS. */
+typedef enum { TSR_MISS = 0, TSR_HIT = 1 } tsr_residency;
+
+/* Shape and numerics of one attention layer.
+ *   (kv_dtype, act_dtype) in {(F32, F32), (BF16, BF16)}.
+ *   RoPE pairs dimension i with i + head_dim/2 at frequency
+ *   rope_theta^(-2i/head_dim) (Section 2.2; the variant is a reading).
+ *   Positions must be < max_position (the RoPE table's length).
+ *   softmax_scale == 0 selects 1/sqrt(head_dim). */
+typedef struct {
+  int32_t n_q_heads;
+  int32_t n_kv_heads;
+  int32_t head_dim;
+  int32_t page_size;
+  int32_t kv_dtype;
+  int32_t act_dtype;
+  double rope_theta;
+  int32_t max_position;
+  float softmax_scale;
+} tsr_model;
+
+/* One occurrence of a context unit in a request (Section 5.1).
+ *   unit_id      stable identity (opaque to the library).
+ *   position     first prompt position of the unit (placement is fixed
+ *                before preparation, Section 5.3).
+ *   n_tokens     unit length n > 0.
+ *   residency    TSR_HIT: its cached state (keys before RoPE, values) is in
+ *                pool_pages; TSR_MISS: it is computed in this pass.
+ *   n_recompute  HIT only: the composition policy recomputes the first
+ *                min(n_recompute, n) tokens (a fixed chunk-initial window,
+ *                Section 7); they become computed rows.
+ *   retain       MISS only: 1 writes the computed state into pool_pages.
+ *   pool_pages   host array of ceil(n / page_size) pool page ids: the source
+ *                of a HIT, the destination of a retained MISS, else unused
+ *                (may be NULL). */
+typedef struct {
+  uint64_t unit_id;
+  int32_t position;
+  int32_t n_tokens;
+  int32_t residency;
+  int32_t n_recompute;
+  int32_t retain;
+  int32_t reserved;
+  const int32_t* pool_pages;
+} tsr_unit;
+
+/* One request: an ordered prompt tiled exactly once by its units and text
+ * segments (instruction, separators, query), and its request KV pages.
+ *   text_segs    host array [n_text][2] of {start, length}, length > 0.
+ *   block_table  host array of ceil(prompt_len / page_size) request page ids,
+ *                not shared with any other request of the batch. */
+typedef struct {
+  int32_t prompt_len;
+  int32_t n_units;
+  const tsr_unit* units;
+  int32_t n_text;
+  int32_t reserved;
+  const int32_t* text_segs;
+  const int32_t* block_table;
+} tsr_request;
+
+typedef struct tsr_plan tsr_plan;
+
+/* ---------------------------------------------------------------- RoPE */
+
+/* Bytes of the RoPE table for `model`: cos and sin planes of
+ * [max_position][head_dim/2] fp32.  0 if the model is invalid. */
+size_t tsr_rope_table_bytes(const tsr_model* model);
+
+/* Fill a caller-owned device buffer with the RoPE table: angles and cos/sin
+ * are evaluated in fp64 on the host and rounded to fp32, then copied with
+ * hipMemcpyAsync on `stream`.  The table is built once per model and may be
+ * shared by every plan of that model. */
+tsr_status tsr_rope_table_init(const tsr_model* model, void* dev_table,
+                               size_t table_bytes, void* stream);
+
+/* ---------------------------------------------------------------- plan */
+
+/* Device workspace bytes tsr_plan_create needs for this batch, or 0 if the
+ * batch fails validation (tsr_last_error says why). */
+size_t tsr_plan_workspace_size(const tsr_model* model, const tsr_request* reqs,
+                               int32_t n_req, int32_t n_pool_pages,
+                               int32_t n_req_pages);
+
+/* Validate a batch and build its plan (Section 5.3, placement before
+ * preparation): the computed rows, the gathered tokens, the retained
+ * tokens and the attention tile schedule.  The device image of the plan is
+ * copied into `dev_workspace` with hipMemcpyAsync on `stream`.
+ *   n_pool_pages / n_req_pages  sizes of the pool / request page arenas.
+ *   dev_rope_table  a table filled by tsr_rope_table_init for this model.
+ *   dev_workspace   NULL builds a host-only plan that can be inspected but
+ *                   not executed (no HIP call is made).
+ * Checks (all on the host, before anything is enqueued): shapes and dtypes;
+ * every request tiled exactly once in order; page ids inside their arena;
+ * request pages not shared between requests; positions < max_position; a
+ * retained unit's pages neither read by a HIT of the batch nor written by
+ * another retained unit. */
+tsr_status tsr_plan_create(const tsr_model* model, const tsr_request* reqs,
+                           int32_t n_req, int32_t n_pool_pages,
+                           int32_t n_req_pages, const void* dev_rope_table,
+                           void* dev_workspace, size_t workspace_bytes,
+                           void* stream, tsr_plan** out_plan);
+
+/* Number of computed rows T (inputs q/k/v and outputs have T rows). */
+int32_t tsr_plan_num_compute_tokens(const tsr_plan* plan);
+/* Number of cached tokens gathered by tsr_compose_kv. */
+int32_t tsr_plan_num_gather_tokens(const tsr_plan* plan);
+/* Number of tokens written by tsr_retain_kv. */
+int32_t tsr_plan_num_retain_tokens(const tsr_plan* plan);
+/* Number of attention work items (row tile x KV head). */
+int32_t tsr_plan_num_attn_items(const tsr_plan* plan);
+
+/* Prompt position and request index of every computed row, in plan order.
+ * host_positions: [T] (required); host_requests: [T] or NULL. */
+tsr_status tsr_plan_compute_positions(const tsr_plan* plan,
+                                      int32_t* host_positions,
+                                      int32_t* host_requests);
+
+void tsr_plan_destroy(tsr_plan* plan);
+
+/* ------------------------------------------------------------ hot path */
+
+/* Compose: for every HIT unit u and token j in [min(r_u, n_u), n_u):
+ *   V_req[pos_u + j] = V_pool[u's block j/B][slot j%B]        (bit copy)
+ *   K_req[pos_u + j] = RoPE(K_pool[...], pos_u + j)  rounded to kv_dtype
+ * (Section 5.3, "Preparing cache hits").  The pool is read only.
+ * Rotation: fp32 table values, fp32 products and one fp32 add each, no
+ * fused multiply-add; bf16 results rounded to nearest even.
+ *   pool_k/pool_v  device, [n_pool_pages][H_kv][B][d] of kv_dtype.
+ *   req_k/req_v    device, [n_req_pages][H_kv][B][d] of kv_dtype.
+ *   pool_scale, req_scale  reserved for scaled 8-bit pools; pass NULL.
+ *   n_layers >= 1 composes that many layers in one launch; layer l uses the
+ *   buffers offset by l * pool_layer_stride / req_layer_stride bytes. */
+tsr_status tsr_compose_kv(const tsr_plan* plan, const void* pool_k,
+                          const void* pool_v, const float* pool_scale,
+                          void* req_k, void* req_v, float* req_scale,
+                          int32_t n_layers, int64_t pool_layer_stride,
+                          int64_t req_layer_stride, void* stream);
+
+/* Final extend pass (Section 5.3, "Completing prefill"):
+ *   1. for every computed row t at position p_t: k_rot = RoPE(k_t, p_t) and
+ *      v_t are written to the request pages at p_t;
+ *   2. o_t,h = softmax(scale * q_rot . K_req[0..p_t, g]^T) V_req[0..p_t, g],
+ *      q_rot = RoPE(q_t,h, p_t) rounded to act_dtype, g = h / (H_q / H_kv),
+ *      causal by absolute position (a key at p_t itself is visible).
+ *   q    device [T][H_q][d], k/v device [T][H_kv][d]: pre-RoPE, act dtype.
+ *   out  device [T][H_q][d] of act_dtype.
+ *   lse  device [T][H_q] fp32 natural-log sum of exp(scale * s), or NULL.
+ * Must run after tsr_compose_kv of the same plan and layer (stream order).
+ * bf16: QK^T in bf16 MFMA with fp32 accumulation; probabilities and values
+ * enter the PV product as fp16 (|v| must stay below 65504). */
+tsr_status tsr_prefill_attn(const tsr_plan* plan, const void* q,
+                            const void* k, const void* v, void* req_k,
+                            void* req_v, float* req_scale, void* out,
+                            float* lse, void* stream);
+
+/* The two halves of tsr_prefill_attn, for callers that schedule them apart
+ * (and for timing the attention kernel alone):
+ *   tsr_append_kv  step 1 only (rotate computed keys, write k_rot and v to
+ *                  the request pages);
+ *   tsr_attn       step 2 only; the request pages must already hold every
+ *                  position's K/V (compose + append, in stream order).
+ * Arguments have the same meaning as in tsr_prefill_attn. */
+tsr_status tsr_append_kv(const tsr_plan* plan, const void* k, const void* v,
+                         void* req_k, void* req_v, float* req_scale,
+                         void* stream);
+tsr_status tsr_attn(const tsr_plan* plan, const void* q, const void* req_k,
+                    const void* req_v, const float* req_scale, void* out,
+                    float* lse, void* stream);
+
+/* Retain (Section 5.4): for every MISS unit with retain = 1 and token j:
+ *   K_pool[block j/B][slot j%B] = k (before RoPE), V_pool[...] = v
+ * as bit copies from the computed rows.  Slots of a unit's last block
+ * beyond n are left untouched.  k/v are the same inputs as
+ * tsr_prefill_attn's and must stay alive until the stream reaches this work
+ * (Section 5.4: sources stay valid until their copies complete).  A caller
+ * may publish the units as HITs only after observing its completion. */
+tsr_status tsr_retain_kv(const tsr_plan* plan, const void* k, const void* v,
+                         void* pool_k, void* pool_v, float* pool_scale,
+                         void* stream);
+
+/* Thread-local message of the last failure on this thread ("" if none). */
+const char* tsr_last_error(void);
+
+int32_t tsr_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TSR_H */

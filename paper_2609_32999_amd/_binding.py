@@ -1,0 +1,277 @@
+"""ctypes binding of libtsr.so (include/tsr.h).  Argument marshalling only.
+
+Functions keep the C names.  Pointer arguments accept an int, None, or any
+object with `data_ptr()` (a torch tensor); stream arguments accept an int,
+None, or an object with `cuda_stream` (a torch stream; on ROCm that handle is
+a hipStream_t).  Non-OK statuses raise TsrError carrying the status and the
+library's message.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from ctypes import POINTER, c_double, c_float, c_int32, c_int64, c_size_t, c_uint64, c_void_p
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libtsr.so")
+
+TSR_OK, TSR_ERR_INVALID_ARG, TSR_ERR_UNSUPPORTED, TSR_ERR_OUT_OF_RANGE, TSR_ERR_DEVICE = range(5)
+STATUS_NAMES = {0: "OK", 1: "INVALID_ARG", 2: "UNSUPPORTED", 3: "OUT_OF_RANGE", 4: "DEVICE"}
+TSR_F32, TSR_BF16, TSR_E4M3 = 0, 1, 2
+DTYPE_CODES = {"f32": TSR_F32, "bf16": TSR_BF16, "e4m3": TSR_E4M3}
+TSR_MISS, TSR_HIT = 0, 1
+
+# Every symbol include/tsr.h declares.
+EXPORTS = (
+    "tsr_abi_version", "tsr_last_error", "tsr_rope_table_bytes",
+    "tsr_rope_table_init", "tsr_plan_workspace_size", "tsr_plan_create",
+    "tsr_plan_num_compute_tokens", "tsr_plan_num_gather_tokens",
+    "tsr_plan_num_retain_tokens", "tsr_plan_num_attn_items",
+    "tsr_plan_compute_positions", "tsr_plan_destroy", "tsr_compose_kv",
+    "tsr_prefill_attn", "tsr_append_kv", "tsr_attn", "tsr_retain_kv",
+)
+
+
+class TsrError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{STATUS_NAMES.get(status, status)}: {message}")
+        self.status = status
+        self.message = message
+
+
+class tsr_model(ctypes.Structure):
+    _fields_ = [("n_q_heads", c_int32), ("n_kv_heads", c_int32),
+                ("head_dim", c_int32), ("page_size", c_int32),
+                ("kv_dtype", c_int32), ("act_dtype", c_int32),
+                ("rope_theta", c_double), ("max_position", c_int32),
+                ("softmax_scale", c_float)]
+
+
+class tsr_unit(ctypes.Structure):
+    _fields_ = [("unit_id", c_uint64), ("position", c_int32),
+                ("n_tokens", c_int32), ("residency", c_int32),
+                ("n_recompute", c_int32), ("retain", c_int32),
+                ("reserved", c_int32), ("pool_pages", POINTER(c_int32))]
+
+
+class tsr_request(ctypes.Structure):
+    _fields_ = [("prompt_len", c_int32), ("n_units", c_int32),
+                ("units", POINTER(tsr_unit)), ("n_text", c_int32),
+                ("reserved", c_int32), ("text_segs", POINTER(c_int32)),
+                ("block_table", POINTER(c_int32))]
+
+
+_lib = None
+
+
+def lib():
+    """Load libtsr.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is missing: build it with "
+                              "`python -m paper_2609_32999_amd.build_lib`")
+        L = ctypes.CDLL(LIB_PATH)
+        P = c_void_p
+        sig = {
+            "tsr_abi_version": (c_int32, []),
+            "tsr_last_error": (ctypes.c_char_p, []),
+            "tsr_rope_table_bytes": (c_size_t, [POINTER(tsr_model)]),
+            "tsr_rope_table_init": (c_int32, [POINTER(tsr_model), P, c_size_t, P]),
+            "tsr_plan_workspace_size": (c_size_t, [POINTER(tsr_model), POINTER(tsr_request),
+                                                   c_int32, c_int32, c_int32]),
+            "tsr_plan_create": (c_int32, [POINTER(tsr_model), POINTER(tsr_request), c_int32,
+                                          c_int32, c_int32, P, P, c_size_t, P,
+                                          POINTER(c_void_p)]),
+            "tsr_plan_num_compute_tokens": (c_int32, [P]),
+            "tsr_plan_num_gather_tokens": (c_int32, [P]),
+            "tsr_plan_num_retain_tokens": (c_int32, [P]),
+            "tsr_plan_num_attn_items": (c_int32, [P]),
+            "tsr_plan_compute_positions": (c_int32, [P, POINTER(c_int32), POINTER(c_int32)]),
+            "tsr_plan_destroy": (None, [P]),
+            "tsr_compose_kv": (c_int32, [P, P, P, P, P, P, P, c_int32, c_int64, c_int64, P]),
+            "tsr_prefill_attn": (c_int32, [P, P, P, P, P, P, P, P, P, P]),
+            "tsr_retain_kv": (c_int32, [P, P, P, P, P, P, P]),
+            "tsr_append_kv": (c_int32, [P, P, P, P, P, P, P]),
+            "tsr_attn": (c_int32, [P, P, P, P, P, P, P, P]),
+        }
+        for name, (res, args) in sig.items():
+            f = getattr(L, name)
+            f.restype = res
+            f.argtypes = args
+        _lib = L
+    return _lib
+
+
+def _ptr(x) -> int | None:
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    return x.data_ptr()
+
+
+def _stream(s) -> int | None:
+    if s is None:
+        return None
+    if isinstance(s, int):
+        return s
+    return s.cuda_stream
+
+
+def _check(status: int) -> None:
+    if status != TSR_OK:
+        raise TsrError(status, tsr_last_error())
+
+
+def tsr_abi_version() -> int:
+    return lib().tsr_abi_version()
+
+
+def tsr_last_error() -> str:
+    return lib().tsr_last_error().decode()
+
+
+def make_model(n_q_heads, n_kv_heads, head_dim, page_size=16, kv_dtype="bf16",
+               act_dtype="bf16", rope_theta=500000.0, max_position=65536,
+               softmax_scale=0.0) -> tsr_model:
+    return tsr_model(n_q_heads, n_kv_heads, head_dim, page_size,
+                     DTYPE_CODES[kv_dtype], DTYPE_CODES[act_dtype],
+                     float(rope_theta), max_position, float(softmax_scale))
+
+
+class RequestBatch:
+    """ctypes arrays for a batch of requests.
+
+    Each request needs `prompt_len`, `units` (objects with unit_id, position,
+    n_tokens, residency, n_recompute, retain, pool_pages), `text_segs`
+    ([(start, length)]) and `block_table`.  The arrays stay alive as long as
+    this object.
+    """
+
+    def __init__(self, requests):
+        self._keep = []
+        arr = (tsr_request * max(1, len(requests)))()
+        for i, r in enumerate(requests):
+            units = (tsr_unit * max(1, len(r.units)))()
+            for j, u in enumerate(r.units):
+                pages = None
+                if u.pool_pages is not None:
+                    pages = np.ascontiguousarray(u.pool_pages, dtype=np.int32)
+                    self._keep.append(pages)
+                units[j] = tsr_unit(
+                    int(u.unit_id), int(u.position), int(u.n_tokens),
+                    int(u.residency), int(u.n_recompute), int(u.retain), 0,
+                    pages.ctypes.data_as(POINTER(c_int32)) if pages is not None else None)
+            segs = np.ascontiguousarray(np.asarray(r.text_segs, dtype=np.int32).reshape(-1, 2))
+            bt = np.ascontiguousarray(r.block_table, dtype=np.int32)
+            self._keep += [units, segs, bt]
+            arr[i] = tsr_request(int(r.prompt_len), len(r.units), units, len(segs), 0,
+                                 segs.ctypes.data_as(POINTER(c_int32)),
+                                 bt.ctypes.data_as(POINTER(c_int32)))
+        self.array = arr
+        self.n = len(requests)
+
+
+def tsr_rope_table_bytes(model: tsr_model) -> int:
+    return lib().tsr_rope_table_bytes(ctypes.byref(model))
+
+
+def tsr_rope_table_init(model: tsr_model, dev_table, table_bytes: int, stream=None) -> None:
+    _check(lib().tsr_rope_table_init(ctypes.byref(model), _ptr(dev_table),
+                                     table_bytes, _stream(stream)))
+
+
+def tsr_plan_workspace_size(model: tsr_model, batch: RequestBatch, n_pool_pages: int,
+                            n_req_pages: int) -> int:
+    n = lib().tsr_plan_workspace_size(ctypes.byref(model), batch.array, batch.n,
+                                      n_pool_pages, n_req_pages)
+    if n == 0:
+        raise TsrError(TSR_ERR_INVALID_ARG, tsr_last_error())
+    return n
+
+
+class Plan:
+    """Owner of a tsr_plan handle."""
+
+    def __init__(self, handle: int, model: tsr_model):
+        self.handle = handle
+        self.model = model
+
+    @property
+    def num_compute_tokens(self) -> int:
+        return lib().tsr_plan_num_compute_tokens(self.handle)
+
+    @property
+    def num_gather_tokens(self) -> int:
+        return lib().tsr_plan_num_gather_tokens(self.handle)
+
+    @property
+    def num_retain_tokens(self) -> int:
+        return lib().tsr_plan_num_retain_tokens(self.handle)
+
+    @property
+    def num_attn_items(self) -> int:
+        return lib().tsr_plan_num_attn_items(self.handle)
+
+    def compute_positions(self):
+        T = self.num_compute_tokens
+        pos = np.empty(max(T, 1), dtype=np.int32)
+        req = np.empty(max(T, 1), dtype=np.int32)
+        _check(lib().tsr_plan_compute_positions(
+            self.handle, pos.ctypes.data_as(POINTER(c_int32)),
+            req.ctypes.data_as(POINTER(c_int32))))
+        return pos[:T], req[:T]
+
+    def destroy(self) -> None:
+        if self.handle:
+            lib().tsr_plan_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.destroy()
+        except Exception:
+            pass
+
+
+def tsr_plan_create(model: tsr_model, batch: RequestBatch, n_pool_pages: int,
+                    n_req_pages: int, dev_rope_table=None, dev_workspace=None,
+                    workspace_bytes: int = 0, stream=None) -> Plan:
+    out = c_void_p()
+    _check(lib().tsr_plan_create(ctypes.byref(model), batch.array, batch.n, n_pool_pages,
+                                 n_req_pages, _ptr(dev_rope_table), _ptr(dev_workspace),
+                                 workspace_bytes, _stream(stream), ctypes.byref(out)))
+    return Plan(out.value, model)
+
+
+def tsr_compose_kv(plan: Plan, pool_k, pool_v, pool_scale, req_k, req_v, req_scale,
+                   n_layers: int = 1, pool_layer_stride: int = 0,
+                   req_layer_stride: int = 0, stream=None) -> None:
+    _check(lib().tsr_compose_kv(plan.handle, _ptr(pool_k), _ptr(pool_v), _ptr(pool_scale),
+                                _ptr(req_k), _ptr(req_v), _ptr(req_scale), n_layers,
+                                pool_layer_stride, req_layer_stride, _stream(stream)))
+
+
+def tsr_prefill_attn(plan: Plan, q, k, v, req_k, req_v, req_scale, out, lse=None,
+                     stream=None) -> None:
+    _check(lib().tsr_prefill_attn(plan.handle, _ptr(q), _ptr(k), _ptr(v), _ptr(req_k),
+                                  _ptr(req_v), _ptr(req_scale), _ptr(out), _ptr(lse),
+                                  _stream(stream)))
+
+
+def tsr_retain_kv(plan: Plan, k, v, pool_k, pool_v, pool_scale, stream=None) -> None:
+    _check(lib().tsr_retain_kv(plan.handle, _ptr(k), _ptr(v), _ptr(pool_k), _ptr(pool_v),
+                               _ptr(pool_scale), _stream(stream)))
+
+
+def tsr_append_kv(plan: Plan, k, v, req_k, req_v, req_scale=None, stream=None) -> None:
+    _check(lib().tsr_append_kv(plan.handle, _ptr(k), _ptr(v), _ptr(req_k), _ptr(req_v),
+                               _ptr(req_scale), _stream(stream)))
+
+
+def tsr_attn(plan: Plan, q, req_k, req_v, req_scale, out, lse=None, stream=None) -> None:
+    _check(lib().tsr_attn(plan.handle, _ptr(q), _ptr(req_k), _ptr(req_v), _ptr(req_scale),
+                          _ptr(out), _ptr(lse), _stream(stream)))

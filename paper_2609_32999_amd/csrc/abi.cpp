@@ -1,0 +1,307 @@
+// Exported C entry points of libtsr.  Every function validates on the host
+// before enqueueing anything, converts failures into a status plus a
+// thread-local message, and lets no exception cross the ABI.
+#include <cmath>
+#include <cstring>
+#include <exception>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "tsr_internal.h"
+
+namespace tsr {
+
+namespace {
+thread_local std::string g_error;
+
+tsr_status device_fail(const char* what, hipError_t e) {
+  set_error(std::string(what) + ": " + hipGetErrorName(e) + " (" +
+            hipGetErrorString(e) + ")");
+  return TSR_ERR_DEVICE;
+}
+
+tsr_status check_exec(const tsr_plan* p) {
+  if (!p) {
+    set_error("plan is NULL");
+    return TSR_ERR_INVALID_ARG;
+  }
+  if (!p->ws) {
+    set_error("plan was created without a device workspace (host-only plan)");
+    return TSR_ERR_INVALID_ARG;
+  }
+  return TSR_OK;
+}
+
+tsr_status check_scales(const tsr_plan* p, const float* a, const float* b) {
+  if (p->model.kv_dtype != TSR_E4M3 && (a || b)) {
+    set_error("scale arrays apply to e4m3 pools only; pass NULL");
+    return TSR_ERR_INVALID_ARG;
+  }
+  return TSR_OK;
+}
+
+template <typename F>
+tsr_status guarded(F&& f) {
+  try {
+    return f();
+  } catch (const std::bad_alloc&) {
+    set_error("host allocation failed");
+    return TSR_ERR_INVALID_ARG;
+  } catch (const std::exception& e) {
+    set_error(std::string("internal error: ") + e.what());
+    return TSR_ERR_INVALID_ARG;
+  } catch (...) {
+    set_error("internal error");
+    return TSR_ERR_INVALID_ARG;
+  }
+}
+}  // namespace
+
+void set_error(const std::string& msg) { g_error = msg; }
+
+}  // namespace tsr
+
+using namespace tsr;
+
+extern "C" {
+
+int32_t tsr_abi_version(void) { return TSR_ABI_VERSION; }
+
+const char* tsr_last_error(void) { return g_error.c_str(); }
+
+size_t tsr_rope_table_bytes(const tsr_model* model) {
+  if (check_model(model) != TSR_OK) return 0;
+  return 2 * (size_t)model->max_position * (size_t)(model->head_dim / 2) * sizeof(float);
+}
+
+tsr_status tsr_rope_table_init(const tsr_model* model, void* dev_table,
+                               size_t table_bytes, void* stream) {
+  return guarded([&]() -> tsr_status {
+    tsr_status st = check_model(model);
+    if (st != TSR_OK) return st;
+    const size_t need = tsr_rope_table_bytes(model);
+    if (!dev_table || table_bytes < need) {
+      set_error("RoPE table buffer is NULL or smaller than tsr_rope_table_bytes()");
+      return TSR_ERR_INVALID_ARG;
+    }
+    const int half = model->head_dim / 2;
+    const size_t n = (size_t)model->max_position * half;
+    std::vector<double> inv(half);
+    for (int i = 0; i < half; ++i)
+      inv[i] = std::pow(model->rope_theta, -2.0 * i / model->head_dim);
+    std::vector<float> host(2 * n);
+    for (int p = 0; p < model->max_position; ++p)
+      for (int i = 0; i < half; ++i) {
+        const double a = (double)p * inv[i];
+        host[(size_t)p * half + i] = (float)std::cos(a);
+        host[n + (size_t)p * half + i] = (float)std::sin(a);
+      }
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    hipError_t e = hipMemcpyAsync(dev_table, host.data(), 2 * n * sizeof(float),
+                                  hipMemcpyHostToDevice, s);
+    if (e != hipSuccess) return device_fail("hipMemcpyAsync(rope table)", e);
+    e = hipStreamSynchronize(s);  // the host image dies with this call
+    if (e != hipSuccess) return device_fail("hipStreamSynchronize(rope table)", e);
+    return TSR_OK;
+  });
+}
+
+size_t tsr_plan_workspace_size(const tsr_model* model, const tsr_request* reqs,
+                               int32_t n_req, int32_t n_pool_pages,
+                               int32_t n_req_pages) {
+  size_t bytes = 0;
+  guarded([&]() -> tsr_status {
+    tsr_plan tmp{};
+    tsr_status st = build_plan(model, reqs, n_req, n_pool_pages, n_req_pages, &tmp);
+    if (st == TSR_OK) bytes = tmp.ws_bytes;
+    return st;
+  });
+  return bytes;
+}
+
+tsr_status tsr_plan_create(const tsr_model* model, const tsr_request* reqs,
+                           int32_t n_req, int32_t n_pool_pages,
+                           int32_t n_req_pages, const void* dev_rope_table,
+                           void* dev_workspace, size_t workspace_bytes,
+                           void* stream, tsr_plan** out_plan) {
+  return guarded([&]() -> tsr_status {
+    if (!out_plan) {
+      set_error("out_plan is NULL");
+      return TSR_ERR_INVALID_ARG;
+    }
+    *out_plan = nullptr;
+    tsr_plan* p = new tsr_plan();
+    tsr_status st = build_plan(model, reqs, n_req, n_pool_pages, n_req_pages, p);
+    if (st != TSR_OK) {
+      delete p;
+      return st;
+    }
+    if (dev_workspace) {
+      if (workspace_bytes < p->ws_bytes) {
+        set_error("workspace smaller than tsr_plan_workspace_size() = " +
+                  std::to_string(p->ws_bytes));
+        delete p;
+        return TSR_ERR_INVALID_ARG;
+      }
+      if (!dev_rope_table) {
+        set_error("dev_rope_table is NULL");
+        delete p;
+        return TSR_ERR_INVALID_ARG;
+      }
+      hipError_t e = hipMemcpyAsync(dev_workspace, p->image.data(), p->ws_bytes,
+                                    hipMemcpyHostToDevice,
+                                    static_cast<hipStream_t>(stream));
+      if (e != hipSuccess) {
+        delete p;
+        return device_fail("hipMemcpyAsync(plan)", e);
+      }
+      char* base = static_cast<char*>(dev_workspace);
+      const size_t half = (size_t)p->model.max_position * (p->model.head_dim / 2);
+      const float* table = static_cast<const float*>(dev_rope_table);
+      p->dev.gather = reinterpret_cast<const GatherDesc*>(base + p->off_gather);
+      p->dev.rows = reinterpret_cast<const RowDesc*>(base + p->off_rows);
+      p->dev.retain = reinterpret_cast<const RetainDesc*>(base + p->off_retain);
+      p->dev.items = reinterpret_cast<const AttnItem*>(base + p->off_items);
+      p->dev.block_tables = reinterpret_cast<const int32_t*>(base + p->off_bt);
+      p->dev.rope_cos = table;
+      p->dev.rope_sin = table + half;
+    }
+    p->rope_table = dev_rope_table;
+    p->ws = dev_workspace;
+    *out_plan = p;
+    return TSR_OK;
+  });
+}
+
+int32_t tsr_plan_num_compute_tokens(const tsr_plan* p) { return p ? p->T : -1; }
+int32_t tsr_plan_num_gather_tokens(const tsr_plan* p) { return p ? p->n_gather : -1; }
+int32_t tsr_plan_num_retain_tokens(const tsr_plan* p) { return p ? p->n_retain : -1; }
+int32_t tsr_plan_num_attn_items(const tsr_plan* p) { return p ? p->n_items : -1; }
+
+tsr_status tsr_plan_compute_positions(const tsr_plan* p, int32_t* host_positions,
+                                      int32_t* host_requests) {
+  if (!p || !host_positions) {
+    set_error("plan or host_positions is NULL");
+    return TSR_ERR_INVALID_ARG;
+  }
+  if (p->T) std::memcpy(host_positions, p->row_pos.data(), p->T * sizeof(int32_t));
+  if (host_requests && p->T)
+    std::memcpy(host_requests, p->row_req.data(), p->T * sizeof(int32_t));
+  return TSR_OK;
+}
+
+void tsr_plan_destroy(tsr_plan* p) { delete p; }
+
+tsr_status tsr_compose_kv(const tsr_plan* p, const void* pool_k,
+                          const void* pool_v, const float* pool_scale,
+                          void* req_k, void* req_v, float* req_scale,
+                          int32_t n_layers, int64_t pool_layer_stride,
+                          int64_t req_layer_stride, void* stream) {
+  return guarded([&]() -> tsr_status {
+    tsr_status st = check_exec(p);
+    if (st != TSR_OK) return st;
+    if ((st = check_scales(p, pool_scale, req_scale)) != TSR_OK) return st;
+    if (n_layers < 1 || n_layers > 65535) {
+      set_error("n_layers must be in [1, 65535]");
+      return TSR_ERR_INVALID_ARG;
+    }
+    if (n_layers > 1 && (pool_layer_stride <= 0 || req_layer_stride <= 0)) {
+      set_error("layer strides must be positive when n_layers > 1");
+      return TSR_ERR_INVALID_ARG;
+    }
+    const int64_t elem = p->model.kv_dtype == TSR_F32 ? 4 : 2;
+    if (pool_layer_stride % (16 * elem) || req_layer_stride % (16 * elem)) {
+      set_error("layer strides must be multiples of 16 elements");
+      return TSR_ERR_INVALID_ARG;
+    }
+    if (p->n_gather == 0) return TSR_OK;
+    if (!pool_k || !pool_v || !req_k || !req_v) {
+      set_error("compose: a KV pointer is NULL");
+      return TSR_ERR_INVALID_ARG;
+    }
+    hipError_t e = launch_compose(p, pool_k, pool_v, req_k, req_v, n_layers,
+                                  pool_layer_stride, req_layer_stride,
+                                  static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return device_fail("compose launch", e);
+    return TSR_OK;
+  });
+}
+
+tsr_status tsr_prefill_attn(const tsr_plan* p, const void* q, const void* k,
+                            const void* v, void* req_k, void* req_v,
+                            float* req_scale, void* out, float* lse,
+                            void* stream) {
+  return guarded([&]() -> tsr_status {
+    tsr_status st = check_exec(p);
+    if (st != TSR_OK) return st;
+    if ((st = check_scales(p, nullptr, req_scale)) != TSR_OK) return st;
+    if (p->T == 0) return TSR_OK;
+    if (!q || !k || !v || !req_k || !req_v || !out) {
+      set_error("prefill_attn: a required pointer is NULL");
+      return TSR_ERR_INVALID_ARG;
+    }
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    hipError_t e = launch_append(p, k, v, req_k, req_v, s);
+    if (e != hipSuccess) return device_fail("append launch", e);
+    e = launch_attn(p, q, req_k, req_v, out, lse, s);
+    if (e != hipSuccess) return device_fail("attention launch", e);
+    return TSR_OK;
+  });
+}
+
+tsr_status tsr_append_kv(const tsr_plan* p, const void* k, const void* v,
+                         void* req_k, void* req_v, float* req_scale,
+                         void* stream) {
+  return guarded([&]() -> tsr_status {
+    tsr_status st = check_exec(p);
+    if (st != TSR_OK) return st;
+    if ((st = check_scales(p, nullptr, req_scale)) != TSR_OK) return st;
+    if (p->T == 0) return TSR_OK;
+    if (!k || !v || !req_k || !req_v) {
+      set_error("append_kv: a required pointer is NULL");
+      return TSR_ERR_INVALID_ARG;
+    }
+    hipError_t e = launch_append(p, k, v, req_k, req_v, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return device_fail("append launch", e);
+    return TSR_OK;
+  });
+}
+
+tsr_status tsr_attn(const tsr_plan* p, const void* q, const void* req_k,
+                    const void* req_v, const float* req_scale, void* out,
+                    float* lse, void* stream) {
+  return guarded([&]() -> tsr_status {
+    tsr_status st = check_exec(p);
+    if (st != TSR_OK) return st;
+    if ((st = check_scales(p, nullptr, req_scale)) != TSR_OK) return st;
+    if (p->T == 0) return TSR_OK;
+    if (!q || !req_k || !req_v || !out) {
+      set_error("attn: a required pointer is NULL");
+      return TSR_ERR_INVALID_ARG;
+    }
+    hipError_t e = launch_attn(p, q, req_k, req_v, out, lse, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return device_fail("attention launch", e);
+    return TSR_OK;
+  });
+}
+
+tsr_status tsr_retain_kv(const tsr_plan* p, const void* k, const void* v,
+                         void* pool_k, void* pool_v, float* pool_scale,
+                         void* stream) {
+  return guarded([&]() -> tsr_status {
+    tsr_status st = check_exec(p);
+    if (st != TSR_OK) return st;
+    if ((st = check_scales(p, nullptr, pool_scale)) != TSR_OK) return st;
+    if (p->n_retain == 0) return TSR_OK;
+    if (!k || !v || !pool_k || !pool_v) {
+      set_error("retain: a required pointer is NULL");
+      return TSR_ERR_INVALID_ARG;
+    }
+    hipError_t e = launch_retain(p, k, v, pool_k, pool_v, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return device_fail("retain launch", e);
+    return TSR_OK;
+  });
+}
+
+}  // extern "C"

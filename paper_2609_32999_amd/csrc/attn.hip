@@ -1,0 +1,439 @@
+// Causal GQA prefill attention of the computed rows over the assembled KV
+// (Section 5.3, "Completing prefill": the recompute ranges and the remaining
+// prompt are processed in one extend pass).
+//
+// Row t at prompt position p_t, query head h, KV head g = h / G:
+//   o = softmax(scale * q_rot . K[0..p_t, g]^T) V[0..p_t, g]
+// with q_rot = RoPE(q, p_t) rounded to the activation dtype and keys visible
+// up to and including p_t.
+//
+// Two kernels:
+//   attn_f32_kernel   fp32 reference mode, scalar, one workgroup per item.
+//   attn_mfma_kernel  bf16 mode.  Work item = up to 32 consecutive computed
+//                     rows of one request x one KV head; the G query heads of
+//                     that KV head are packed into the workgroup (wave w owns
+//                     heads w, w+4, ...), so every K/V tile staged in LDS feeds
+//                     all of them.  Per 64-key tile:
+//                       S^T = K Q^T        v_mfma_f32_32x32x16_bf16
+//                       online softmax     fp32, exp2 with folded scale
+//                       O^T += V^T P^T     v_mfma_f32_32x32x16_f16
+//                     Keeping S and O transposed gives every lane one query
+//                     row, so row statistics are lane-local except for one
+//                     exchange between the two half-waves.  P and V enter the
+//                     second product as fp16 (bf16 P would cost ~2e-3
+//                     relative error; fp16 keeps it near 2e-4).
+#include <cmath>
+
+#include "kernels_common.h"
+#include "tsr_internal.h"
+
+namespace tsr {
+
+namespace {
+
+// ------------------------------------------------------------- fp32 mode
+template <int D>
+__global__ __launch_bounds__(256) void attn_f32_kernel(
+    const float* __restrict__ q, const float* __restrict__ kc,
+    const float* __restrict__ vc, const AttnItem* __restrict__ items,
+    const int32_t* __restrict__ bts, const RowDesc* __restrict__ rows,
+    const float* __restrict__ rope_cos, const float* __restrict__ rope_sin,
+    float* __restrict__ out, float* __restrict__ lse, int n_q_heads,
+    int n_kv_heads, int log2_page, float scale) {
+  __shared__ float qs[D];
+  __shared__ float ps[256];
+  __shared__ float red[8];
+  const AttnItem it = items[blockIdx.x];
+  if (it.n_rows == 0) return;
+  const int t = threadIdx.x;
+  const int G = n_q_heads / n_kv_heads;
+  const int g = it.kv_head;
+  const int page_mask = (1 << log2_page) - 1;
+  const int32_t* bt = bts + it.bt_off;
+
+  auto block_max = [&](float v) {
+    for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+    if ((t & 63) == 0) red[t >> 6] = v;
+    __syncthreads();
+    v = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+    __syncthreads();
+    return v;
+  };
+  auto block_sum = [&](float v) {
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+    if ((t & 63) == 0) red[4 + (t >> 6)] = v;
+    __syncthreads();
+    v = (red[4] + red[5]) + (red[6] + red[7]);
+    __syncthreads();
+    return v;
+  };
+  auto key_row = [&](const float* base, int k) {
+    const int page = bt[k >> log2_page];
+    return base + ((((int64_t)page * n_kv_heads + g) << log2_page) + (k & page_mask)) * D;
+  };
+
+  for (int rr = 0; rr < it.n_rows; ++rr) {
+    const int row = it.row0 + rr;
+    const int pos = rows[row].pos;
+    for (int hh = 0; hh < G; ++hh) {
+      const int hq = g * G + hh;
+      const float* qp = q + ((int64_t)row * n_q_heads + hq) * D;
+      if (t < D / 2) {
+        float lo = qp[t], hi = qp[t + D / 2];
+        const float c = rope_cos[(int64_t)pos * (D / 2) + t];
+        const float s = rope_sin[(int64_t)pos * (D / 2) + t];
+        rope_rotate<1>(&lo, &hi, &c, &s);
+        qs[t] = lo;
+        qs[t + D / 2] = hi;
+      }
+      __syncthreads();
+      float m = -INFINITY, l = 0.0f, o = 0.0f;
+      for (int k0 = 0; k0 <= pos; k0 += 256) {
+        const int k = k0 + t;
+        float s = -INFINITY;
+        if (k <= pos) {
+          const float* kp = key_row(kc, k);
+          float acc = 0.0f;
+          for (int e = 0; e < D; ++e) acc += qs[e] * kp[e];
+          s = acc * scale;
+        }
+        const float mn = fmaxf(m, block_max(s));
+        const float p = (k <= pos) ? expf(s - mn) : 0.0f;
+        ps[t] = p;
+        const float alpha = expf(m - mn);
+        l = l * alpha + block_sum(p);
+        if (t < D) {
+          const int nk = min(256, pos + 1 - k0);
+          float acc = 0.0f;
+          for (int j = 0; j < nk; ++j) acc += ps[j] * key_row(vc, k0 + j)[t];
+          o = o * alpha + acc;
+        }
+        m = mn;
+        __syncthreads();
+      }
+      if (t < D) out[((int64_t)row * n_q_heads + hq) * D + t] = o / l;
+      if (t == 0 && lse) lse[(int64_t)row * n_q_heads + hq] = m + logf(l);
+      __syncthreads();
+    }
+  }
+}
+
+// ------------------------------------------------------------- bf16 mode
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+union Frag {
+  uint4 u;
+  uint32_t w[4];
+  bf16x8 b;
+  f16x8 h;
+};
+
+constexpr int kD = 128;
+constexpr int kKT = kKvTile;           // keys per tile
+constexpr int kKStr = kD + 8;          // bf16 elements per K row in LDS
+constexpr int kVStr = kKT + 4;         // fp16 elements per V^T row in LDS
+constexpr int kKElems = kKT * kKStr;
+constexpr int kVElems = kD * kVStr;
+constexpr int kStage = kKElems + kVElems;
+
+__device__ __forceinline__ uint32_t pack_f16x2(float a, float b) {
+  // bf16 values convert to fp16 exactly inside fp16's normal range
+  const auto h = __builtin_amdgcn_cvt_pkrtz(a, b);
+  return __builtin_bit_cast(uint32_t, h);
+}
+
+template <int G>
+__global__ __launch_bounds__(256, (G > 4 ? 1 : 2)) void attn_mfma_kernel(
+    const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc,
+    const uint16_t* __restrict__ vc, const AttnItem* __restrict__ items,
+    const int32_t* __restrict__ bts, const RowDesc* __restrict__ rows,
+    const float* __restrict__ rope_cos, const float* __restrict__ rope_sin,
+    uint16_t* __restrict__ out, float* __restrict__ lse, int n_q_heads,
+    int n_kv_heads, int log2_page, float scale, float scale_log2e) {
+  constexpr int HPW = (G + 3) / 4;  // query heads per wave
+  __shared__ __attribute__((aligned(16))) uint16_t smem[2 * kStage];
+
+  const AttnItem it = items[blockIdx.x];
+  if (it.n_rows == 0) return;
+  const int tid = threadIdx.x;
+  const int w = tid >> 6;
+  const int lane = tid & 63;
+  const int lrow = lane & 31;
+  const int lh = lane >> 5;
+  const int g = it.kv_head;
+  const int page_mask = (1 << log2_page) - 1;
+  const int32_t* bt = bts + it.bt_off;
+
+  const int row = it.row0 + min(lrow, it.n_rows - 1);
+  const int pos = rows[row].pos;
+
+  // ---- rotated queries as bf16 B operands: lane = query row, k = head dim
+  bf16x8 qf[HPW][8];
+#pragma unroll
+  for (int i = 0; i < HPW; ++i) {
+    const int hl = min(w + 4 * i, G - 1);
+    const uint16_t* qp = q + ((int64_t)row * n_q_heads + g * G + hl) * kD;
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      const int d0 = 16 * ks + 8 * lh;
+      float lo[8], hi[8], c[8], s[8];
+      load8(qp + d0, lo);
+      load8(qp + d0 + kD / 2, hi);
+      load8(rope_cos + (int64_t)pos * (kD / 2) + d0, c);
+      load8(rope_sin + (int64_t)pos * (kD / 2) + d0, s);
+      rope_rotate<8>(lo, hi, c, s);
+      Frag a, b;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        a.w[e] = f32_to_bf16(lo[2 * e]) | (f32_to_bf16(lo[2 * e + 1]) << 16);
+        b.w[e] = f32_to_bf16(hi[2 * e]) | (f32_to_bf16(hi[2 * e + 1]) << 16);
+      }
+      qf[i][ks] = a.b;
+      qf[i][ks + 4] = b.b;
+    }
+  }
+
+  f32x16 o[HPW][4];
+  float m[HPW], l[HPW];
+#pragma unroll
+  for (int i = 0; i < HPW; ++i) {
+    m[i] = -INFINITY;
+    l[i] = 0.0f;
+#pragma unroll
+    for (int db = 0; db < 4; ++db)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) o[i][db][r] = 0.0f;
+  }
+  bool wave_active[HPW];
+#pragma unroll
+  for (int i = 0; i < HPW; ++i) wave_active[i] = (w + 4 * i) < G;
+
+  // ---- global -> register staging of one K/V tile
+  // K: thread owns 16 bytes (8 dims) of keys 16*pb + tid/16, pb = 0..3.
+  // V: thread owns 16 bytes of keys 4*(tid/16) + pb, so it can write four
+  //    consecutive keys of each of its 8 dims to the transposed V tile.
+  uint4 kr[4], vr[4];
+  const int kc8 = (tid & 15) * 8;
+  auto load_tile = [&](int j) {
+#pragma unroll
+    for (int pb = 0; pb < 4; ++pb) {
+      const int kk = j * kKT + 16 * pb + (tid >> 4);
+      uint4 x = make_uint4(0, 0, 0, 0);
+      if (kk < it.kv_len) {
+        const int64_t a = ((((int64_t)bt[kk >> log2_page] * n_kv_heads + g) << log2_page) +
+                           (kk & page_mask)) * kD + kc8;
+        x = *reinterpret_cast<const uint4*>(kc + a);
+      }
+      kr[pb] = x;
+      const int kv = j * kKT + 4 * (tid >> 4) + pb;
+      uint4 y = make_uint4(0, 0, 0, 0);
+      if (kv < it.kv_len) {
+        const int64_t a = ((((int64_t)bt[kv >> log2_page] * n_kv_heads + g) << log2_page) +
+                           (kv & page_mask)) * kD + kc8;
+        y = *reinterpret_cast<const uint4*>(vc + a);
+      }
+      vr[pb] = y;
+    }
+  };
+  auto store_tile = [&](int buf) {
+    uint16_t* ks = smem + buf * kStage;
+    uint16_t* vs = ks + kKElems;
+#pragma unroll
+    for (int pb = 0; pb < 4; ++pb)
+      *reinterpret_cast<uint4*>(ks + (16 * pb + (tid >> 4)) * kKStr + kc8) = kr[pb];
+    const uint32_t* v0 = reinterpret_cast<const uint32_t*>(&vr[0]);
+    const uint32_t* v1 = reinterpret_cast<const uint32_t*>(&vr[1]);
+    const uint32_t* v2 = reinterpret_cast<const uint32_t*>(&vr[2]);
+    const uint32_t* v3 = reinterpret_cast<const uint32_t*>(&vr[3]);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int sh = (e & 1) ? 16 : 0;
+      const float f0 = bf16_to_f32((v0[e >> 1] >> sh) & 0xffffu);
+      const float f1 = bf16_to_f32((v1[e >> 1] >> sh) & 0xffffu);
+      const float f2 = bf16_to_f32((v2[e >> 1] >> sh) & 0xffffu);
+      const float f3 = bf16_to_f32((v3[e >> 1] >> sh) & 0xffffu);
+      *reinterpret_cast<uint2*>(vs + (kc8 + e) * kVStr + 4 * (tid >> 4)) =
+          make_uint2(pack_f16x2(f0, f1), pack_f16x2(f2, f3));
+    }
+  };
+
+  const int ntiles = (it.kv_len + kKT - 1) / kKT;
+  load_tile(0);
+  store_tile(0);
+  __syncthreads();
+
+  for (int j = 0; j < ntiles; ++j) {
+    const bool more = j + 1 < ntiles;
+    if (more) load_tile(j + 1);
+    const uint16_t* ks = smem + (j & 1) * kStage;
+    const uint16_t* vs = ks + kKElems;
+
+    // S^T[key][row] for two 32-key blocks
+    f32x16 s[HPW][2];
+#pragma unroll
+    for (int i = 0; i < HPW; ++i)
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) s[i][kb][r] = 0.0f;
+#pragma unroll
+    for (int kst = 0; kst < 8; ++kst) {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+        Frag a;
+        a.u = *reinterpret_cast<const uint4*>(ks + (32 * kb + lrow) * kKStr + 16 * kst + 8 * lh);
+#pragma unroll
+        for (int i = 0; i < HPW; ++i)
+          if (wave_active[i])
+            s[i][kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a.b, qf[i][kst], s[i][kb], 0, 0, 0);
+      }
+    }
+
+    // causal mask (only tiles reaching past the tile's first row position)
+    const int kbase = j * kKT;
+    if (kbase + kKT - 1 > it.min_pos) {
+#pragma unroll
+      for (int i = 0; i < HPW; ++i)
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int key = kbase + 32 * kb + 8 * (r >> 2) + 4 * lh + (r & 3);
+            if (key > pos) s[i][kb][r] = -INFINITY;
+          }
+    }
+
+    // online softmax; P^T fragments for the PV product
+    f16x8 pf[HPW][4];
+#pragma unroll
+    for (int i = 0; i < HPW; ++i) {
+      float mt = -INFINITY;
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) mt = fmaxf(mt, s[i][kb][r]);
+      mt = fmaxf(mt, __shfl_xor(mt, 32));
+      const float mn = fmaxf(m[i], mt);
+      const float alpha = __builtin_amdgcn_exp2f((m[i] - mn) * scale_log2e);
+      const float mc = mn * scale_log2e;
+      float ls = 0.0f;
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const float p = __builtin_amdgcn_exp2f(fmaf(s[i][kb][r], scale_log2e, -mc));
+          s[i][kb][r] = p;
+          ls += p;
+        }
+      l[i] = l[i] * alpha + ls;
+      m[i] = mn;
+#pragma unroll
+      for (int db = 0; db < 4; ++db)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) o[i][db][r] *= alpha;
+#pragma unroll
+      for (int k2 = 0; k2 < 4; ++k2) {
+        const int kb = k2 >> 1, base = 8 * (k2 & 1);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) pf[i][k2][e] = (_Float16)s[i][kb][base + e];
+      }
+    }
+
+    // O^T[d][row] += V^T[d][keys] P^T[keys][row]
+#pragma unroll
+    for (int k2 = 0; k2 < 4; ++k2) {
+#pragma unroll
+      for (int db = 0; db < 4; ++db) {
+        const uint16_t* vp = vs + (32 * db + lrow) * kVStr + 16 * k2 + 4 * lh;
+        Frag a;
+        const uint2 lo = *reinterpret_cast<const uint2*>(vp);
+        const uint2 hi = *reinterpret_cast<const uint2*>(vp + 8);
+        a.w[0] = lo.x; a.w[1] = lo.y; a.w[2] = hi.x; a.w[3] = hi.y;
+#pragma unroll
+        for (int i = 0; i < HPW; ++i)
+          if (wave_active[i])
+            o[i][db] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a.h, pf[i][k2], o[i][db], 0, 0, 0);
+      }
+    }
+
+    if (more) store_tile((j + 1) & 1);
+    __syncthreads();
+  }
+
+  // ---- epilogue: normalise, round to bf16, store rows of this tile
+#pragma unroll
+  for (int i = 0; i < HPW; ++i) {
+    if (!wave_active[i]) continue;
+    const float lt = l[i] + __shfl_xor(l[i], 32);
+    if (lrow >= it.n_rows) continue;
+    const float inv = 1.0f / lt;
+    const int hq = g * G + w + 4 * i;
+    uint16_t* op = out + ((int64_t)row * n_q_heads + hq) * kD;
+#pragma unroll
+    for (int db = 0; db < 4; ++db)
+#pragma unroll
+      for (int rg = 0; rg < 4; ++rg) {
+        const int d0 = 32 * db + 8 * rg + 4 * lh;
+        uint2 v;
+        v.x = f32_to_bf16(o[i][db][4 * rg] * inv) | (f32_to_bf16(o[i][db][4 * rg + 1] * inv) << 16);
+        v.y = f32_to_bf16(o[i][db][4 * rg + 2] * inv) | (f32_to_bf16(o[i][db][4 * rg + 3] * inv) << 16);
+        *reinterpret_cast<uint2*>(op + d0) = v;
+      }
+    if (lse && lh == 0) lse[(int64_t)row * n_q_heads + hq] = m[i] * scale + logf(lt);
+  }
+}
+
+int ilog2(int x) {
+  int l = 0;
+  while ((1 << l) < x) ++l;
+  return l;
+}
+
+}  // namespace
+
+hipError_t launch_attn(const tsr_plan* p, const void* q, const void* req_k,
+                       const void* req_v, void* out, float* lse, hipStream_t s) {
+  if (p->n_items == 0 || p->T == 0) return hipSuccess;
+  const tsr_model& m = p->model;
+  const int lp = ilog2(m.page_size);
+  const int G = m.n_q_heads / m.n_kv_heads;
+  const dim3 grid(p->n_items), block(256);
+  if (m.act_dtype == TSR_F32) {
+#define TSR_F32K(DIM)                                                             \
+  hipLaunchKernelGGL(attn_f32_kernel<DIM>, grid, block, 0, s,                     \
+                     static_cast<const float*>(q), static_cast<const float*>(req_k), \
+                     static_cast<const float*>(req_v), p->dev.items,               \
+                     p->dev.block_tables, p->dev.rows, p->dev.rope_cos,            \
+                     p->dev.rope_sin, static_cast<float*>(out), lse, m.n_q_heads,  \
+                     m.n_kv_heads, lp, p->scale)
+    switch (m.head_dim) {
+      case 64: TSR_F32K(64); break;
+      case 128: TSR_F32K(128); break;
+      case 256: TSR_F32K(256); break;
+      default: return hipErrorInvalidValue;
+    }
+#undef TSR_F32K
+    return hipGetLastError();
+  }
+  const float sl2e = (float)((double)p->scale * 1.4426950408889634);
+#define TSR_MFMA(GG)                                                               \
+  hipLaunchKernelGGL(attn_mfma_kernel<GG>, grid, block, 0, s,                      \
+                     static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(req_k), \
+                     static_cast<const uint16_t*>(req_v), p->dev.items,             \
+                     p->dev.block_tables, p->dev.rows, p->dev.rope_cos,             \
+                     p->dev.rope_sin, static_cast<uint16_t*>(out), lse,             \
+                     m.n_q_heads, m.n_kv_heads, lp, p->scale, sl2e)
+  switch (G) {
+    case 1: TSR_MFMA(1); break;
+    case 2: TSR_MFMA(2); break;
+    case 4: TSR_MFMA(4); break;
+    case 8: TSR_MFMA(8); break;
+    default: return hipErrorInvalidValue;
+  }
+#undef TSR_MFMA
+  return hipGetLastError();
+}
+
+}  // namespace tsr

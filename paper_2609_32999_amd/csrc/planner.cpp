@@ -1,0 +1,335 @@
+// Host planner: validates a batch of requests and builds the device image of
+// its plan (Section 5.3, placement before preparation: the prompt layout and
+// the request's KV slots are fixed before any unit is prepared).
+//
+// The plan lists
+//   * computed rows  -- text tokens, every token of a MISS unit, and the
+//                       first min(r, n) tokens of each HIT unit (the fixed
+//                       chunk-initial recompute window of the composition
+//                       policy, Section 7), by increasing position;
+//   * gathered tokens -- the remaining tokens of HIT units, pool slot ->
+//                       request slot (Section 5.1 storage blocks: token j of
+//                       a unit is in block j / B at slot j % B);
+//   * retained tokens -- tokens of MISS units allowed to be retained;
+//   * attention items -- tiles of consecutive computed rows x KV heads, in an
+//                       XCD-aware, longest-first launch order.
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <numeric>
+#include <sstream>
+
+#include "tsr_internal.h"
+
+namespace tsr {
+
+namespace {
+
+size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+bool is_pow2(int x) { return x > 0 && (x & (x - 1)) == 0; }
+
+tsr_status fail(tsr_status st, const std::string& msg) {
+  set_error(msg);
+  return st;
+}
+
+struct Seg {
+  int32_t start, len;
+  int unit;  // -1 for text
+};
+
+}  // namespace
+
+tsr_status check_model(const tsr_model* m) {
+  if (!m) return fail(TSR_ERR_INVALID_ARG, "model is NULL");
+  if (m->n_q_heads <= 0 || m->n_kv_heads <= 0)
+    return fail(TSR_ERR_INVALID_ARG, "head counts must be positive");
+  if (m->n_q_heads % m->n_kv_heads)
+    return fail(TSR_ERR_INVALID_ARG, "n_q_heads must be a multiple of n_kv_heads");
+  if (!is_pow2(m->page_size) || m->page_size < 8 || m->page_size > 64)
+    return fail(TSR_ERR_UNSUPPORTED, "page_size must be a power of two in [8, 64]");
+  if (!(m->rope_theta > 0.0) || !std::isfinite(m->rope_theta))
+    return fail(TSR_ERR_INVALID_ARG, "rope_theta must be positive and finite");
+  if (m->max_position <= 0 || m->max_position > (1 << 20))
+    return fail(TSR_ERR_INVALID_ARG, "max_position must be in [1, 2^20]");
+  if (!(m->softmax_scale >= 0.0f) || !std::isfinite(m->softmax_scale))
+    return fail(TSR_ERR_INVALID_ARG, "softmax_scale must be >= 0 and finite");
+  const int G = m->n_q_heads / m->n_kv_heads;
+  if (m->kv_dtype == TSR_F32 && m->act_dtype == TSR_F32) {
+    if (m->head_dim != 64 && m->head_dim != 128 && m->head_dim != 256)
+      return fail(TSR_ERR_UNSUPPORTED, "fp32 path supports head_dim 64, 128, 256");
+    return TSR_OK;
+  }
+  if (m->kv_dtype == TSR_BF16 && m->act_dtype == TSR_BF16) {
+    if (m->head_dim != 128)
+      return fail(TSR_ERR_UNSUPPORTED, "bf16 path supports head_dim 128");
+    if (m->page_size < 16)
+      return fail(TSR_ERR_UNSUPPORTED, "bf16 path needs page_size >= 16");
+    if (G != 1 && G != 2 && G != 4 && G != 8)
+      return fail(TSR_ERR_UNSUPPORTED, "bf16 path supports GQA group 1, 2, 4, 8");
+    return TSR_OK;
+  }
+  if (m->kv_dtype == TSR_E4M3)
+    return fail(TSR_ERR_UNSUPPORTED, "e4m3 KV pools are not implemented yet");
+  return fail(TSR_ERR_UNSUPPORTED, "unsupported (kv_dtype, act_dtype) pair");
+}
+
+tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
+                      int32_t n_req, int32_t n_pool_pages, int32_t n_req_pages,
+                      tsr_plan* p) {
+  tsr_status st = check_model(model);
+  if (st != TSR_OK) return st;
+  if (n_req < 0) return fail(TSR_ERR_INVALID_ARG, "n_req < 0");
+  if (n_req > 0 && !reqs) return fail(TSR_ERR_INVALID_ARG, "reqs is NULL");
+  if (n_pool_pages < 0 || n_req_pages < 0)
+    return fail(TSR_ERR_INVALID_ARG, "arena page counts must be >= 0");
+  if ((int64_t)n_pool_pages * model->page_size >= INT32_MAX ||
+      (int64_t)n_req_pages * model->page_size >= INT32_MAX)
+    return fail(TSR_ERR_OUT_OF_RANGE, "arena too large: pages * page_size must fit int32");
+  const tsr_model& m = *model;
+  const int B = m.page_size;
+  const int Hkv = m.n_kv_heads;
+
+  p->model = m;
+  p->scale = m.softmax_scale > 0.0f ? m.softmax_scale
+                                    : (float)(1.0 / std::sqrt((double)m.head_dim));
+  p->n_pool_pages = n_pool_pages;
+  p->n_req_pages = n_req_pages;
+  p->n_req = n_req;
+
+  std::vector<GatherDesc> gather;
+  std::vector<RowDesc> rows;
+  std::vector<RetainDesc> retain;
+  std::vector<int32_t> bts;
+  std::vector<int32_t> bt_off(n_req), bt_len(n_req), req_row0(n_req + 1, 0);
+  p->row_pos.clear();
+  p->row_req.clear();
+
+  std::vector<uint8_t> req_page_used((size_t)n_req_pages, 0);
+  // pool pages: bit 1 = read by a HIT, bit 2 = written by a retained MISS
+  std::vector<uint8_t> pool_use((size_t)n_pool_pages, 0);
+  std::ostringstream err;
+
+  for (int r = 0; r < n_req; ++r) {
+    const tsr_request& q = reqs[r];
+    if (q.prompt_len <= 0) {
+      err << "request " << r << ": prompt_len must be positive";
+      return fail(TSR_ERR_INVALID_ARG, err.str());
+    }
+    if (q.prompt_len > m.max_position) {
+      err << "request " << r << ": prompt_len " << q.prompt_len
+          << " exceeds max_position " << m.max_position;
+      return fail(TSR_ERR_OUT_OF_RANGE, err.str());
+    }
+    if (q.n_units < 0 || q.n_text < 0 || (q.n_units && !q.units) ||
+        (q.n_text && !q.text_segs) || !q.block_table) {
+      err << "request " << r << ": null or negative-size member";
+      return fail(TSR_ERR_INVALID_ARG, err.str());
+    }
+    // tiling: segments sorted by start must cover [0, prompt_len) once
+    std::vector<Seg> segs;
+    segs.reserve(q.n_units + q.n_text);
+    for (int t = 0; t < q.n_text; ++t)
+      segs.push_back({q.text_segs[2 * t], q.text_segs[2 * t + 1], -1});
+    for (int u = 0; u < q.n_units; ++u)
+      segs.push_back({q.units[u].position, q.units[u].n_tokens, u});
+    std::stable_sort(segs.begin(), segs.end(),
+                     [](const Seg& a, const Seg& b) { return a.start < b.start; });
+    int32_t expect = 0;
+    int last_unit = -1;
+    for (const Seg& s : segs) {
+      if (s.len <= 0 || s.start != expect) {
+        err << "request " << r << ": segments do not tile the prompt (segment at "
+            << s.start << " length " << s.len << ", expected start " << expect << ")";
+        return fail(TSR_ERR_INVALID_ARG, err.str());
+      }
+      if (s.unit >= 0) {
+        if (s.unit < last_unit) {
+          err << "request " << r << ": units are not in prompt order";
+          return fail(TSR_ERR_INVALID_ARG, err.str());
+        }
+        last_unit = s.unit;
+      }
+      expect += s.len;
+    }
+    if (expect != q.prompt_len) {
+      err << "request " << r << ": segments cover " << expect
+          << " tokens but prompt_len is " << q.prompt_len;
+      return fail(TSR_ERR_INVALID_ARG, err.str());
+    }
+    // block table
+    const int npg = (q.prompt_len + B - 1) / B;
+    bt_off[r] = (int32_t)bts.size();
+    bt_len[r] = npg;
+    for (int i = 0; i < npg; ++i) {
+      int32_t pg = q.block_table[i];
+      if (pg < 0 || pg >= n_req_pages) {
+        err << "request " << r << ": block_table[" << i << "] = " << pg
+            << " outside the request arena of " << n_req_pages << " pages";
+        return fail(TSR_ERR_OUT_OF_RANGE, err.str());
+      }
+      if (req_page_used[pg]) {
+        err << "request " << r << ": request page " << pg << " is used twice";
+        return fail(TSR_ERR_INVALID_ARG, err.str());
+      }
+      req_page_used[pg] = 1;
+      bts.push_back(pg);
+    }
+    auto req_slot = [&](int32_t pos) {
+      return q.block_table[pos / B] * B + pos % B;
+    };
+    // walk the prompt in position order
+    for (const Seg& s : segs) {
+      if (s.unit < 0) {
+        for (int32_t j = 0; j < s.len; ++j) {
+          rows.push_back({req_slot(s.start + j), s.start + j});
+          p->row_pos.push_back(s.start + j);
+          p->row_req.push_back(r);
+        }
+        continue;
+      }
+      const tsr_unit& u = q.units[s.unit];
+      if (u.residency != TSR_HIT && u.residency != TSR_MISS) {
+        err << "request " << r << " unit " << s.unit << ": residency must be HIT or MISS";
+        return fail(TSR_ERR_INVALID_ARG, err.str());
+      }
+      if (u.retain != 0 && u.retain != 1) {
+        err << "request " << r << " unit " << s.unit << ": retain must be 0 or 1";
+        return fail(TSR_ERR_INVALID_ARG, err.str());
+      }
+      if (u.residency == TSR_HIT && u.n_recompute < 0) {
+        err << "request " << r << " unit " << s.unit << ": n_recompute < 0";
+        return fail(TSR_ERR_INVALID_ARG, err.str());
+      }
+      const bool hit = u.residency == TSR_HIT;
+      const bool keep = !hit && u.retain == 1;
+      const int upg = (u.n_tokens + B - 1) / B;
+      if ((hit || keep) && !u.pool_pages) {
+        err << "request " << r << " unit " << s.unit << ": pool_pages is NULL";
+        return fail(TSR_ERR_INVALID_ARG, err.str());
+      }
+      if (hit || keep) {
+        for (int i = 0; i < upg; ++i) {
+          int32_t pg = u.pool_pages[i];
+          if (pg < 0 || pg >= n_pool_pages) {
+            err << "request " << r << " unit " << s.unit << ": pool page " << pg
+                << " outside the pool arena of " << n_pool_pages << " pages";
+            return fail(TSR_ERR_OUT_OF_RANGE, err.str());
+          }
+          if (keep) {
+            if (pool_use[pg] & 2) {
+              err << "request " << r << " unit " << s.unit << ": pool page " << pg
+                  << " is retained twice in this batch";
+              return fail(TSR_ERR_INVALID_ARG, err.str());
+            }
+            pool_use[pg] |= 2;
+          } else {
+            pool_use[pg] |= 1;
+          }
+        }
+      }
+      const int32_t ncomp = hit ? std::min(u.n_recompute, u.n_tokens) : u.n_tokens;
+      const int32_t row0 = (int32_t)rows.size();
+      for (int32_t j = 0; j < ncomp; ++j) {
+        rows.push_back({req_slot(u.position + j), u.position + j});
+        p->row_pos.push_back(u.position + j);
+        p->row_req.push_back(r);
+      }
+      if (hit) {
+        for (int32_t j = ncomp; j < u.n_tokens; ++j)
+          gather.push_back({u.pool_pages[j / B] * B + j % B,
+                            req_slot(u.position + j), u.position + j, 0});
+      } else if (keep) {
+        for (int32_t j = 0; j < u.n_tokens; ++j)
+          retain.push_back({row0 + j, u.pool_pages[j / B] * B + j % B});
+      }
+    }
+    req_row0[r + 1] = (int32_t)rows.size();
+  }
+  for (int32_t pg = 0; pg < n_pool_pages; ++pg) {
+    if (pool_use[pg] == 3) {
+      err << "pool page " << pg << " is both read by a HIT and written by a retained "
+          << "unit in this batch";
+      return fail(TSR_ERR_INVALID_ARG, err.str());
+    }
+  }
+  const size_t limit = (size_t)INT32_MAX;
+  if (rows.size() >= limit || gather.size() >= limit) {
+    return fail(TSR_ERR_OUT_OF_RANGE, "batch too large");
+  }
+
+  // attention items: tiles of kTileRows consecutive rows x KV heads
+  struct Item { AttnItem it; int64_t cost; int group; };
+  std::vector<Item> items;
+  int32_t max_kv = 0;
+  for (int r = 0; r < n_req; ++r) {
+    for (int32_t t0 = req_row0[r]; t0 < req_row0[r + 1]; t0 += kTileRows) {
+      const int32_t n = std::min(kTileRows, req_row0[r + 1] - t0);
+      const int32_t lo = p->row_pos[t0], hi = p->row_pos[t0 + n - 1];
+      max_kv = std::max(max_kv, hi + 1);
+      for (int g = 0; g < Hkv; ++g) {
+        AttnItem a{t0, n, hi + 1, lo, g, bt_off[r], bt_len[r], r};
+        items.push_back({a, (int64_t)(hi + 1), r * Hkv + g});
+      }
+    }
+  }
+  // XCD-aware order: (request, KV head) groups share K/V, so each group is
+  // bound to one XCD bin (workgroup w runs on XCD w % kNumXcd); bins are
+  // balanced by cost (longest group first onto the lightest bin) and each
+  // bin is issued longest item first.  Short bins are padded with empty items.
+  std::vector<int64_t> gcost((size_t)std::max(1, n_req * Hkv), 0);
+  for (const Item& x : items) gcost[x.group] += x.cost;
+  std::vector<int> gorder(gcost.size());
+  std::iota(gorder.begin(), gorder.end(), 0);
+  std::stable_sort(gorder.begin(), gorder.end(),
+                   [&](int a, int b) { return gcost[a] > gcost[b]; });
+  std::vector<int> gbin(gcost.size(), 0);
+  int64_t bin_load[kNumXcd] = {0};
+  for (int g : gorder) {
+    int best = 0;
+    for (int b = 1; b < kNumXcd; ++b)
+      if (bin_load[b] < bin_load[best]) best = b;
+    gbin[g] = best;
+    bin_load[best] += gcost[g];
+  }
+  std::vector<std::vector<AttnItem>> bins(kNumXcd);
+  std::stable_sort(items.begin(), items.end(),
+                   [](const Item& a, const Item& b) { return a.cost > b.cost; });
+  for (const Item& x : items) bins[gbin[x.group]].push_back(x.it);
+  size_t per_bin = 0;
+  for (auto& b : bins) per_bin = std::max(per_bin, b.size());
+  std::vector<AttnItem> order;
+  order.reserve(per_bin * kNumXcd);
+  for (size_t i = 0; i < per_bin; ++i)
+    for (int b = 0; b < kNumXcd; ++b)
+      order.push_back(i < bins[b].size() ? bins[b][i]
+                                         : AttnItem{0, 0, 0, 0, 0, 0, 0, -1});
+
+  p->T = (int32_t)rows.size();
+  p->n_gather = (int32_t)gather.size();
+  p->n_retain = (int32_t)retain.size();
+  p->n_items = (int32_t)order.size();
+  p->max_kv_len = max_kv;
+
+  // device image: arrays at 256-byte aligned offsets
+  size_t off = 0;
+  p->off_gather = off;  off = align_up(off + gather.size() * sizeof(GatherDesc), 256);
+  p->off_rows = off;    off = align_up(off + rows.size() * sizeof(RowDesc), 256);
+  p->off_retain = off;  off = align_up(off + retain.size() * sizeof(RetainDesc), 256);
+  p->off_items = off;   off = align_up(off + order.size() * sizeof(AttnItem), 256);
+  p->off_bt = off;      off = align_up(off + bts.size() * sizeof(int32_t), 256);
+  p->ws_bytes = std::max<size_t>(off, 256);
+  p->image.assign(p->ws_bytes, 0);
+  auto put = [&](size_t o, const void* src, size_t n) {
+    if (n) std::memcpy(p->image.data() + o, src, n);
+  };
+  put(p->off_gather, gather.data(), gather.size() * sizeof(GatherDesc));
+  put(p->off_rows, rows.data(), rows.size() * sizeof(RowDesc));
+  put(p->off_retain, retain.data(), retain.size() * sizeof(RetainDesc));
+  put(p->off_items, order.data(), order.size() * sizeof(AttnItem));
+  put(p->off_bt, bts.data(), bts.size() * sizeof(int32_t));
+  return TSR_OK;
+}
+
+}  // namespace tsr

@@ -1,0 +1,114 @@
+// Internal declarations of libtsr: the device image of a plan and the kernel
+// launchers.  Not part of the ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "../../include/tsr.h"
+
+namespace tsr {
+
+// Rows of one attention tile: consecutive computed rows of one request.
+constexpr int kTileRows = 32;
+// Keys per attention KV tile.
+constexpr int kKvTile = 64;
+// Workgroups of the MFMA attention are dealt round-robin over this many XCDs.
+constexpr int kNumXcd = 8;
+
+// A cached token moved by compose: pool slot -> request slot at `pos`.
+// Slots are page * page_size + slot-in-page.
+struct alignas(16) GatherDesc {
+  int32_t src;
+  int32_t dst;
+  int32_t pos;
+  int32_t pad;
+};
+
+// A computed row: its request slot and prompt position.
+struct alignas(8) RowDesc {
+  int32_t dst;
+  int32_t pos;
+};
+
+// A retained token: computed row -> pool slot.
+struct alignas(8) RetainDesc {
+  int32_t row;
+  int32_t dst;
+};
+
+// One attention work item: up to kTileRows consecutive computed rows of one
+// request against one KV head.  n_rows == 0 marks padding.
+struct alignas(16) AttnItem {
+  int32_t row0;      // first computed row (plan order)
+  int32_t n_rows;    // rows in the tile (<= kTileRows)
+  int32_t kv_len;    // keys 0 .. kv_len-1 are visible to some row (max pos + 1)
+  int32_t min_pos;   // smallest position among the rows
+  int32_t kv_head;
+  int32_t bt_off;    // offset of the request's block table in the plan
+  int32_t n_pages;   // entries of that block table
+  int32_t req;
+};
+
+// Device-side view of a plan (pointers into the caller's workspace).
+struct PlanDev {
+  const GatherDesc* gather;
+  const RowDesc* rows;
+  const RetainDesc* retain;
+  const AttnItem* items;
+  const int32_t* block_tables;
+  const float* rope_cos;   // [max_position][d/2]
+  const float* rope_sin;   // [max_position][d/2]
+};
+
+}  // namespace tsr
+
+struct tsr_plan {
+  tsr_model model;
+  float scale;              // resolved softmax scale
+  int32_t n_pool_pages;
+  int32_t n_req_pages;
+  int32_t n_req;
+  int32_t T;                // computed rows
+  int32_t n_gather;
+  int32_t n_retain;
+  int32_t n_items;          // attention items incl. padding
+  int32_t max_kv_len;
+  std::vector<int32_t> row_pos, row_req;
+  std::vector<char> image;  // host copy of the device image
+  size_t off_gather, off_rows, off_retain, off_items, off_bt, ws_bytes;
+  const void* rope_table;   // device
+  void* ws;                 // device, NULL for host-only plans
+  tsr::PlanDev dev;
+};
+
+namespace tsr {
+
+// Thread-local error text, set by every failing entry point.
+void set_error(const std::string& msg);
+
+// Validate a model; on failure returns a status and sets the error.
+tsr_status check_model(const tsr_model* m);
+
+// Build a plan's host part (validation + descriptors + image layout).
+tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
+                      int32_t n_req, int32_t n_pool_pages, int32_t n_req_pages,
+                      tsr_plan* plan);
+
+// Kernel launchers (return hipSuccess or the launch error).
+hipError_t launch_compose(const tsr_plan* p, const void* pool_k,
+                          const void* pool_v, void* req_k, void* req_v,
+                          int32_t n_layers, int64_t pool_stride,
+                          int64_t req_stride, hipStream_t s);
+hipError_t launch_append(const tsr_plan* p, const void* k, const void* v,
+                         void* req_k, void* req_v, hipStream_t s);
+hipError_t launch_attn(const tsr_plan* p, const void* q, const void* req_k,
+                       const void* req_v, void* out, float* lse, hipStream_t s);
+hipError_t launch_retain(const tsr_plan* p, const void* k, const void* v,
+                         void* pool_k, void* pool_v, hipStream_t s);
+
+}  // namespace tsr

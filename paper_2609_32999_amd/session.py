@@ -1,0 +1,106 @@
+"""Device buffers for one attention layer of the composed-prefill path.
+
+PyTorch provides device memory and streams only; every step of the path runs
+in libtsr's kernels through the C ABI.  A Session owns, for one layer shape:
+
+* the pool arena     [n_pool_pages][H_kv][B][d] for K (pre-RoPE) and V;
+* the request arena  [n_req_pages][H_kv][B][d] for the assembled K and V;
+* the RoPE table     built once per model by tsr_rope_table_init.
+
+Plans (one per batch of requests) own their device workspace.
+"""
+from __future__ import annotations
+
+import torch
+
+from . import _binding as B
+
+TORCH_DTYPE = {"f32": torch.float32, "bf16": torch.bfloat16}
+
+
+def _require_device():
+    if not torch.cuda.is_available():
+        raise RuntimeError("libtsr needs a ROCm GPU; none is visible")
+
+
+class Session:
+    def __init__(self, shape, n_pool_pages: int, n_req_pages: int,
+                 device: str = "cuda", n_layers: int = 1, stream=None):
+        """`shape` has n_q_heads, n_kv_heads, head_dim, page_size, kv_dtype,
+        act_dtype, rope_theta, max_position (workloads.ModelShape)."""
+        _require_device()
+        B.lib()
+        self.shape = shape
+        self.model = B.make_model(shape.n_q_heads, shape.n_kv_heads, shape.head_dim,
+                                  shape.page_size, shape.kv_dtype, shape.act_dtype,
+                                  shape.rope_theta, shape.max_position)
+        if shape.kv_dtype not in TORCH_DTYPE:
+            raise B.TsrError(B.TSR_ERR_UNSUPPORTED, f"kv dtype {shape.kv_dtype}")
+        self.device = torch.device(device)
+        self.kv_dtype = TORCH_DTYPE[shape.kv_dtype]
+        self.act_dtype = TORCH_DTYPE[shape.act_dtype]
+        self.n_layers = n_layers
+        self.n_pool_pages = n_pool_pages
+        self.n_req_pages = n_req_pages
+        page = (shape.n_kv_heads, shape.page_size, shape.head_dim)
+        self.pool_k = torch.empty((n_layers, n_pool_pages, *page), dtype=self.kv_dtype,
+                                  device=self.device)
+        self.pool_v = torch.empty_like(self.pool_k)
+        self.req_k = torch.empty((n_layers, n_req_pages, *page), dtype=self.kv_dtype,
+                                 device=self.device)
+        self.req_v = torch.empty_like(self.req_k)
+        nbytes = B.tsr_rope_table_bytes(self.model)
+        if nbytes == 0:
+            raise B.TsrError(B.TSR_ERR_INVALID_ARG, B.tsr_last_error())
+        self.rope = torch.empty(nbytes // 4, dtype=torch.float32, device=self.device)
+        self.stream = stream if stream is not None else torch.cuda.current_stream(self.device)
+        B.tsr_rope_table_init(self.model, self.rope, nbytes, self.stream)
+
+    # ------------------------------------------------------------- plans
+    def plan(self, requests, stream=None):
+        batch = B.RequestBatch(requests)
+        ws_bytes = B.tsr_plan_workspace_size(self.model, batch, self.n_pool_pages,
+                                             self.n_req_pages)
+        ws = torch.empty(ws_bytes, dtype=torch.uint8, device=self.device)
+        plan = B.tsr_plan_create(self.model, batch, self.n_pool_pages, self.n_req_pages,
+                                 self.rope, ws, ws_bytes, stream or self.stream)
+        plan.workspace = ws     # keep the workspace alive with the plan
+        plan.batch = batch
+        return plan
+
+    # ---------------------------------------------------------- hot path
+    def compose(self, plan, layer: int | None = None, stream=None):
+        """Compose one layer (default 0), or all layers when layer == 'all'."""
+        s = stream or self.stream
+        if layer == "all":
+            B.tsr_compose_kv(plan, self.pool_k, self.pool_v, None, self.req_k, self.req_v,
+                             None, self.n_layers, self.pool_k[0].nbytes if self.n_layers > 1 else 0,
+                             self.req_k[0].nbytes if self.n_layers > 1 else 0, s)
+            return
+        li = layer or 0
+        B.tsr_compose_kv(plan, self.pool_k[li], self.pool_v[li], None, self.req_k[li],
+                         self.req_v[li], None, 1, 0, 0, s)
+
+    def new_outputs(self, plan, with_lse: bool = True):
+        T = plan.num_compute_tokens
+        out = torch.empty((T, self.shape.n_q_heads, self.shape.head_dim),
+                          dtype=self.act_dtype, device=self.device)
+        lse = (torch.empty((T, self.shape.n_q_heads), dtype=torch.float32,
+                           device=self.device) if with_lse else None)
+        return out, lse
+
+    def prefill_attn(self, plan, q, k, v, out, lse=None, layer: int = 0, stream=None):
+        B.tsr_prefill_attn(plan, q, k, v, self.req_k[layer], self.req_v[layer], None,
+                           out, lse, stream or self.stream)
+
+    def append(self, plan, k, v, layer: int = 0, stream=None):
+        B.tsr_append_kv(plan, k, v, self.req_k[layer], self.req_v[layer], None,
+                        stream or self.stream)
+
+    def attn(self, plan, q, out, lse=None, layer: int = 0, stream=None):
+        B.tsr_attn(plan, q, self.req_k[layer], self.req_v[layer], None, out, lse,
+                   stream or self.stream)
+
+    def retain(self, plan, k, v, layer: int = 0, stream=None):
+        B.tsr_retain_kv(plan, k, v, self.pool_k[layer], self.pool_v[layer], None,
+                        stream or self.stream)

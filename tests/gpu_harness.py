@@ -1,0 +1,179 @@
+"""Shared helpers of the GPU parity tests: run the HIP path on a workload and
+compare it with the oracle.  Test infrastructure (imports the oracle)."""
+from __future__ import annotations
+
+import math
+import sys
+
+import numpy as np
+import torch
+
+from oracle import layout as L
+from oracle import pipeline as PL
+from oracle.compose import retained_pages
+from oracle.numerics import round_bf16
+from paper_2609_32999_amd import staging
+from paper_2609_32999_amd.session import Session
+
+# spec tolerances (relative Frobenius error per request and query head)
+TOL_BF16 = 2e-3
+TOL_F32 = 1e-5
+
+SENTINEL_BITS = {torch.bfloat16: 0x7FC1, torch.float32: 0x7FC00001}
+
+
+def fill_sentinel(t: torch.Tensor) -> None:
+    if t.dtype == torch.bfloat16:
+        t.view(torch.int16).fill_(SENTINEL_BITS[torch.bfloat16])
+    else:
+        t.view(torch.int32).fill_(SENTINEL_BITS[torch.float32])
+
+
+def is_sentinel(a: torch.Tensor) -> torch.Tensor:
+    if a.dtype == torch.bfloat16:
+        return a.view(torch.int16) == SENTINEL_BITS[torch.bfloat16]
+    return a.view(torch.int32) == SENTINEL_BITS[torch.float32]
+
+
+def say(msg: str) -> None:
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+class GpuRun:
+    """Runs compose -> prefill_attn -> retain on a workload (one layer)."""
+
+    def __init__(self, wl, with_lse=True):
+        self.wl = wl
+        m = wl.model
+        say(f"[gpu] workload={wl.name} seed={wl.seed} H={m.n_q_heads}/{m.n_kv_heads} "
+            f"d={m.head_dim} {m.kv_dtype} prompt_tokens={wl.prompt_tokens}")
+        s = Session(m, wl.n_pool_pages, wl.n_req_pages)
+        self.sess = s
+        for t in (s.pool_k, s.pool_v, s.req_k, s.req_v):
+            fill_sentinel(t)
+        staging.upload_pool(s, wl)
+        self.pool_k0 = s.pool_k.clone()
+        self.pool_v0 = s.pool_v.clone()
+        self.plan = s.plan(wl.requests)
+        self.q, self.k, self.v = staging.fresh_inputs(s, wl, self.plan)
+        self.pos, self.req = self.plan.compute_positions()
+        s.compose(self.plan)
+        torch.cuda.synchronize()
+        self.pool_after_compose_ok = bool(torch.equal(s.pool_k.view(torch.uint8),
+                                                      self.pool_k0.view(torch.uint8)))
+        self.out, self.lse = s.new_outputs(self.plan, with_lse)
+        s.prefill_attn(self.plan, self.q, self.k, self.v, self.out, self.lse)
+        torch.cuda.synchronize()
+        self.pool_after_attn_ok = bool(torch.equal(s.pool_k.view(torch.uint8),
+                                                   self.pool_k0.view(torch.uint8)) and
+                                       torch.equal(s.pool_v.view(torch.uint8),
+                                                   self.pool_v0.view(torch.uint8)))
+        s.retain(self.plan, self.k, self.v)
+        torch.cuda.synchronize()
+        say(f"[gpu] ran T={self.plan.num_compute_tokens} gather={self.plan.num_gather_tokens} "
+            f"retain={self.plan.num_retain_tokens} items={self.plan.num_attn_items}")
+
+    def request_kv(self, r):
+        return staging.request_kv(self.sess, self.wl, r)
+
+    def rows_of(self, r):
+        return np.nonzero(self.req == r)[0]
+
+
+def rel_frob(a, b) -> float:
+    a = np.asarray(a, np.float64)
+    b = np.asarray(b, np.float64)
+    den = np.linalg.norm(b)
+    return float(np.linalg.norm(a - b) / den) if den > 0 else float(np.linalg.norm(a))
+
+
+def check_request(run: GpuRun, r: int, kv_heads=None, check_kv=True):
+    """Compare request r (optionally a subset of KV heads) with the oracle.
+
+    Returns a dict of the measured errors; asserts the spec bars."""
+    wl = run.wl
+    m = wl.model
+    res = PL.run_request(wl, r, kv_heads=kv_heads)
+    report = {}
+    rows = run.rows_of(r)
+    assert np.array_equal(run.pos[rows], res.positions), "computed positions differ"
+    if check_kv:
+        K, V = run.request_kv(r)
+        K, V = K[:, res.kv_heads], V[:, res.kv_heads]
+        assert not np.isnan(K).any() and not np.isnan(V).any(), "unwritten request slot"
+        assert np.array_equal(V.view(np.uint32), res.V.view(np.uint32)), "V not bit-exact"
+        kd = K.view(np.uint32) != res.K.view(np.uint32)
+        report["k_mismatch"] = int(kd.sum())
+        assert report["k_mismatch"] == 0, f"K differs in {kd.sum()} elements"
+    out = run.out[torch.as_tensor(rows, device=run.out.device)].float().cpu().numpy()
+    out = out[:, res.q_heads]
+    tol = TOL_F32 if m.act_dtype == "f32" else TOL_BF16
+    worst = 0.0
+    worst_unrounded = 0.0
+    for hi, h in enumerate(res.q_heads):
+        ref = res.out[:, hi]
+        if m.act_dtype == "bf16":
+            e = rel_frob(out[:, hi], round_bf16(ref.astype(np.float32)))
+            worst_unrounded = max(worst_unrounded, rel_frob(out[:, hi], ref))
+        else:
+            e = rel_frob(out[:, hi], ref)
+        worst = max(worst, e)
+    report["out_rel_err"] = worst
+    report["out_rel_err_unrounded"] = worst_unrounded
+    assert worst <= tol, f"request {r}: attention rel err {worst:.3g} > {tol}"
+    if run.lse is not None:
+        lse = run.lse[torch.as_tensor(rows, device=run.lse.device)].cpu().numpy()[:, res.q_heads]
+        lerr = float(np.abs(lse - res.lse).max())
+        report["lse_abs_err"] = lerr
+        assert lerr <= (1e-4 if m.act_dtype == "f32" else 2e-2), f"lse err {lerr}"
+        # softmax rows sum to one under the GPU's lse (a sampled set of rows)
+        G = m.n_q_heads // m.n_kv_heads
+        scale = 1.0 / math.sqrt(m.head_dim)
+        sel = np.linspace(0, len(rows) - 1, num=min(8, len(rows))).astype(int)
+        for t in sel:
+            for hi in range(0, len(res.q_heads), max(1, len(res.q_heads) // 4)):
+                g = hi // G
+                p = int(res.positions[t])
+                s = scale * (res.K[:p + 1, g].astype(np.float64) @ res.q[t, hi].astype(np.float64))
+                tot = float(np.exp(s - float(lse[t, hi])).sum())
+                assert abs(tot - 1.0) <= (1e-5 if m.act_dtype == "f32" else 1e-3), tot
+    say(f"[gpu] request {r}: {report}")
+    return report
+
+
+def check_retained(run: GpuRun):
+    wl = run.wl
+    pages = retained_pages(wl)
+    s = run.sess
+    B = wl.model.page_size
+    for pg, (kref, vref, filled) in pages.items():
+        gk = s.pool_k[0, pg].float().cpu().numpy()          # [H][B][d]
+        gv = s.pool_v[0, pg].float().cpu().numpy()
+        assert np.array_equal(gk[:, filled].view(np.uint32), kref[:, filled].view(np.uint32))
+        assert np.array_equal(gv[:, filled].view(np.uint32), vref[:, filled].view(np.uint32))
+        if (~filled).any():
+            sk = is_sentinel(s.pool_k[0, pg])[:, torch.as_tensor(~filled, device=s.device)]
+            assert bool(sk.all()), "retain wrote past the unit's last token"
+    # every other pool page is untouched
+    touched = torch.zeros(wl.n_pool_pages, dtype=torch.bool, device=s.device)
+    if pages:
+        touched[torch.as_tensor(list(pages), device=s.device)] = True
+    same_k = (s.pool_k[0].view(torch.uint8) == run.pool_k0[0].view(torch.uint8))
+    same_v = (s.pool_v[0].view(torch.uint8) == run.pool_v0[0].view(torch.uint8))
+    untouched = ~touched
+    assert bool(same_k[untouched].all()) and bool(same_v[untouched].all())
+    return len(pages)
+
+
+def check_request_sentinels(run: GpuRun, r: int):
+    """Slots past prompt_len in the request's last page keep the sentinel."""
+    wl = run.wl
+    req = wl.requests[r]
+    B = wl.model.page_size
+    tail = req.prompt_len % B
+    if tail == 0:
+        return
+    last = int(req.block_table[-1])
+    assert bool(is_sentinel(run.sess.req_k[0, last][:, tail:]).all())
+    assert bool(is_sentinel(run.sess.req_v[0, last][:, tail:]).all())

@@ -1,0 +1,175 @@
+"""C-ABI checks that need no GPU: exports, validation, host-only plans."""
+import os
+import re
+from types import SimpleNamespace as NS
+
+import numpy as np
+import pytest
+
+import paper_2609_32999_amd as P
+import workloads
+from oracle import layout as L
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _model(wl, **kw):
+    m = wl.model
+    args = dict(n_q_heads=m.n_q_heads, n_kv_heads=m.n_kv_heads, head_dim=m.head_dim,
+                page_size=m.page_size, kv_dtype=m.kv_dtype, act_dtype=m.act_dtype,
+                rope_theta=m.rope_theta, max_position=m.max_position)
+    args.update(kw)
+    return P.make_model(**args)
+
+
+def _plan(wl, reqs=None, **kw):
+    reqs = wl.requests if reqs is None else reqs
+    return P.tsr_plan_create(_model(wl, **kw), P.RequestBatch(reqs), wl.n_pool_pages,
+                             wl.n_req_pages)
+
+
+def test_library_exports_every_declared_symbol():
+    with open(os.path.join(ROOT, "include", "tsr.h")) as f:
+        header = f.read()
+    declared = set(re.findall(r"^\s*(?:[\w\*]+\s+)+\**(tsr_\w+)\s*\(", header, re.M))
+    assert declared == set(P.EXPORTS), declared ^ set(P.EXPORTS)
+    lib = P.lib()
+    for name in declared:
+        assert getattr(lib, name) is not None
+
+
+def test_abi_version():
+    assert P.tsr_abi_version() == 1
+
+
+@pytest.mark.parametrize("name", ["tiny", "small_bf16", "small_f32", "small_bf16_g8",
+                                  "rag8b", "long70b"])
+def test_host_plan_matches_oracle_sets(name):
+    wl = workloads.generate(name)
+    plan = _plan(wl)
+    pos, req = plan.compute_positions()
+    opos = np.concatenate([L.compute_positions(r) for r in wl.requests])
+    oreq = np.concatenate([np.full(len(L.compute_positions(r)), i)
+                           for i, r in enumerate(wl.requests)])
+    assert np.array_equal(pos, opos) and np.array_equal(req, oreq)
+    assert plan.num_gather_tokens == sum(len(L.gather_tokens(r)) for r in wl.requests)
+    assert plan.num_retain_tokens == sum(len(L.retain_tokens(r, wl.model.page_size))
+                                         for r in wl.requests)
+    assert plan.num_attn_items % 8 == 0
+
+
+def _tiny_req(**over):
+    wl = workloads.generate("tiny")
+    req = wl.requests[0]
+    units = [NS(**vars(u)) for u in req.units]
+    r = NS(prompt_len=req.prompt_len, units=units, text_segs=list(req.text_segs),
+           block_table=req.block_table.copy())
+    for k, v in over.items():
+        setattr(r, k, v)
+    return wl, r
+
+
+def _expect(status, wl, reqs, match, **kw):
+    with pytest.raises(P.TsrError) as e:
+        _plan(wl, reqs, **kw)
+    assert e.value.status == status
+    assert re.search(match, e.value.message), e.value.message
+    assert re.search(match, P.tsr_last_error())
+
+
+def test_rejects_gap_and_overlap():
+    wl, r = _tiny_req()
+    r.units[1].position += 1
+    _expect(P._binding.TSR_ERR_INVALID_ARG, wl, [r], "tile")
+    wl, r = _tiny_req()
+    r.units[1].n_tokens += 1
+    _expect(P._binding.TSR_ERR_INVALID_ARG, wl, [r], "tile")
+    wl, r = _tiny_req(prompt_len=300)
+    _expect(P._binding.TSR_ERR_INVALID_ARG, wl, [r], "prompt_len")
+
+
+def test_rejects_out_of_range_pages():
+    wl, r = _tiny_req()
+    r.units[1].pool_pages = r.units[1].pool_pages.copy()
+    r.units[1].pool_pages[0] = wl.n_pool_pages
+    _expect(P._binding.TSR_ERR_OUT_OF_RANGE, wl, [r], "pool page")
+    wl, r = _tiny_req()
+    r.block_table[3] = -1
+    _expect(P._binding.TSR_ERR_OUT_OF_RANGE, wl, [r], "block_table")
+
+
+def test_rejects_shared_request_pages():
+    wl, r = _tiny_req()
+    r2 = NS(**vars(r))
+    _expect(P._binding.TSR_ERR_INVALID_ARG, wl, [r, r2], "used twice")
+
+
+def test_rejects_retain_into_pages_read_by_a_hit():
+    wl, r = _tiny_req()
+    # unit 0 is a retained MISS; point it at the pages of the HIT unit 1
+    assert r.units[0].residency == 0 and r.units[0].retain == 1
+    r.units[0].pool_pages = r.units[1].pool_pages
+    _expect(P._binding.TSR_ERR_INVALID_ARG, wl, [r], "both read")
+
+
+def test_rejects_double_retain():
+    wl, r = _tiny_req()
+    r.units[2].retain = 1
+    r.units[2].pool_pages = r.units[0].pool_pages
+    _expect(P._binding.TSR_ERR_INVALID_ARG, wl, [r], "retained twice")
+
+
+def test_rejects_unsupported_shapes():
+    wl, r = _tiny_req()
+    _expect(P._binding.TSR_ERR_UNSUPPORTED, wl, [r], "e4m3", kv_dtype="e4m3", act_dtype="bf16")
+    _expect(P._binding.TSR_ERR_UNSUPPORTED, wl, [r], "head_dim", head_dim=96)
+    _expect(P._binding.TSR_ERR_UNSUPPORTED, wl, [r], "bf16 path", kv_dtype="bf16",
+            act_dtype="bf16")           # tiny has head_dim 64
+    _expect(P._binding.TSR_ERR_OUT_OF_RANGE, wl, [r], "max_position", max_position=100)
+    _expect(P._binding.TSR_ERR_INVALID_ARG, wl, [r], "multiple", n_q_heads=6)
+
+
+def test_rejects_bad_unit_fields():
+    wl, r = _tiny_req()
+    r.units[1].residency = 2
+    _expect(P._binding.TSR_ERR_INVALID_ARG, wl, [r], "residency")
+    wl, r = _tiny_req()
+    r.units[1].n_recompute = -1
+    _expect(P._binding.TSR_ERR_INVALID_ARG, wl, [r], "n_recompute")
+    wl, r = _tiny_req()
+    r.units[1].pool_pages = None
+    _expect(P._binding.TSR_ERR_INVALID_ARG, wl, [r], "pool_pages")
+
+
+def test_host_only_plan_cannot_execute():
+    wl = workloads.generate("tiny")
+    plan = _plan(wl)
+    with pytest.raises(P.TsrError) as e:
+        P.tsr_compose_kv(plan, 1, 1, None, 1, 1, None)
+    assert e.value.status == P._binding.TSR_ERR_INVALID_ARG
+    assert "host-only" in e.value.message
+
+
+def test_workspace_size_and_rope_table_size():
+    wl = workloads.generate("rag8b")
+    m = _model(wl)
+    ws = P.tsr_plan_workspace_size(m, P.RequestBatch(wl.requests), wl.n_pool_pages,
+                                   wl.n_req_pages)
+    assert ws > 0 and ws % 256 == 0
+    assert P.tsr_rope_table_bytes(m) == 2 * 4 * m.max_position * (m.head_dim // 2)
+
+
+def test_edge_requests_plan():
+    # a prompt made only of reused units with no window: nothing to compute
+    wl, r = _tiny_req()
+    for u in r.units:
+        u.residency, u.n_recompute, u.retain = 1, 0, 0
+    r.units[-1].n_tokens += 16
+    r.units[-1].pool_pages = np.append(r.units[-1].pool_pages, 0).astype(np.int32)
+    r.text_segs = []
+    plan = _plan(wl, [r])
+    assert plan.num_compute_tokens == 0 and plan.num_gather_tokens == 272
+    # single-token prompt of text only
+    r1 = NS(prompt_len=1, units=[], text_segs=[(0, 1)], block_table=np.array([5], np.int32))
+    plan = _plan(wl, [r1])
+    assert plan.num_compute_tokens == 1 and plan.num_attn_items == 8
