@@ -65,6 +65,9 @@ def main():
     ap.add_argument("--layers", type=int, default=8)
     ap.add_argument("--cpu-requests", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calib-copy-mib", type=int, default=0,
+                    help="run one plain device copy of this size first (to scale "
+                         "HBM byte counters against a kernel of known traffic)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the path "
@@ -75,6 +78,16 @@ def main():
     import workloads
     from paper_2609_32999_amd import staging
     from paper_2609_32999_amd.session import Session
+
+    if args.calib_copy_mib:
+        n = args.calib_copy_mib << 20
+        a = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)
+        b = torch.empty_like(a)
+        torch.cuda.synchronize()
+        b.copy_(a)
+        torch.cuda.synchronize()
+        log(f"[bench] calibration copy of {args.calib_copy_mib} MiB done")
+        del a, b
 
     wl = workloads.generate(args.workload)
     m = wl.model
@@ -105,25 +118,28 @@ def main():
     evr = [[E(), E()] for _ in range(n_ev)]
 
     def step(i, rec=None, recr=None):
+        # main: compose -> append -> attention.  side: retain, started once
+        # append has been issued so that it overlaps the MFMA-bound attention
+        # rather than competing with compose for HBM bandwidth.
         l = i % L
         if rec:
             rec[0].record(main_s)
-        side.wait_stream(main_s)
-        with torch.cuda.stream(side):
-            if recr:
-                recr[0].record(side)
-            sess.retain(plan, ks[l], vs[l], layer=l, stream=side)
-            if recr:
-                recr[1].record(side)
         sess.compose(plan, layer=l, stream=main_s)
         if rec:
             rec[1].record(main_s)
         sess.append(plan, ks[l], vs[l], layer=l, stream=main_s)
         if rec:
             rec[2].record(main_s)
+        side.wait_stream(main_s)
         sess.attn(plan, qs[l], out, lse, layer=l, stream=main_s)
         if rec:
             rec[3].record(main_s)
+        with torch.cuda.stream(side):
+            if recr:
+                recr[0].record(side)
+            sess.retain(plan, ks[l], vs[l], layer=l, stream=side)
+            if recr:
+                recr[1].record(side)
         main_s.wait_stream(side)
 
     for i in range(args.warmup):

@@ -23,6 +23,7 @@
 //                     second product as fp16 (bf16 P would cost ~2e-3
 //                     relative error; fp16 keeps it near 2e-4).
 #include <cmath>
+#include <type_traits>
 
 #include "kernels_common.h"
 #include "tsr_internal.h"
@@ -137,6 +138,9 @@ constexpr int kVStr = kKT + 4;         // fp16 elements per V^T row in LDS
 constexpr int kKElems = kKT * kKStr;
 constexpr int kVElems = kD * kVStr;
 constexpr int kStage = kKElems + kVElems;
+// Lazy rescale threshold (log2 units): P may grow to 2^kLazy before the
+// running max is moved.
+constexpr float kLazy = 8.0f;
 
 __device__ __forceinline__ uint32_t pack_f16x2(float a, float b) {
   // bf16 values convert to fp16 exactly inside fp16's normal range
@@ -206,35 +210,47 @@ __global__ __launch_bounds__(256, (G > 4 ? 1 : 2)) void attn_mfma_kernel(
 #pragma unroll
       for (int r = 0; r < 16; ++r) o[i][db][r] = 0.0f;
   }
+  // With G < 4 some waves own no head: they compute a duplicate of head
+  // G-1 (branch-free MFMA code) and store nothing.
   bool wave_active[HPW];
 #pragma unroll
   for (int i = 0; i < HPW; ++i) wave_active[i] = (w + 4 * i) < G;
 
   // ---- global -> register staging of one K/V tile
-  // K: thread owns 16 bytes (8 dims) of keys 16*pb + tid/16, pb = 0..3.
-  // V: thread owns 16 bytes of keys 4*(tid/16) + pb, so it can write four
-  //    consecutive keys of each of its 8 dims to the transposed V tile.
+  // The tile's 64 keys form four 16-key blocks; with B >= 16 each block lies
+  // in one page, so its base address is uniform (scalar block-table loads)
+  // and every lane adds a fixed offset.
+  // K: thread owns 16 bytes (8 dims) of key 16*pb + tid/16 of block pb.
+  // V: thread owns 16 bytes of keys 4*(tid/16) + pb, i.e. of block w (its
+  //    wave), so it can write four consecutive keys of each of its 8 dims to
+  //    the transposed V tile.
   uint4 kr[4], vr[4];
   const int kc8 = (tid & 15) * 8;
+  const int koff = (tid >> 4) * kD + kc8;
+  const int voff = 4 * ((tid >> 4) & 3) * kD + kc8;
+  const int wu = __builtin_amdgcn_readfirstlane(w);
   auto load_tile = [&](int j) {
+    const int key0 = j * kKT;
+    int64_t base[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int kq = key0 + 16 * q;
+      const int page = bt[min(kq >> log2_page, it.n_pages - 1)];
+      base[q] = ((((int64_t)page * n_kv_heads + g) << log2_page) + (kq & page_mask)) * kD;
+    }
+    const int64_t vbase = wu == 0 ? base[0] : wu == 1 ? base[1] : wu == 2 ? base[2] : base[3];
 #pragma unroll
     for (int pb = 0; pb < 4; ++pb) {
-      const int kk = j * kKT + 16 * pb + (tid >> 4);
-      uint4 x = make_uint4(0, 0, 0, 0);
-      if (kk < it.kv_len) {
-        const int64_t a = ((((int64_t)bt[kk >> log2_page] * n_kv_heads + g) << log2_page) +
-                           (kk & page_mask)) * kD + kc8;
-        x = *reinterpret_cast<const uint4*>(kc + a);
+      kr[pb] = *reinterpret_cast<const uint4*>(kc + base[pb] + koff);
+      vr[pb] = *reinterpret_cast<const uint4*>(vc + vbase + voff + pb * kD);
+    }
+    if (key0 + kKT > it.kv_len) {
+      // last, partial tile: keys past kv_len may be unwritten slots
+#pragma unroll
+      for (int pb = 0; pb < 4; ++pb) {
+        if (key0 + 16 * pb + (tid >> 4) >= it.kv_len) kr[pb] = make_uint4(0, 0, 0, 0);
+        if (key0 + 4 * (tid >> 4) + pb >= it.kv_len) vr[pb] = make_uint4(0, 0, 0, 0);
       }
-      kr[pb] = x;
-      const int kv = j * kKT + 4 * (tid >> 4) + pb;
-      uint4 y = make_uint4(0, 0, 0, 0);
-      if (kv < it.kv_len) {
-        const int64_t a = ((((int64_t)bt[kv >> log2_page] * n_kv_heads + g) << log2_page) +
-                           (kv & page_mask)) * kD + kc8;
-        y = *reinterpret_cast<const uint4*>(vc + a);
-      }
-      vr[pb] = y;
     }
   };
   auto store_tile = [&](int buf) {
@@ -259,14 +275,11 @@ __global__ __launch_bounds__(256, (G > 4 ? 1 : 2)) void attn_mfma_kernel(
     }
   };
 
-  const int ntiles = (it.kv_len + kKT - 1) / kKT;
-  load_tile(0);
-  store_tile(0);
-  __syncthreads();
-
-  for (int j = 0; j < ntiles; ++j) {
-    const bool more = j + 1 < ntiles;
-    if (more) load_tile(j + 1);
+  // One 64-key tile: S^T = K Q^T, online softmax, O^T += V^T P^T.
+  // MASK: apply the causal mask (only tiles reaching past the smallest row
+  // position of the item need it).
+  auto tile = [&](int j, auto mask_tag) {
+    constexpr bool MASK = decltype(mask_tag)::value;
     const uint16_t* ks = smem + (j & 1) * kStage;
     const uint16_t* vs = ks + kKElems;
 
@@ -286,14 +299,12 @@ __global__ __launch_bounds__(256, (G > 4 ? 1 : 2)) void attn_mfma_kernel(
         a.u = *reinterpret_cast<const uint4*>(ks + (32 * kb + lrow) * kKStr + 16 * kst + 8 * lh);
 #pragma unroll
         for (int i = 0; i < HPW; ++i)
-          if (wave_active[i])
-            s[i][kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a.b, qf[i][kst], s[i][kb], 0, 0, 0);
+          s[i][kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a.b, qf[i][kst], s[i][kb], 0, 0, 0);
       }
     }
 
-    // causal mask (only tiles reaching past the tile's first row position)
-    const int kbase = j * kKT;
-    if (kbase + kKT - 1 > it.min_pos) {
+    if constexpr (MASK) {
+      const int kbase = j * kKT;
 #pragma unroll
       for (int i = 0; i < HPW; ++i)
 #pragma unroll
@@ -301,11 +312,14 @@ __global__ __launch_bounds__(256, (G > 4 ? 1 : 2)) void attn_mfma_kernel(
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
             const int key = kbase + 32 * kb + 8 * (r >> 2) + 4 * lh + (r & 3);
-            if (key > pos) s[i][kb][r] = -INFINITY;
+            s[i][kb][r] = key > pos ? -INFINITY : s[i][kb][r];
           }
     }
 
-    // online softmax; P^T fragments for the PV product
+    // Online softmax with a lazily updated running max: the max (and with
+    // it O and l) is only rescaled when a row's tile max exceeds it by more
+    // than 2^kLazy in probability units, so P stays <= 2^kLazy (exact range
+    // for fp16) and the rescale is skipped on almost every tile.
     f16x8 pf[HPW][4];
 #pragma unroll
     for (int i = 0; i < HPW; ++i) {
@@ -315,9 +329,18 @@ __global__ __launch_bounds__(256, (G > 4 ? 1 : 2)) void attn_mfma_kernel(
 #pragma unroll
         for (int r = 0; r < 16; ++r) mt = fmaxf(mt, s[i][kb][r]);
       mt = fmaxf(mt, __shfl_xor(mt, 32));
-      const float mn = fmaxf(m[i], mt);
-      const float alpha = __builtin_amdgcn_exp2f((m[i] - mn) * scale_log2e);
-      const float mc = mn * scale_log2e;
+      const bool grow = mt * scale_log2e > m[i] * scale_log2e + kLazy;
+      if (__builtin_amdgcn_ballot_w64(grow)) {
+        const float mn = fmaxf(m[i], mt);
+        const float alpha = __builtin_amdgcn_exp2f((m[i] - mn) * scale_log2e);
+        m[i] = mn;
+        l[i] *= alpha;
+#pragma unroll
+        for (int db = 0; db < 4; ++db)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) o[i][db][r] *= alpha;
+      }
+      const float mc = m[i] * scale_log2e;
       float ls = 0.0f;
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
@@ -327,12 +350,7 @@ __global__ __launch_bounds__(256, (G > 4 ? 1 : 2)) void attn_mfma_kernel(
           s[i][kb][r] = p;
           ls += p;
         }
-      l[i] = l[i] * alpha + ls;
-      m[i] = mn;
-#pragma unroll
-      for (int db = 0; db < 4; ++db)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) o[i][db][r] *= alpha;
+      l[i] += ls;
 #pragma unroll
       for (int k2 = 0; k2 < 4; ++k2) {
         const int kb = k2 >> 1, base = 8 * (k2 & 1);
@@ -353,11 +371,28 @@ __global__ __launch_bounds__(256, (G > 4 ? 1 : 2)) void attn_mfma_kernel(
         a.w[0] = lo.x; a.w[1] = lo.y; a.w[2] = hi.x; a.w[3] = hi.y;
 #pragma unroll
         for (int i = 0; i < HPW; ++i)
-          if (wave_active[i])
-            o[i][db] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a.h, pf[i][k2], o[i][db], 0, 0, 0);
+          o[i][db] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a.h, pf[i][k2], o[i][db], 0, 0, 0);
       }
     }
+  };
 
+  const int ntiles = (it.kv_len + kKT - 1) / kKT;
+  // tiles whose last key is <= the smallest row position need no mask
+  const int nfull = min(ntiles, (it.min_pos + 1) / kKT);
+  load_tile(0);
+  store_tile(0);
+  __syncthreads();
+  for (int j = 0; j < nfull; ++j) {
+    const bool more = j + 1 < ntiles;
+    if (more) load_tile(j + 1);
+    tile(j, std::false_type{});
+    if (more) store_tile((j + 1) & 1);
+    __syncthreads();
+  }
+  for (int j = nfull; j < ntiles; ++j) {
+    const bool more = j + 1 < ntiles;
+    if (more) load_tile(j + 1);
+    tile(j, std::true_type{});
     if (more) store_tile((j + 1) & 1);
     __syncthreads();
   }

@@ -25,6 +25,45 @@ namespace {
 
 enum MoveMode { kCompose = 0, kAppend = 1, kRetain = 2 };
 
+// Eight raw storage elements held in registers (16 bytes for bf16, 32 for
+// fp32), loaded non-temporally: every source row is read exactly once.
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+template <typename T> struct Vec8;
+template <> struct Vec8<uint16_t> {
+  u32x4 u;
+  __device__ void load(const uint16_t* p) {
+    u = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+  }
+  __device__ void store(uint16_t* p) const { *reinterpret_cast<u32x4*>(p) = u; }
+  __device__ void to_f32(float* o) const {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      o[2 * i] = bf16_to_f32(u[i] & 0xffffu);
+      o[2 * i + 1] = bf16_to_f32(u[i] >> 16);
+    }
+  }
+};
+template <> struct Vec8<float> {
+  f32x4 a, b;
+  __device__ void load(const float* p) {
+    a = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(p));
+    b = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(p + 4));
+  }
+  __device__ void store(float* p) const {
+    *reinterpret_cast<f32x4*>(p) = a;
+    *reinterpret_cast<f32x4*>(p + 4) = b;
+  }
+  __device__ void to_f32(float* o) const {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      o[i] = a[i];
+      o[4 + i] = b[i];
+    }
+  }
+};
+
 constexpr int kTok = 16;     // descriptors per workgroup
 constexpr int kThreads = 256;
 
@@ -69,28 +108,53 @@ __global__ __launch_bounds__(kThreads) void kv_move_kernel(
     load8(rope_cos + (int64_t)pos * (D / 2) + c * 8, cs);
     load8(rope_sin + (int64_t)pos * (D / 2) + c * 8, sn);
   }
-  for (int h = h0; h < n_kv_heads; h += kHeadStep) {
-    int64_t sb;
+  // Issue the loads of up to kBatch heads before any store so that each
+  // thread keeps several 16-byte requests in flight.
+  constexpr int kBatch = 4;
+  const int lo = c * 8, hi = D / 2 + c * 8;
+  auto src_off = [&](int h) -> int64_t {
     if constexpr (MODE == kCompose)
-      sb = ((((int64_t)(src >> log2_page) * n_kv_heads + h) << log2_page) +
-            (src & page_mask)) * D;
+      return ((((int64_t)(src >> log2_page) * n_kv_heads + h) << log2_page) +
+              (src & page_mask)) * D;
     else
-      sb = ((int64_t)src * n_kv_heads + h) * D;
-    const int64_t db = ((((int64_t)(dst >> log2_page) * n_kv_heads + h) << log2_page) +
-                        (dst & page_mask)) * D;
-    const int lo = c * 8, hi = D / 2 + c * 8;
-    copy8(dst_v + db + lo, src_v + sb + lo);
-    copy8(dst_v + db + hi, src_v + sb + hi);
-    if constexpr (MODE == kRetain) {
-      copy8(dst_k + db + lo, src_k + sb + lo);
-      copy8(dst_k + db + hi, src_k + sb + hi);
-    } else {
-      float a[8], b[8];
-      load8(src_k + sb + lo, a);
-      load8(src_k + sb + hi, b);
-      rope_rotate<8>(a, b, cs, sn);
-      store8(dst_k + db + lo, a);
-      store8(dst_k + db + hi, b);
+      return ((int64_t)src * n_kv_heads + h) * D;
+  };
+  auto dst_off = [&](int h) -> int64_t {
+    return ((((int64_t)(dst >> log2_page) * n_kv_heads + h) << log2_page) +
+            (dst & page_mask)) * D;
+  };
+  for (int hb = h0; hb < n_kv_heads; hb += kBatch * kHeadStep) {
+    Vec8<T> kl[kBatch], kh[kBatch], vl[kBatch], vh[kBatch];
+#pragma unroll
+    for (int b = 0; b < kBatch; ++b) {
+      const int h = hb + b * kHeadStep;
+      if (h < n_kv_heads) {
+        const int64_t sb = src_off(h);
+        kl[b].load(src_k + sb + lo);
+        kh[b].load(src_k + sb + hi);
+        vl[b].load(src_v + sb + lo);
+        vh[b].load(src_v + sb + hi);
+      }
+    }
+#pragma unroll
+    for (int b = 0; b < kBatch; ++b) {
+      const int h = hb + b * kHeadStep;
+      if (h < n_kv_heads) {
+        const int64_t db = dst_off(h);
+        vl[b].store(dst_v + db + lo);
+        vh[b].store(dst_v + db + hi);
+        if constexpr (MODE == kRetain) {
+          kl[b].store(dst_k + db + lo);
+          kh[b].store(dst_k + db + hi);
+        } else {
+          float a[8], bb[8];
+          kl[b].to_f32(a);
+          kh[b].to_f32(bb);
+          rope_rotate<8>(a, bb, cs, sn);
+          store8(dst_k + db + lo, a);
+          store8(dst_k + db + hi, bb);
+        }
+      }
     }
   }
 }
