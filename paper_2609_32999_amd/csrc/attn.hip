@@ -220,15 +220,19 @@ __global__ __launch_bounds__(256, (G > 4 ? 1 : 2)) void attn_mfma_kernel(
   // The tile's 64 keys form four 16-key blocks; with B >= 16 each block lies
   // in one page, so its base address is uniform (scalar block-table loads)
   // and every lane adds a fixed offset.
-  // K: thread owns 16 bytes (8 dims) of key 16*pb + tid/16 of block pb.
-  // V: thread owns 16 bytes of keys 4*(tid/16) + pb, i.e. of block w (its
-  //    wave), so it can write four consecutive keys of each of its 8 dims to
-  //    the transposed V tile.
+  // K: thread owns 16 bytes (dims 8*(tid%16) ..) of key 16*pb + tid/16 of
+  //    block pb; the K tile is stored row-major.
+  // V: thread owns 16 bytes (dims 8*(tid/16) ..) of keys 4*(tid%16) + pb, so
+  //    it writes four consecutive keys of each of its 8 dims to the
+  //    transposed V tile, and the 16 lanes of a group fill one 128-byte row
+  //    segment (no LDS bank conflicts).
   uint4 kr[4], vr[4];
   const int kc8 = (tid & 15) * 8;
+  const int vkg = tid & 15;
+  const int vc8 = (tid >> 4) * 8;
   const int koff = (tid >> 4) * kD + kc8;
-  const int voff = 4 * ((tid >> 4) & 3) * kD + kc8;
-  const int wu = __builtin_amdgcn_readfirstlane(w);
+  const int voff = 4 * (vkg & 3) * kD + vc8;
+  const int vq = vkg >> 2;
   auto load_tile = [&](int j) {
     const int key0 = j * kKT;
     int64_t base[4];
@@ -238,7 +242,7 @@ __global__ __launch_bounds__(256, (G > 4 ? 1 : 2)) void attn_mfma_kernel(
       const int page = bt[min(kq >> log2_page, it.n_pages - 1)];
       base[q] = ((((int64_t)page * n_kv_heads + g) << log2_page) + (kq & page_mask)) * kD;
     }
-    const int64_t vbase = wu == 0 ? base[0] : wu == 1 ? base[1] : wu == 2 ? base[2] : base[3];
+    const int64_t vbase = vq == 0 ? base[0] : vq == 1 ? base[1] : vq == 2 ? base[2] : base[3];
 #pragma unroll
     for (int pb = 0; pb < 4; ++pb) {
       kr[pb] = *reinterpret_cast<const uint4*>(kc + base[pb] + koff);
@@ -249,10 +253,11 @@ __global__ __launch_bounds__(256, (G > 4 ? 1 : 2)) void attn_mfma_kernel(
 #pragma unroll
       for (int pb = 0; pb < 4; ++pb) {
         if (key0 + 16 * pb + (tid >> 4) >= it.kv_len) kr[pb] = make_uint4(0, 0, 0, 0);
-        if (key0 + 4 * (tid >> 4) + pb >= it.kv_len) vr[pb] = make_uint4(0, 0, 0, 0);
+        if (key0 + 4 * vkg + pb >= it.kv_len) vr[pb] = make_uint4(0, 0, 0, 0);
       }
     }
   };
+
   auto store_tile = [&](int buf) {
     uint16_t* ks = smem + buf * kStage;
     uint16_t* vs = ks + kKElems;
@@ -270,7 +275,7 @@ __global__ __launch_bounds__(256, (G > 4 ? 1 : 2)) void attn_mfma_kernel(
       const float f1 = bf16_to_f32((v1[e >> 1] >> sh) & 0xffffu);
       const float f2 = bf16_to_f32((v2[e >> 1] >> sh) & 0xffffu);
       const float f3 = bf16_to_f32((v3[e >> 1] >> sh) & 0xffffu);
-      *reinterpret_cast<uint2*>(vs + (kc8 + e) * kVStr + 4 * (tid >> 4)) =
+      *reinterpret_cast<uint2*>(vs + (vc8 + e) * kVStr + 4 * vkg) =
           make_uint2(pack_f16x2(f0, f1), pack_f16x2(f2, f3));
     }
   };
