@@ -25,6 +25,9 @@ sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBS = 8000.0
 PEAK_MFMA_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
+# e4m3 KV: QK^T runs in fp8 MFMA (5.0 PFLOP/s dense) and PV in fp16 MFMA
+# (2.5 PFLOP/s), half of the FLOPs each: blended peak 1 / (0.5/5.0 + 0.5/2.5).
+PEAK_E4M3_BLEND = 1.0 / (0.5 / 5000.0 + 0.5 / 2500.0)
 
 
 def log(msg):
@@ -173,7 +176,7 @@ def main():
     attn_flops = 4.0 * m.head_dim * m.n_q_heads * visible
     attn_tflops = attn_flops / (attn_ms * 1e-3) / 1e12
     compose_gbs = gather_bytes / (compose_ms * 1e-3) / 1e9
-    peak = PEAK_MFMA_TFLOPS[m.act_dtype]
+    peak = PEAK_E4M3_BLEND if m.kv_dtype == "e4m3" else PEAK_MFMA_TFLOPS[m.act_dtype]
     value = wl.prompt_tokens / (ms * 1e-3)
 
     rec = {
@@ -183,7 +186,8 @@ def main():
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": ms,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": m.act_dtype, "data": "synthetic",
+        "dtype": ("e4m3 KV / bf16 act" if m.kv_dtype == "e4m3" else m.act_dtype),
+        "data": "synthetic",
         "config": {
             "workload": f"{wl.name}: {wl.cfg.description}",
             "requests": len(wl.requests), "prompt_tokens": wl.prompt_tokens,
@@ -198,7 +202,9 @@ def main():
                       "attention": attn_ms * 1e3, "retain_side_stream": retain_ms * 1e3},
         "roofline": {"bound": "mfma", "achieved": attn_tflops, "peak": peak,
                      "unit": "TFLOP/s", "frac": attn_tflops / peak, "traffic": None,
-                     "kernel": "attn_mfma_kernel", "flops_per_launch": attn_flops},
+                     "kernel": ("attn_fp8_kernel" if m.kv_dtype == "e4m3"
+                                else "attn_mfma_kernel"),
+                     "flops_per_launch": attn_flops},
         "roofline_compose": {"bound": "hbm", "achieved": compose_gbs, "peak": PEAK_HBM_GBS,
                              "unit": "GB/s", "frac": compose_gbs / PEAK_HBM_GBS,
                              "bytes_per_launch": gather_bytes},

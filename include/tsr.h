@@ -65,7 +65,13 @@ typedef enum { TSR_F32 = 0, TSR_BF16 = 1, TSR_E4M3 = 2 } tsr_dtype;
 typedef enum { TSR_MISS = 0, TSR_HIT = 1 } tsr_residency;
 
 /* Shape and numerics of one attention layer.
- *   (kv_dtype, act_dtype) in {(F32, F32), (BF16, BF16)}.
+ *   (kv_dtype, act_dtype) in {(F32, F32), (BF16, BF16), (E4M3, BF16)}.
+ *   E4M3 (OCP e4m3fn) pools store codes plus one power-of-two fp32 scale per
+ *   (page, K|V); a value is decode(code) * scale.  Scale arrays are
+ *   [n_pages][2] fp32 ({K, V}) per layer.  An e4m3 plan must be page aligned
+ *   (every request page has one writer: segments start on page boundaries
+ *   and end on one or at the prompt's end; recompute windows are whole
+ *   pages or the whole unit), else tsr_plan_create returns UNSUPPORTED.
  *   RoPE pairs dimension i with i + head_dim/2 at frequency
  *   rope_theta^(-2i/head_dim) (Section 2.2; the variant is a reading).
  *   Positions must be < max_position (the RoPE table's length).
@@ -191,7 +197,10 @@ void tsr_plan_destroy(tsr_plan* plan);
  * fused multiply-add; bf16 results rounded to nearest even.
  *   pool_k/pool_v  device, [n_pool_pages][H_kv][B][d] of kv_dtype.
  *   req_k/req_v    device, [n_req_pages][H_kv][B][d] of kv_dtype.
- *   pool_scale, req_scale  reserved for scaled 8-bit pools; pass NULL.
+ *   pool_scale, req_scale  e4m3 only (else NULL): [n_layers][pages][2] fp32.
+ *   e4m3: V codes and V scale are copied; K is dequantized, rotated in fp32
+ *   and requantized with the smallest power-of-two scale s such that
+ *   max |K| / s <= 448 over the request page (nearest even, saturating).
  *   n_layers >= 1 composes that many layers in one launch; layer l uses the
  *   buffers offset by l * pool_layer_stride / req_layer_stride bytes. */
 tsr_status tsr_compose_kv(const tsr_plan* plan, const void* pool_k,
@@ -211,7 +220,10 @@ tsr_status tsr_compose_kv(const tsr_plan* plan, const void* pool_k,
  *   lse  device [T][H_q] fp32 natural-log sum of exp(scale * s), or NULL.
  * Must run after tsr_compose_kv of the same plan and layer (stream order).
  * bf16: QK^T in bf16 MFMA with fp32 accumulation; probabilities and values
- * enter the PV product as fp16 (|v| must stay below 65504). */
+ * enter the PV product as fp16 (|v| must stay below 65504).
+ * e4m3: computed pages are quantized like composed ones (k after rotation);
+ * q_rot is quantized per (row, head) to e4m3 with the smallest power-of-two
+ * scale covering the row, QK^T runs in fp8 MFMA, PV in fp16 MFMA. */
 tsr_status tsr_prefill_attn(const tsr_plan* plan, const void* q,
                             const void* k, const void* v, void* req_k,
                             void* req_v, float* req_scale, void* out,
@@ -233,7 +245,8 @@ tsr_status tsr_attn(const tsr_plan* plan, const void* q, const void* req_k,
 
 /* Retain (Section 5.4): for every MISS unit with retain = 1 and token j:
  *   K_pool[block j/B][slot j%B] = k (before RoPE), V_pool[...] = v
- * as bit copies from the computed rows.  Slots of a unit's last block
+ * as bit copies from the computed rows (e4m3: quantized per pool page, both
+ * scales written).  Slots of a unit's last block
  * beyond n are left untouched.  k/v are the same inputs as
  * tsr_prefill_attn's and must stay alive until the stream reaches this work
  * (Section 5.4: sources stay valid until their copies complete).  A caller

@@ -117,3 +117,124 @@ def retained_pages(wl):
             pv[:, slot] = vr
             filled[slot] = True
     return out
+
+
+# ------------------------------------------------------------------ e4m3 pool
+# Readings (the paper has no 8-bit path): the pool holds e4m3 codes with one
+# power-of-two fp32 scale per (page, K|V); a value is decode(code) * scale.
+# Request pages use the same format.  Every request page has one writer:
+#   gathered page   V codes and scale copied; K dequantized, rotated to the
+#                   new positions in fp32 (rope_fp32), and requantized with a
+#                   fresh page scale (rotation can grow |x| by up to sqrt(2));
+#   computed page   fresh k rotated in fp32 and v, each quantized per page;
+# retention quantizes the unit's pre-RoPE k and v per pool page.  The page
+# scale is the smallest power of two s with amax / s <= 448 over the page's
+# valid tokens (all heads and dims); codes are nearest-even, saturating.
+
+def quantize_page(x):
+    """x [n][H][d] fp32 -> (codes uint8, scale fp32) with one page scale."""
+    from .numerics import e4m3_encode, e4m3_page_scale
+    x = np.asarray(x, dtype=np.float32)
+    amax = float(np.abs(x).max()) if x.size else 0.0
+    scale = np.float32(e4m3_page_scale(np.array([amax]))[0])
+    return e4m3_encode(x / scale), scale
+
+
+def dequantize(codes, scale):
+    from .numerics import e4m3_decode
+    return e4m3_decode(codes) * np.float32(scale)
+
+
+def check_page_aligned(req, page_size: int) -> None:
+    """Raise ValueError unless every request page has a single writer."""
+    B = page_size
+    for kind, s, n, u in L.segments(req):
+        end = s + n
+        if s % B or (end % B and end != req.prompt_len):
+            raise ValueError(f"segment [{s}, {end}) is not page aligned")
+        if u is not None and u.residency == L.HIT:
+            r = L.recompute_count(u)
+            if r % B and r != n:
+                raise ValueError("recompute window is not page aligned")
+
+
+def assemble_request_kv_e4m3(wl, r: int):
+    """Request r's pages: per position K codes, V codes ([P][H][d] uint8) and
+    the page scale of each position's page (k_scale[P], v_scale[P])."""
+    m = wl.model
+    B = m.page_size
+    req = wl.requests[r]
+    L.check_tiling(req)
+    check_page_aligned(req, B)
+    P = req.prompt_len
+    Kc = np.zeros((P, m.n_kv_heads, m.head_dim), dtype=np.uint8)
+    Vc = np.zeros_like(Kc)
+    ks = np.zeros(P, dtype=np.float32)
+    vs = np.zeros(P, dtype=np.float32)
+    cpos = L.compute_positions(req)
+    _, kf, vf = wl.fresh(r, cpos) if cpos.size else (None, None, None)
+    row_of = {int(p): i for i, p in enumerate(cpos)}
+    cache = {}
+    for pg in range(-(-P // B)):
+        p0, p1 = pg * B, min(P, (pg + 1) * B)
+        pos = np.arange(p0, p1)
+        if p0 in row_of:           # computed page
+            rows = np.array([row_of[int(p)] for p in pos])
+            kc, ksc = quantize_page(rope_fp32(kf[rows], pos, m.rope_theta))
+            vc, vsc = quantize_page(vf[rows])
+        else:                      # gathered page of a HIT unit
+            u = next(u for u in req.units if u.position <= p0 < u.position + u.n_tokens)
+            if u.unit_id not in cache:
+                cache[u.unit_id] = wl.unit_state_e4m3(u.unit_id)
+            kcodes, vcodes, kscale, vscale = cache[u.unit_id]
+            j0 = p0 - u.position
+            src = j0 // B
+            j = np.arange(j0, j0 + (p1 - p0))
+            kx = dequantize(kcodes[j], kscale[src])
+            kc, ksc = quantize_page(rope_fp32(kx, pos, m.rope_theta))
+            vc, vsc = vcodes[j], vscale[src]
+        Kc[p0:p1], Vc[p0:p1], ks[p0:p1], vs[p0:p1] = kc, vc, ksc, vsc
+    return Kc, Vc, ks, vs
+
+
+def quantized_queries_e4m3(wl, r: int, q_heads=None):
+    """Rotated fresh queries quantized per (row, head) with a power-of-two
+    scale, as the fp8 attention consumes them (a kernel choice mirrored
+    here).  Returns (positions, dequantized q [T][h][d] fp32)."""
+    from .numerics import e4m3_decode, e4m3_encode, e4m3_page_scale
+    m = wl.model
+    cpos = L.compute_positions(wl.requests[r])
+    q, _, _ = wl.fresh(r, cpos)
+    if q_heads is not None:
+        q = q[:, np.asarray(q_heads)]
+    qr = rope_fp32(q, cpos, m.rope_theta)
+    amax = np.abs(qr).max(axis=-1)                     # [T][h]
+    sc = e4m3_page_scale(amax.ravel()).reshape(amax.shape)
+    codes = e4m3_encode(qr / sc[..., None])
+    return cpos, e4m3_decode(codes) * sc[..., None]
+
+
+def retained_pages_e4m3(wl):
+    """Pool blocks written by retention in the e4m3 pool:
+    {page: (k_codes [H][B][d], v_codes, k_scale, v_scale, filled[B])}."""
+    m = wl.model
+    B = m.page_size
+    out = {}
+    for r, req in enumerate(wl.requests):
+        for u in req.units:
+            if u.residency != L.MISS or not u.retain:
+                continue
+            pos = np.arange(u.position, u.position + u.n_tokens)
+            _, k, v = wl.fresh(r, pos)
+            for pi, page in enumerate(u.pool_pages):
+                j = np.arange(pi * B, min(u.n_tokens, (pi + 1) * B))
+                kc, ksc = quantize_page(k[j])
+                vc, vsc = quantize_page(v[j])
+                kp = np.zeros((m.n_kv_heads, B, m.head_dim), np.uint8)
+                vp = np.zeros_like(kp)
+                filled = np.zeros(B, dtype=bool)
+                kp[:, :len(j)] = kc.transpose(1, 0, 2)
+                vp[:, :len(j)] = vc.transpose(1, 0, 2)
+                filled[:len(j)] = True
+                out[int(page)] = (kp, vp, ksc, vsc, filled)
+    return out

@@ -16,7 +16,9 @@ import numpy as np
 
 from . import layout as L
 from .attention import causal_gqa_attention
-from .compose import assemble_request_kv, retained_pages, round_storage, rotated_queries
+from .compose import (assemble_request_kv, assemble_request_kv_e4m3, dequantize,
+                      quantized_queries_e4m3, retained_pages, round_storage,
+                      rotated_queries)
 from .rope import rope_fp32
 
 
@@ -38,17 +40,26 @@ def run_request(wl, r: int, kv_heads=None, scale=None) -> RequestResult:
     G = m.n_q_heads // m.n_kv_heads
     kvh = np.arange(m.n_kv_heads) if kv_heads is None else np.asarray(kv_heads)
     qh = np.concatenate([np.arange(g * G, (g + 1) * G) for g in kvh])
-    K, V, src = assemble_request_kv(wl, r, kvh)
-    cpos, q = rotated_queries(wl, r, qh)
+    if m.kv_dtype == "e4m3":
+        Kc, Vc, ks, vs = assemble_request_kv_e4m3(wl, r)
+        K = (dequantize(Kc, 1.0) * ks[:, None, None])[:, kvh]
+        V = (dequantize(Vc, 1.0) * vs[:, None, None])[:, kvh]
+        src = None
+        cpos, q = quantized_queries_e4m3(wl, r, qh)
+    else:
+        K, V, src = assemble_request_kv(wl, r, kvh)
+        cpos, q = rotated_queries(wl, r, qh)
     out, lse = causal_gqa_attention(q, cpos, K, V, scale=scale)
     return RequestResult(cpos, K, V, src, q, out, lse, kvh, qh)
 
 
 def run(wl, requests=None, kv_heads=None, scale=None):
     """Oracle results per request (list), and the retained pool pages."""
+    from .compose import retained_pages_e4m3
     reqs = range(len(wl.requests)) if requests is None else requests
     results = {r: run_request(wl, r, kv_heads, scale) for r in reqs}
-    return results, retained_pages(wl)
+    kept = retained_pages_e4m3(wl) if wl.model.kv_dtype == "e4m3" else retained_pages(wl)
+    return results, kept
 
 
 def full_prefill(wl, r: int, scale=None):

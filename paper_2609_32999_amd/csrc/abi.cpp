@@ -33,9 +33,20 @@ tsr_status check_exec(const tsr_plan* p) {
   return TSR_OK;
 }
 
-tsr_status check_scales(const tsr_plan* p, const float* a, const float* b) {
-  if (p->model.kv_dtype != TSR_E4M3 && (a || b)) {
-    set_error("scale arrays apply to e4m3 pools only; pass NULL");
+bool is_e4m3(const tsr_plan* p) { return p->model.kv_dtype == TSR_E4M3; }
+
+// e4m3 plans need every scale array the call touches; other plans take none.
+tsr_status check_scales(const tsr_plan* p, const float* a, const float* b,
+                        bool need_a, bool need_b) {
+  if (!is_e4m3(p)) {
+    if (a || b) {
+      set_error("scale arrays apply to e4m3 pools only; pass NULL");
+      return TSR_ERR_INVALID_ARG;
+    }
+    return TSR_OK;
+  }
+  if ((need_a && !a) || (need_b && !b)) {
+    set_error("e4m3 pools need their page-scale arrays");
     return TSR_ERR_INVALID_ARG;
   }
   return TSR_OK;
@@ -164,6 +175,9 @@ tsr_status tsr_plan_create(const tsr_model* model, const tsr_request* reqs,
       p->dev.retain = reinterpret_cast<const RetainDesc*>(base + p->off_retain);
       p->dev.items = reinterpret_cast<const AttnItem*>(base + p->off_items);
       p->dev.block_tables = reinterpret_cast<const int32_t*>(base + p->off_bt);
+      p->dev.gpages = reinterpret_cast<const PageDesc*>(base + p->off_gpages);
+      p->dev.apages = reinterpret_cast<const PageDesc*>(base + p->off_apages);
+      p->dev.rpages = reinterpret_cast<const PageDesc*>(base + p->off_rpages);
       p->dev.rope_cos = table;
       p->dev.rope_sin = table + half;
     }
@@ -201,7 +215,7 @@ tsr_status tsr_compose_kv(const tsr_plan* p, const void* pool_k,
   return guarded([&]() -> tsr_status {
     tsr_status st = check_exec(p);
     if (st != TSR_OK) return st;
-    if ((st = check_scales(p, pool_scale, req_scale)) != TSR_OK) return st;
+    if ((st = check_scales(p, pool_scale, req_scale, true, true)) != TSR_OK) return st;
     if (n_layers < 1 || n_layers > 65535) {
       set_error("n_layers must be in [1, 65535]");
       return TSR_ERR_INVALID_ARG;
@@ -210,7 +224,7 @@ tsr_status tsr_compose_kv(const tsr_plan* p, const void* pool_k,
       set_error("layer strides must be positive when n_layers > 1");
       return TSR_ERR_INVALID_ARG;
     }
-    const int64_t elem = p->model.kv_dtype == TSR_F32 ? 4 : 2;
+    const int64_t elem = p->model.kv_dtype == TSR_F32 ? 4 : is_e4m3(p) ? 1 : 2;
     if (pool_layer_stride % (16 * elem) || req_layer_stride % (16 * elem)) {
       set_error("layer strides must be multiples of 16 elements");
       return TSR_ERR_INVALID_ARG;
@@ -220,9 +234,14 @@ tsr_status tsr_compose_kv(const tsr_plan* p, const void* pool_k,
       set_error("compose: a KV pointer is NULL");
       return TSR_ERR_INVALID_ARG;
     }
-    hipError_t e = launch_compose(p, pool_k, pool_v, req_k, req_v, n_layers,
-                                  pool_layer_stride, req_layer_stride,
-                                  static_cast<hipStream_t>(stream));
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    hipError_t e =
+        is_e4m3(p)
+            ? launch_compose_e4m3(p, pool_k, pool_v, pool_scale, req_k, req_v, req_scale,
+                                  n_layers, pool_layer_stride, req_layer_stride,
+                                  2 * (int64_t)p->n_pool_pages, 2 * (int64_t)p->n_req_pages, s)
+            : launch_compose(p, pool_k, pool_v, req_k, req_v, n_layers, pool_layer_stride,
+                             req_layer_stride, s);
     if (e != hipSuccess) return device_fail("compose launch", e);
     return TSR_OK;
   });
@@ -235,16 +254,18 @@ tsr_status tsr_prefill_attn(const tsr_plan* p, const void* q, const void* k,
   return guarded([&]() -> tsr_status {
     tsr_status st = check_exec(p);
     if (st != TSR_OK) return st;
-    if ((st = check_scales(p, nullptr, req_scale)) != TSR_OK) return st;
+    if ((st = check_scales(p, nullptr, req_scale, false, true)) != TSR_OK) return st;
     if (p->T == 0) return TSR_OK;
     if (!q || !k || !v || !req_k || !req_v || !out) {
       set_error("prefill_attn: a required pointer is NULL");
       return TSR_ERR_INVALID_ARG;
     }
     hipStream_t s = static_cast<hipStream_t>(stream);
-    hipError_t e = launch_append(p, k, v, req_k, req_v, s);
+    hipError_t e = is_e4m3(p) ? launch_append_e4m3(p, k, v, req_k, req_v, req_scale, s)
+                              : launch_append(p, k, v, req_k, req_v, s);
     if (e != hipSuccess) return device_fail("append launch", e);
-    e = launch_attn(p, q, req_k, req_v, out, lse, s);
+    e = is_e4m3(p) ? launch_attn_e4m3(p, q, req_k, req_v, req_scale, out, lse, s)
+                   : launch_attn(p, q, req_k, req_v, out, lse, s);
     if (e != hipSuccess) return device_fail("attention launch", e);
     return TSR_OK;
   });
@@ -256,13 +277,15 @@ tsr_status tsr_append_kv(const tsr_plan* p, const void* k, const void* v,
   return guarded([&]() -> tsr_status {
     tsr_status st = check_exec(p);
     if (st != TSR_OK) return st;
-    if ((st = check_scales(p, nullptr, req_scale)) != TSR_OK) return st;
+    if ((st = check_scales(p, nullptr, req_scale, false, true)) != TSR_OK) return st;
     if (p->T == 0) return TSR_OK;
     if (!k || !v || !req_k || !req_v) {
       set_error("append_kv: a required pointer is NULL");
       return TSR_ERR_INVALID_ARG;
     }
-    hipError_t e = launch_append(p, k, v, req_k, req_v, static_cast<hipStream_t>(stream));
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    hipError_t e = is_e4m3(p) ? launch_append_e4m3(p, k, v, req_k, req_v, req_scale, s)
+                              : launch_append(p, k, v, req_k, req_v, s);
     if (e != hipSuccess) return device_fail("append launch", e);
     return TSR_OK;
   });
@@ -274,13 +297,15 @@ tsr_status tsr_attn(const tsr_plan* p, const void* q, const void* req_k,
   return guarded([&]() -> tsr_status {
     tsr_status st = check_exec(p);
     if (st != TSR_OK) return st;
-    if ((st = check_scales(p, nullptr, req_scale)) != TSR_OK) return st;
+    if ((st = check_scales(p, nullptr, req_scale, false, true)) != TSR_OK) return st;
     if (p->T == 0) return TSR_OK;
     if (!q || !req_k || !req_v || !out) {
       set_error("attn: a required pointer is NULL");
       return TSR_ERR_INVALID_ARG;
     }
-    hipError_t e = launch_attn(p, q, req_k, req_v, out, lse, static_cast<hipStream_t>(stream));
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    hipError_t e = is_e4m3(p) ? launch_attn_e4m3(p, q, req_k, req_v, req_scale, out, lse, s)
+                              : launch_attn(p, q, req_k, req_v, out, lse, s);
     if (e != hipSuccess) return device_fail("attention launch", e);
     return TSR_OK;
   });
@@ -292,13 +317,15 @@ tsr_status tsr_retain_kv(const tsr_plan* p, const void* k, const void* v,
   return guarded([&]() -> tsr_status {
     tsr_status st = check_exec(p);
     if (st != TSR_OK) return st;
-    if ((st = check_scales(p, nullptr, pool_scale)) != TSR_OK) return st;
+    if ((st = check_scales(p, nullptr, pool_scale, false, true)) != TSR_OK) return st;
     if (p->n_retain == 0) return TSR_OK;
     if (!k || !v || !pool_k || !pool_v) {
       set_error("retain: a required pointer is NULL");
       return TSR_ERR_INVALID_ARG;
     }
-    hipError_t e = launch_retain(p, k, v, pool_k, pool_v, static_cast<hipStream_t>(stream));
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    hipError_t e = is_e4m3(p) ? launch_retain_e4m3(p, k, v, pool_k, pool_v, pool_scale, s)
+                              : launch_retain(p, k, v, pool_k, pool_v, s);
     if (e != hipSuccess) return device_fail("retain launch", e);
     return TSR_OK;
   });

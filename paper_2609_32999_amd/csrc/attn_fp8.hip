@@ -1,0 +1,389 @@
+// Causal GQA prefill attention over an e4m3 request KV (codes + one
+// power-of-two scale per (page, K|V)).  Same work decomposition, tile
+// schedule and online softmax as the bf16 kernel (attn.hip); what differs:
+//
+//   * rotated queries are quantized to e4m3 per (row, head) with the
+//     smallest power-of-two scale covering the row (a kernel choice that the
+//     CPU oracle mirrors exactly);
+//   * S^T = K Q^T runs on the codes with v_mfma_scale_f32_32x32x64_f8f6f4
+//     (unit block scales); the row's Q scale and each key's page scale are
+//     applied to S afterwards (per lane: one row, four pages per tile);
+//   * V codes are dequantized to fp16 (exact for e4m3 values times a
+//     power-of-two scale inside fp16 range) while being transposed into LDS,
+//     and P V runs in fp16 MFMA as in the bf16 kernel, so P keeps fp16
+//     precision (e4m3 P would cost several percent of relative error).
+#include <cmath>
+#include <type_traits>
+
+#include "kernels_common.h"
+#include "tsr_internal.h"
+
+namespace tsr {
+
+namespace {
+
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef int i32x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+
+union Frag8 {
+  uint4 u;
+  uint32_t w[4];
+  f16x8 h;
+};
+
+constexpr int kD = 128;
+constexpr int kKT = kKvTile;           // keys per tile
+constexpr int kKStr = kD + 16;         // bytes per e4m3 K row in LDS
+constexpr int kVStr = kKT + 4;         // fp16 elements per V^T row in LDS
+constexpr int kKBytes = kKT * kKStr;
+constexpr int kVElems = kD * kVStr;
+constexpr float kLazy = 8.0f;          // lazy-rescale threshold (log2 units)
+
+__device__ __forceinline__ int page_scale_exp(float amax) {
+  if (!(amax > 0.0f)) return 0;
+  int e;
+  const float mfr = frexpf(amax, &e);
+  return mfr <= 0.875f ? e - 9 : e - 8;
+}
+
+template <int G>
+__global__ __launch_bounds__(256, (G > 4 ? 1 : 2)) void attn_fp8_kernel(
+    const uint16_t* __restrict__ q, const uint8_t* __restrict__ kc,
+    const uint8_t* __restrict__ vc, const float* __restrict__ scales,
+    const AttnItem* __restrict__ items, const int32_t* __restrict__ bts,
+    const RowDesc* __restrict__ rows, const float* __restrict__ rope_cos,
+    const float* __restrict__ rope_sin, uint16_t* __restrict__ out,
+    float* __restrict__ lse, int n_q_heads, int n_kv_heads, int log2_page,
+    float scale_log2e) {
+  constexpr int HPW = (G + 3) / 4;
+  __shared__ __attribute__((aligned(16))) uint8_t kmem[2][kKBytes];
+  __shared__ __attribute__((aligned(16))) uint16_t vmem[2][kVElems];
+
+  const AttnItem it = items[blockIdx.x];
+  if (it.n_rows == 0) return;
+  const int tid = threadIdx.x;
+  const int w = tid >> 6;
+  const int lane = tid & 63;
+  const int lrow = lane & 31;
+  const int lh = lane >> 5;
+  const int g = it.kv_head;
+  const int page_mask = (1 << log2_page) - 1;
+  const int32_t* bt = bts + it.bt_off;
+  const int row = it.row0 + min(lrow, it.n_rows - 1);
+  const int pos = rows[row].pos;
+
+  // ---- queries: rotate in fp32, quantize per (row, head) to e4m3.  Lane
+  // half lh holds dims [32 lh, 32 lh + 32) of both RoPE halves, i.e. the
+  // B operands of the two 64-deep k steps.
+  i32x8 qf[HPW][2];
+  float qs[HPW];
+#pragma unroll
+  for (int i = 0; i < HPW; ++i) {
+    const int hl = min(w + 4 * i, G - 1);
+    const uint16_t* qp = q + ((int64_t)row * n_q_heads + g * G + hl) * kD;
+    float lo[32], hi[32];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int d0 = 32 * lh + 8 * c;
+      float cs[8], sn[8];
+      load8(qp + d0, lo + 8 * c);
+      load8(qp + d0 + kD / 2, hi + 8 * c);
+      load8(rope_cos + (int64_t)pos * (kD / 2) + d0, cs);
+      load8(rope_sin + (int64_t)pos * (kD / 2) + d0, sn);
+      rope_rotate<8>(lo + 8 * c, hi + 8 * c, cs, sn);
+    }
+    float amax = 0.0f;
+#pragma unroll
+    for (int e = 0; e < 32; ++e) amax = fmaxf(amax, fmaxf(fabsf(lo[e]), fabsf(hi[e])));
+    amax = fmaxf(amax, __shfl_xor(amax, 32));
+    const int ek = page_scale_exp(amax);
+    qs[i] = ldexpf(1.0f, ek);
+#pragma unroll
+    for (int half = 0; half < 2; ++half) {
+      const float* x = half ? hi : lo;
+#pragma unroll
+      for (int wd = 0; wd < 8; ++wd) {
+        float a[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          a[e] = fminf(fmaxf(ldexpf(x[4 * wd + e], -ek), -448.0f), 448.0f);
+        int p = __builtin_amdgcn_cvt_pk_fp8_f32(a[0], a[1], 0, false);
+        p = __builtin_amdgcn_cvt_pk_fp8_f32(a[2], a[3], p, true);
+        qf[i][half][wd] = p;
+      }
+    }
+  }
+
+  f32x16 o[HPW][4];
+  float m[HPW], l[HPW];
+#pragma unroll
+  for (int i = 0; i < HPW; ++i) {
+    m[i] = -INFINITY;
+    l[i] = 0.0f;
+#pragma unroll
+    for (int db = 0; db < 4; ++db)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) o[i][db][r] = 0.0f;
+  }
+  bool wave_active[HPW];
+#pragma unroll
+  for (int i = 0; i < HPW; ++i) wave_active[i] = (w + 4 * i) < G;
+
+  // ---- global -> register staging.  16-key blocks of a tile lie in one page.
+  // K: two 16-byte chunks per thread; chunk c covers block c/128, key
+  //    (c/8)%16 of the block, dims 16*(c%8) ..
+  // V: keys 4*(tid%16) .. +3, dims 8*(tid/16) .. +7 (8 bytes per key).
+  uint4 kr[2];
+  uint2 vr[4];
+  const int vkg = tid & 15;
+  const int vc8 = (tid >> 4) * 8;
+  const int vq = vkg >> 2;
+  float nks[4], nvs[4];   // page scales of the staged tile (uniform)
+  float tks[4];           // K page scales of the tile being computed
+  auto load_tile = [&](int j) {
+    const int key0 = j * kKT;
+    int64_t base[4];
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+      const int kq = key0 + 16 * b;
+      const int page = bt[min(kq >> log2_page, it.n_pages - 1)];
+      base[b] = ((((int64_t)page * n_kv_heads + g) << log2_page) + (kq & page_mask)) * kD;
+      nks[b] = scales[2 * page];
+      nvs[b] = scales[2 * page + 1];
+    }
+#pragma unroll
+    for (int h2 = 0; h2 < 2; ++h2) {
+      const int c = tid + 256 * h2;
+      const int64_t bb = h2 == 0 ? ((tid >> 7) ? base[1] : base[0])
+                                 : ((tid >> 7) ? base[3] : base[2]);
+      kr[h2] = *reinterpret_cast<const uint4*>(kc + bb + ((c >> 3) & 15) * kD + (c & 7) * 16);
+    }
+    const int64_t vb = vq == 0 ? base[0] : vq == 1 ? base[1] : vq == 2 ? base[2] : base[3];
+#pragma unroll
+    for (int pb = 0; pb < 4; ++pb)
+      vr[pb] = *reinterpret_cast<const uint2*>(vc + vb + (4 * (vkg & 3) + pb) * kD + vc8);
+    if (key0 + kKT > it.kv_len) {  // last, partial tile
+#pragma unroll
+      for (int h2 = 0; h2 < 2; ++h2) {
+        const int c = tid + 256 * h2;
+        if (key0 + 16 * (c >> 7) + ((c >> 3) & 15) >= it.kv_len) kr[h2] = make_uint4(0, 0, 0, 0);
+      }
+#pragma unroll
+      for (int pb = 0; pb < 4; ++pb)
+        if (key0 + 4 * vkg + pb >= it.kv_len) vr[pb] = make_uint2(0, 0);
+    }
+  };
+  auto store_tile = [&](int buf) {
+#pragma unroll
+    for (int h2 = 0; h2 < 2; ++h2) {
+      const int c = tid + 256 * h2;
+      const int key = 16 * (c >> 7) + ((c >> 3) & 15);
+      *reinterpret_cast<uint4*>(&kmem[buf][key * kKStr + (c & 7) * 16]) = kr[h2];
+    }
+    // V^T[d][key] in fp16: gather byte e of keys (k0, k1) and (k2, k3) into
+    // one word each and convert two codes at a time with the page scale.
+    const float s = vq == 0 ? nvs[0] : vq == 1 ? nvs[1] : vq == 2 ? nvs[2] : nvs[3];
+    uint16_t* vs = vmem[buf];
+#pragma unroll
+    for (int half = 0; half < 2; ++half) {
+      const uint32_t a0 = half ? vr[0].y : vr[0].x, a1 = half ? vr[1].y : vr[1].x;
+      const uint32_t a2 = half ? vr[2].y : vr[2].x, a3 = half ? vr[3].y : vr[3].x;
+#pragma unroll
+      for (int e2 = 0; e2 < 2; ++e2) {
+        // bytes (k0[e], k1[e], k0[e+1], k1[e+1]) for e = 2*e2 within the word
+        const uint32_t sel = e2 ? 0x07030602u : 0x05010400u;
+        const uint32_t p01 = __builtin_amdgcn_perm(a1, a0, sel);
+        const uint32_t p23 = __builtin_amdgcn_perm(a3, a2, sel);
+        // low word: keys (0,1) / (2,3) at dim e; high word: at dim e + 1
+        const f16x2 l01 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(p01, s, false);
+        const f16x2 l23 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(p23, s, false);
+        const f16x2 h01 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(p01, s, true);
+        const f16x2 h23 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(p23, s, true);
+        const int d = vc8 + 4 * half + 2 * e2;
+        *reinterpret_cast<uint2*>(vs + d * kVStr + 4 * vkg) =
+            make_uint2(__builtin_bit_cast(uint32_t, l01), __builtin_bit_cast(uint32_t, l23));
+        *reinterpret_cast<uint2*>(vs + (d + 1) * kVStr + 4 * vkg) =
+            make_uint2(__builtin_bit_cast(uint32_t, h01), __builtin_bit_cast(uint32_t, h23));
+      }
+    }
+  };
+
+  auto tile = [&](int j, auto mask_tag) {
+    constexpr bool MASK = decltype(mask_tag)::value;
+    const uint8_t* ks = kmem[j & 1];
+    const uint16_t* vs = vmem[j & 1];
+    f32x16 s[HPW][2];
+#pragma unroll
+    for (int i = 0; i < HPW; ++i)
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) s[i][kb][r] = 0.0f;
+#pragma unroll
+    for (int kst = 0; kst < 2; ++kst) {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+        const uint8_t* kp = ks + (32 * kb + lrow) * kKStr + 64 * kst + 32 * lh;
+        const uint4 x0 = *reinterpret_cast<const uint4*>(kp);
+        const uint4 x1 = *reinterpret_cast<const uint4*>(kp + 16);
+        const i32x8 a = {(int)x0.x, (int)x0.y, (int)x0.z, (int)x0.w,
+                         (int)x1.x, (int)x1.y, (int)x1.z, (int)x1.w};
+#pragma unroll
+        for (int i = 0; i < HPW; ++i)
+          s[i][kb] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
+              a, qf[i][kst], s[i][kb], 0, 0, 0, 127, 0, 127);
+      }
+    }
+    // page of S register r of key block kb: 2*kb + r/8 within the tile
+    f16x8 pf[HPW][4];
+#pragma unroll
+    for (int i = 0; i < HPW; ++i) {
+      float f[4];
+#pragma unroll
+      for (int b = 0; b < 4; ++b) f[b] = qs[i] * tks[b] * scale_log2e;
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) s[i][kb][r] *= f[2 * kb + (r >> 3)];
+      if constexpr (MASK) {
+        const int kbase = j * kKT;
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int key = kbase + 32 * kb + 8 * (r >> 2) + 4 * lh + (r & 3);
+            s[i][kb][r] = key > pos ? -INFINITY : s[i][kb][r];
+          }
+      }
+      float mt = -INFINITY;
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) mt = fmaxf(mt, s[i][kb][r]);
+      mt = fmaxf(mt, __shfl_xor(mt, 32));
+      // scores are in log2 units here; see attn.hip for the lazy rescale
+      if (__builtin_amdgcn_ballot_w64(mt > m[i] + kLazy)) {
+        const float mn = fmaxf(m[i], mt);
+        const float alpha = __builtin_amdgcn_exp2f(m[i] - mn);
+        m[i] = mn;
+        l[i] *= alpha;
+#pragma unroll
+        for (int db = 0; db < 4; ++db)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) o[i][db][r] *= alpha;
+      }
+      float ls = 0.0f;
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const float p = __builtin_amdgcn_exp2f(s[i][kb][r] - m[i]);
+          s[i][kb][r] = p;
+          ls += p;
+        }
+      l[i] += ls;
+#pragma unroll
+      for (int k2 = 0; k2 < 4; ++k2) {
+        const int kb = k2 >> 1, base = 8 * (k2 & 1);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) pf[i][k2][e] = (_Float16)s[i][kb][base + e];
+      }
+    }
+#pragma unroll
+    for (int k2 = 0; k2 < 4; ++k2) {
+#pragma unroll
+      for (int db = 0; db < 4; ++db) {
+        const uint16_t* vp = vs + (32 * db + lrow) * kVStr + 16 * k2 + 4 * lh;
+        Frag8 a;
+        const uint2 lo = *reinterpret_cast<const uint2*>(vp);
+        const uint2 hi = *reinterpret_cast<const uint2*>(vp + 8);
+        a.w[0] = lo.x; a.w[1] = lo.y; a.w[2] = hi.x; a.w[3] = hi.y;
+#pragma unroll
+        for (int i = 0; i < HPW; ++i)
+          o[i][db] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a.h, pf[i][k2], o[i][db], 0, 0, 0);
+      }
+    }
+  };
+
+  const int ntiles = (it.kv_len + kKT - 1) / kKT;
+  const int nfull = min(ntiles, (it.min_pos + 1) / kKT);
+  load_tile(0);
+  store_tile(0);
+#pragma unroll
+  for (int b = 0; b < 4; ++b) tks[b] = nks[b];
+  __syncthreads();
+  for (int j = 0; j < ntiles; ++j) {
+    const bool more = j + 1 < ntiles;
+    if (more) load_tile(j + 1);
+    if (j < nfull)
+      tile(j, std::false_type{});
+    else
+      tile(j, std::true_type{});
+    if (more) store_tile((j + 1) & 1);
+#pragma unroll
+    for (int b = 0; b < 4; ++b) tks[b] = nks[b];
+    __syncthreads();
+  }
+
+  // ---- epilogue
+#pragma unroll
+  for (int i = 0; i < HPW; ++i) {
+    if (!wave_active[i]) continue;
+    const float lt = l[i] + __shfl_xor(l[i], 32);
+    if (lrow >= it.n_rows) continue;
+    const float inv = 1.0f / lt;
+    const int hq = g * G + w + 4 * i;
+    uint16_t* op = out + ((int64_t)row * n_q_heads + hq) * kD;
+#pragma unroll
+    for (int db = 0; db < 4; ++db)
+#pragma unroll
+      for (int rg = 0; rg < 4; ++rg) {
+        const int d0 = 32 * db + 8 * rg + 4 * lh;
+        uint2 v;
+        v.x = f32_to_bf16(o[i][db][4 * rg] * inv) | (f32_to_bf16(o[i][db][4 * rg + 1] * inv) << 16);
+        v.y = f32_to_bf16(o[i][db][4 * rg + 2] * inv) | (f32_to_bf16(o[i][db][4 * rg + 3] * inv) << 16);
+        *reinterpret_cast<uint2*>(op + d0) = v;
+      }
+    // lse (natural log) = (m + log2 l) * ln 2 with m in log2 units
+    if (lse && lh == 0)
+      lse[(int64_t)row * n_q_heads + hq] = (m[i] + log2f(lt)) * 0.69314718055994531f;
+  }
+}
+
+int ilog2(int x) {
+  int l = 0;
+  while ((1 << l) < x) ++l;
+  return l;
+}
+
+}  // namespace
+
+hipError_t launch_attn_e4m3(const tsr_plan* p, const void* q, const void* req_k,
+                            const void* req_v, const float* req_scale, void* out,
+                            float* lse, hipStream_t s) {
+  if (p->n_items == 0 || p->T == 0) return hipSuccess;
+  const tsr_model& m = p->model;
+  const int lp = ilog2(m.page_size);
+  const int G = m.n_q_heads / m.n_kv_heads;
+  const float sl2e = (float)((double)p->scale * 1.4426950408889634);
+#define TSR_FP8(GG)                                                                   \
+  hipLaunchKernelGGL(attn_fp8_kernel<GG>, dim3(p->n_items), dim3(256), 0, s,          \
+                     static_cast<const uint16_t*>(q), static_cast<const uint8_t*>(req_k), \
+                     static_cast<const uint8_t*>(req_v), req_scale, p->dev.items,     \
+                     p->dev.block_tables, p->dev.rows, p->dev.rope_cos,               \
+                     p->dev.rope_sin, static_cast<uint16_t*>(out), lse, m.n_q_heads,  \
+                     m.n_kv_heads, lp, sl2e)
+  switch (G) {
+    case 1: TSR_FP8(1); break;
+    case 2: TSR_FP8(2); break;
+    case 4: TSR_FP8(4); break;
+    case 8: TSR_FP8(8); break;
+    default: return hipErrorInvalidValue;
+  }
+#undef TSR_FP8
+  return hipGetLastError();
+}
+
+}  // namespace tsr

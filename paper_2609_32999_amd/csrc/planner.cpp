@@ -70,8 +70,17 @@ tsr_status check_model(const tsr_model* m) {
       return fail(TSR_ERR_UNSUPPORTED, "bf16 path supports GQA group 1, 2, 4, 8");
     return TSR_OK;
   }
-  if (m->kv_dtype == TSR_E4M3)
-    return fail(TSR_ERR_UNSUPPORTED, "e4m3 KV pools are not implemented yet");
+  if (m->kv_dtype == TSR_E4M3 && m->act_dtype == TSR_BF16) {
+    if (m->head_dim != 128)
+      return fail(TSR_ERR_UNSUPPORTED, "e4m3 path supports head_dim 128");
+    if (m->page_size != 16)
+      return fail(TSR_ERR_UNSUPPORTED, "e4m3 path supports page_size 16");
+    if (m->n_kv_heads > 16)
+      return fail(TSR_ERR_UNSUPPORTED, "e4m3 path supports at most 16 KV heads");
+    if (G != 1 && G != 2 && G != 4 && G != 8)
+      return fail(TSR_ERR_UNSUPPORTED, "e4m3 path supports GQA group 1, 2, 4, 8");
+    return TSR_OK;
+  }
   return fail(TSR_ERR_UNSUPPORTED, "unsupported (kv_dtype, act_dtype) pair");
 }
 
@@ -98,6 +107,8 @@ tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
   p->n_req_pages = n_req_pages;
   p->n_req = n_req;
 
+  const bool e4m3 = m.kv_dtype == TSR_E4M3;
+  std::vector<PageDesc> gpages, apages, rpages;
   std::vector<GatherDesc> gather;
   std::vector<RowDesc> rows;
   std::vector<RetainDesc> retain;
@@ -158,6 +169,24 @@ tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
           << " tokens but prompt_len is " << q.prompt_len;
       return fail(TSR_ERR_INVALID_ARG, err.str());
     }
+    if (e4m3) {
+      // every request page must have a single writer (its scale is computed
+      // from its own values): segments and recompute windows page aligned
+      for (const Seg& sg : segs) {
+        const int32_t end = sg.start + sg.len;
+        bool ok = sg.start % B == 0 && (end % B == 0 || end == q.prompt_len);
+        if (ok && sg.unit >= 0 && q.units[sg.unit].residency == TSR_HIT) {
+          const tsr_unit& u = q.units[sg.unit];
+          const int32_t rc = std::max(0, std::min(u.n_recompute, u.n_tokens));
+          ok = rc % B == 0 || rc == u.n_tokens;
+        }
+        if (!ok) {
+          err << "request " << r << ": e4m3 plans must be page aligned (segment at "
+              << sg.start << " length " << sg.len << ")";
+          return fail(TSR_ERR_UNSUPPORTED, err.str());
+        }
+      }
+    }
     // block table
     const int npg = (q.prompt_len + B - 1) / B;
     bt_off[r] = (int32_t)bts.size();
@@ -182,6 +211,10 @@ tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
     // walk the prompt in position order
     for (const Seg& s : segs) {
       if (s.unit < 0) {
+        if (e4m3)
+          for (int32_t j = 0; j < s.len; j += B)
+            apages.push_back({(int32_t)rows.size() + j, q.block_table[(s.start + j) / B],
+                              s.start + j, std::min(B, s.len - j)});
         for (int32_t j = 0; j < s.len; ++j) {
           rows.push_back({req_slot(s.start + j), s.start + j});
           p->row_pos.push_back(s.start + j);
@@ -231,6 +264,19 @@ tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
       }
       const int32_t ncomp = hit ? std::min(u.n_recompute, u.n_tokens) : u.n_tokens;
       const int32_t row0 = (int32_t)rows.size();
+      if (e4m3) {
+        for (int32_t j = 0; j < ncomp; j += B)
+          apages.push_back({row0 + j, q.block_table[(u.position + j) / B], u.position + j,
+                            std::min(B, ncomp - j)});
+        if (hit)
+          for (int32_t j = ncomp; j < u.n_tokens; j += B)
+            gpages.push_back({u.pool_pages[j / B], q.block_table[(u.position + j) / B],
+                              u.position + j, std::min(B, u.n_tokens - j)});
+        else if (keep)
+          for (int32_t j = 0; j < u.n_tokens; j += B)
+            rpages.push_back({row0 + j, u.pool_pages[j / B], u.position + j,
+                              std::min(B, u.n_tokens - j)});
+      }
       for (int32_t j = 0; j < ncomp; ++j) {
         rows.push_back({req_slot(u.position + j), u.position + j});
         p->row_pos.push_back(u.position + j);
@@ -319,6 +365,12 @@ tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
   p->off_retain = off;  off = align_up(off + retain.size() * sizeof(RetainDesc), 256);
   p->off_items = off;   off = align_up(off + order.size() * sizeof(AttnItem), 256);
   p->off_bt = off;      off = align_up(off + bts.size() * sizeof(int32_t), 256);
+  p->off_gpages = off;  off = align_up(off + gpages.size() * sizeof(PageDesc), 256);
+  p->off_apages = off;  off = align_up(off + apages.size() * sizeof(PageDesc), 256);
+  p->off_rpages = off;  off = align_up(off + rpages.size() * sizeof(PageDesc), 256);
+  p->n_gpages = (int32_t)gpages.size();
+  p->n_apages = (int32_t)apages.size();
+  p->n_rpages = (int32_t)rpages.size();
   p->ws_bytes = std::max<size_t>(off, 256);
   p->image.assign(p->ws_bytes, 0);
   auto put = [&](size_t o, const void* src, size_t n) {
@@ -329,6 +381,9 @@ tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
   put(p->off_retain, retain.data(), retain.size() * sizeof(RetainDesc));
   put(p->off_items, order.data(), order.size() * sizeof(AttnItem));
   put(p->off_bt, bts.data(), bts.size() * sizeof(int32_t));
+  put(p->off_gpages, gpages.data(), gpages.size() * sizeof(PageDesc));
+  put(p->off_apages, apages.data(), apages.size() * sizeof(PageDesc));
+  put(p->off_rpages, rpages.data(), rpages.size() * sizeof(PageDesc));
   return TSR_OK;
 }
 

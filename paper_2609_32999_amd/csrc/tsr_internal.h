@@ -41,6 +41,19 @@ struct alignas(8) RetainDesc {
   int32_t dst;
 };
 
+// One whole page moved by the e4m3 kernels (each request page of an e4m3
+// plan has a single writer, so its scale is computed from its own values).
+//   compose: src = pool page, dst = request page, pos = position of slot 0
+//   append:  src = first computed row, dst = request page, pos = position
+//   retain:  src = first computed row, dst = pool page
+// n = valid slots (< page_size only for a unit's or a prompt's last page).
+struct alignas(16) PageDesc {
+  int32_t src;
+  int32_t dst;
+  int32_t pos;
+  int32_t n;
+};
+
 // One attention work item: up to kTileRows consecutive computed rows of one
 // request against one KV head.  n_rows == 0 marks padding.
 struct alignas(16) AttnItem {
@@ -61,6 +74,9 @@ struct PlanDev {
   const RetainDesc* retain;
   const AttnItem* items;
   const int32_t* block_tables;
+  const PageDesc* gpages;  // e4m3 plans only
+  const PageDesc* apages;
+  const PageDesc* rpages;
   const float* rope_cos;   // [max_position][d/2]
   const float* rope_sin;   // [max_position][d/2]
 };
@@ -78,9 +94,11 @@ struct tsr_plan {
   int32_t n_retain;
   int32_t n_items;          // attention items incl. padding
   int32_t max_kv_len;
+  int32_t n_gpages, n_apages, n_rpages;   // e4m3 plans only
   std::vector<int32_t> row_pos, row_req;
   std::vector<char> image;  // host copy of the device image
   size_t off_gather, off_rows, off_retain, off_items, off_bt, ws_bytes;
+  size_t off_gpages, off_apages, off_rpages;
   const void* rope_table;   // device
   void* ws;                 // device, NULL for host-only plans
   tsr::PlanDev dev;
@@ -110,5 +128,22 @@ hipError_t launch_attn(const tsr_plan* p, const void* q, const void* req_k,
                        const void* req_v, void* out, float* lse, hipStream_t s);
 hipError_t launch_retain(const tsr_plan* p, const void* k, const void* v,
                          void* pool_k, void* pool_v, hipStream_t s);
+
+// e4m3 pools: codes plus one fp32 scale per (page, K|V), scales [pages][2].
+hipError_t launch_compose_e4m3(const tsr_plan* p, const void* pool_k,
+                               const void* pool_v, const float* pool_scale,
+                               void* req_k, void* req_v, float* req_scale,
+                               int32_t n_layers, int64_t pool_stride,
+                               int64_t req_stride, int64_t pool_scale_stride,
+                               int64_t req_scale_stride, hipStream_t s);
+hipError_t launch_append_e4m3(const tsr_plan* p, const void* k, const void* v,
+                              void* req_k, void* req_v, float* req_scale,
+                              hipStream_t s);
+hipError_t launch_retain_e4m3(const tsr_plan* p, const void* k, const void* v,
+                              void* pool_k, void* pool_v, float* pool_scale,
+                              hipStream_t s);
+hipError_t launch_attn_e4m3(const tsr_plan* p, const void* q, const void* req_k,
+                            const void* req_v, const float* req_scale, void* out,
+                            float* lse, hipStream_t s);
 
 }  // namespace tsr

@@ -5,7 +5,9 @@ in libtsr's kernels through the C ABI.  A Session owns, for one layer shape:
 
 * the pool arena     [n_pool_pages][H_kv][B][d] for K (pre-RoPE) and V;
 * the request arena  [n_req_pages][H_kv][B][d] for the assembled K and V;
-* the RoPE table     built once per model by tsr_rope_table_init.
+* the RoPE table     built once per model by tsr_rope_table_init;
+* for e4m3 pools, page scales [n_layers][pages][2] fp32 ({K, V}) for both
+  arenas.
 
 Plans (one per batch of requests) own their device workspace.
 """
@@ -15,7 +17,7 @@ import torch
 
 from . import _binding as B
 
-TORCH_DTYPE = {"f32": torch.float32, "bf16": torch.bfloat16}
+TORCH_DTYPE = {"f32": torch.float32, "bf16": torch.bfloat16, "e4m3": torch.uint8}
 
 
 def _require_device():
@@ -39,6 +41,8 @@ class Session:
         self.device = torch.device(device)
         self.kv_dtype = TORCH_DTYPE[shape.kv_dtype]
         self.act_dtype = TORCH_DTYPE[shape.act_dtype]
+        if shape.act_dtype == "e4m3":
+            raise B.TsrError(B.TSR_ERR_UNSUPPORTED, "activations cannot be e4m3")
         self.n_layers = n_layers
         self.n_pool_pages = n_pool_pages
         self.n_req_pages = n_req_pages
@@ -49,6 +53,13 @@ class Session:
         self.req_k = torch.empty((n_layers, n_req_pages, *page), dtype=self.kv_dtype,
                                  device=self.device)
         self.req_v = torch.empty_like(self.req_k)
+        self.e4m3 = shape.kv_dtype == "e4m3"
+        self.pool_scale = self.req_scale = None
+        if self.e4m3:
+            self.pool_scale = torch.empty((n_layers, n_pool_pages, 2), dtype=torch.float32,
+                                          device=self.device)
+            self.req_scale = torch.empty((n_layers, n_req_pages, 2), dtype=torch.float32,
+                                         device=self.device)
         nbytes = B.tsr_rope_table_bytes(self.model)
         if nbytes == 0:
             raise B.TsrError(B.TSR_ERR_INVALID_ARG, B.tsr_last_error())
@@ -73,13 +84,20 @@ class Session:
         """Compose one layer (default 0), or all layers when layer == 'all'."""
         s = stream or self.stream
         if layer == "all":
-            B.tsr_compose_kv(plan, self.pool_k, self.pool_v, None, self.req_k, self.req_v,
-                             None, self.n_layers, self.pool_k[0].nbytes if self.n_layers > 1 else 0,
+            B.tsr_compose_kv(plan, self.pool_k, self.pool_v, self.pool_scale, self.req_k,
+                             self.req_v, self.req_scale, self.n_layers,
+                             self.pool_k[0].nbytes if self.n_layers > 1 else 0,
                              self.req_k[0].nbytes if self.n_layers > 1 else 0, s)
             return
         li = layer or 0
-        B.tsr_compose_kv(plan, self.pool_k[li], self.pool_v[li], None, self.req_k[li],
-                         self.req_v[li], None, 1, 0, 0, s)
+        B.tsr_compose_kv(plan, self.pool_k[li], self.pool_v[li], self._ps(li), self.req_k[li],
+                         self.req_v[li], self._rs(li), 1, 0, 0, s)
+
+    def _ps(self, layer):
+        return self.pool_scale[layer] if self.e4m3 else None
+
+    def _rs(self, layer):
+        return self.req_scale[layer] if self.e4m3 else None
 
     def new_outputs(self, plan, with_lse: bool = True):
         T = plan.num_compute_tokens
@@ -90,17 +108,17 @@ class Session:
         return out, lse
 
     def prefill_attn(self, plan, q, k, v, out, lse=None, layer: int = 0, stream=None):
-        B.tsr_prefill_attn(plan, q, k, v, self.req_k[layer], self.req_v[layer], None,
-                           out, lse, stream or self.stream)
+        B.tsr_prefill_attn(plan, q, k, v, self.req_k[layer], self.req_v[layer],
+                           self._rs(layer), out, lse, stream or self.stream)
 
     def append(self, plan, k, v, layer: int = 0, stream=None):
-        B.tsr_append_kv(plan, k, v, self.req_k[layer], self.req_v[layer], None,
+        B.tsr_append_kv(plan, k, v, self.req_k[layer], self.req_v[layer], self._rs(layer),
                         stream or self.stream)
 
     def attn(self, plan, q, out, lse=None, layer: int = 0, stream=None):
-        B.tsr_attn(plan, q, self.req_k[layer], self.req_v[layer], None, out, lse,
+        B.tsr_attn(plan, q, self.req_k[layer], self.req_v[layer], self._rs(layer), out, lse,
                    stream or self.stream)
 
     def retain(self, plan, k, v, layer: int = 0, stream=None):
-        B.tsr_retain_kv(plan, k, v, self.pool_k[layer], self.pool_v[layer], None,
+        B.tsr_retain_kv(plan, k, v, self.pool_k[layer], self.pool_v[layer], self._ps(layer),
                         stream or self.stream)

@@ -26,9 +26,14 @@ def upload_pool(sess, wl, unit_ids=None, layer: int = 0) -> None:
     B = wl.model.page_size
     ids = wl.hit_unit_ids() if unit_ids is None else unit_ids
     for uid in ids:
-        k, v = wl.unit_state(uid)
         pages = torch.as_tensor(np.asarray(wl.unit_pages[uid], dtype=np.int64),
                                 device=sess.device)
+        if sess.e4m3:
+            k, v, ks, vs = wl.unit_state_e4m3(uid)
+            sc = torch.from_numpy(np.stack([ks, vs], axis=1)).to(sess.device)
+            sess.pool_scale[layer][pages] = sc
+        else:
+            k, v = wl.unit_state(uid)
         for src, dst in ((k, sess.pool_k[layer]), (v, sess.pool_v[layer])):
             t = torch.from_numpy(_pages_from_tokens(src, B)).to(sess.device)
             dst[pages] = t.to(dst.dtype)
@@ -50,7 +55,9 @@ def fresh_inputs(sess, wl, plan):
 
 
 def request_kv(sess, wl, r: int, layer: int = 0):
-    """Assembled K, V of request r from the request pages, [P][H_kv][d] (fp32, host)."""
+    """Assembled K, V of request r from the request pages, [P][H_kv][d] on the
+    host: fp32 values, or for e4m3 arenas (codes_k, codes_v, scale_k[P],
+    scale_v[P]) with each position's page scale."""
     req = wl.requests[r]
     B = wl.model.page_size
     bt = torch.as_tensor(np.asarray(req.block_table, dtype=np.int64), device=sess.device)
@@ -58,5 +65,10 @@ def request_kv(sess, wl, r: int, layer: int = 0):
     for arena in (sess.req_k[layer], sess.req_v[layer]):
         pages = arena[bt]                                   # [npg][H][B][d]
         dense = pages.permute(0, 2, 1, 3).reshape(-1, *pages.shape[1:2], pages.shape[-1])
-        out.append(dense[:req.prompt_len].float().cpu().numpy())
-    return out[0], out[1]
+        dense = dense[:req.prompt_len]
+        out.append(dense.cpu().numpy() if sess.e4m3 else dense.float().cpu().numpy())
+    if not sess.e4m3:
+        return out[0], out[1]
+    sc = sess.req_scale[layer][bt].cpu().numpy()            # [npg][2]
+    per_pos = np.repeat(sc, B, axis=0)[:req.prompt_len]
+    return out[0], out[1], per_pos[:, 0].copy(), per_pos[:, 1].copy()

@@ -10,8 +10,9 @@ import torch
 
 from oracle import layout as L
 from oracle import pipeline as PL
-from oracle.compose import retained_pages
-from oracle.numerics import round_bf16
+from oracle.compose import (assemble_request_kv_e4m3, retained_pages,
+                            retained_pages_e4m3)
+from oracle.numerics import e4m3_decode, round_bf16
 from paper_2609_32999_amd import staging
 from paper_2609_32999_amd.session import Session
 
@@ -19,12 +20,15 @@ from paper_2609_32999_amd.session import Session
 TOL_BF16 = 2e-3
 TOL_F32 = 1e-5
 
-SENTINEL_BITS = {torch.bfloat16: 0x7FC1, torch.float32: 0x7FC00001}
+SENTINEL_BITS = {torch.bfloat16: 0x7FC1, torch.float32: 0x7FC00001,
+                 torch.uint8: 0x7F}          # e4m3fn NaN code
 
 
 def fill_sentinel(t: torch.Tensor) -> None:
     if t.dtype == torch.bfloat16:
         t.view(torch.int16).fill_(SENTINEL_BITS[torch.bfloat16])
+    elif t.dtype == torch.uint8:
+        t.fill_(SENTINEL_BITS[torch.uint8])
     else:
         t.view(torch.int32).fill_(SENTINEL_BITS[torch.float32])
 
@@ -32,6 +36,8 @@ def fill_sentinel(t: torch.Tensor) -> None:
 def is_sentinel(a: torch.Tensor) -> torch.Tensor:
     if a.dtype == torch.bfloat16:
         return a.view(torch.int16) == SENTINEL_BITS[torch.bfloat16]
+    if a.dtype == torch.uint8:
+        return a == SENTINEL_BITS[torch.uint8]
     return a.view(torch.int32) == SENTINEL_BITS[torch.float32]
 
 
@@ -52,9 +58,13 @@ class GpuRun:
         self.sess = s
         for t in (s.pool_k, s.pool_v, s.req_k, s.req_v):
             fill_sentinel(t)
+        if s.e4m3:
+            s.pool_scale.fill_(float("nan"))
+            s.req_scale.fill_(float("nan"))
         staging.upload_pool(s, wl)
         self.pool_k0 = s.pool_k.clone()
         self.pool_v0 = s.pool_v.clone()
+        self.pool_s0 = s.pool_scale.clone() if s.e4m3 else None
         self.plan = s.plan(wl.requests)
         self.q, self.k, self.v = staging.fresh_inputs(s, wl, self.plan)
         self.pos, self.req = self.plan.compute_positions()
@@ -98,7 +108,16 @@ def check_request(run: GpuRun, r: int, kv_heads=None, check_kv=True):
     report = {}
     rows = run.rows_of(r)
     assert np.array_equal(run.pos[rows], res.positions), "computed positions differ"
-    if check_kv:
+    if check_kv and m.kv_dtype == "e4m3":
+        Kc, Vc, ks, vs = run.request_kv(r)
+        oKc, oVc, oks, ovs = assemble_request_kv_e4m3(wl, r)
+        assert not np.isnan(ks).any() and not np.isnan(vs).any(), "unwritten page scale"
+        assert np.array_equal(ks, oks) and np.array_equal(vs, ovs), "page scales differ"
+        assert np.array_equal(e4m3_decode(Vc), e4m3_decode(oVc)), "V codes differ"
+        kd = e4m3_decode(Kc) != e4m3_decode(oKc)
+        report["k_mismatch"] = int(kd.sum())
+        assert report["k_mismatch"] == 0, f"K codes differ in {kd.sum()} elements"
+    elif check_kv:
         K, V = run.request_kv(r)
         K, V = K[:, res.kv_heads], V[:, res.kv_heads]
         assert not np.isnan(K).any() and not np.isnan(V).any(), "unwritten request slot"
@@ -144,6 +163,8 @@ def check_request(run: GpuRun, r: int, kv_heads=None, check_kv=True):
 
 def check_retained(run: GpuRun):
     wl = run.wl
+    if wl.model.kv_dtype == "e4m3":
+        return _check_retained_e4m3(run)
     pages = retained_pages(wl)
     s = run.sess
     B = wl.model.page_size
@@ -177,3 +198,29 @@ def check_request_sentinels(run: GpuRun, r: int):
     last = int(req.block_table[-1])
     assert bool(is_sentinel(run.sess.req_k[0, last][:, tail:]).all())
     assert bool(is_sentinel(run.sess.req_v[0, last][:, tail:]).all())
+
+
+def _check_retained_e4m3(run: GpuRun):
+    wl = run.wl
+    s = run.sess
+    pages = retained_pages_e4m3(wl)
+    for pg, (kref, vref, ks, vs, filled) in pages.items():
+        f = torch.as_tensor(filled, device=s.device)
+        gk = s.pool_k[0, pg][:, f].cpu().numpy()
+        gv = s.pool_v[0, pg][:, f].cpu().numpy()
+        assert np.array_equal(e4m3_decode(gk), e4m3_decode(kref[:, filled]))
+        assert np.array_equal(e4m3_decode(gv), e4m3_decode(vref[:, filled]))
+        sc = s.pool_scale[0, pg].cpu().numpy()
+        assert sc[0] == ks and sc[1] == vs, (pg, sc, ks, vs)
+        if (~filled).any():
+            assert bool(is_sentinel(s.pool_k[0, pg][:, ~f]).all())
+    touched = torch.zeros(wl.n_pool_pages, dtype=torch.bool, device=s.device)
+    if pages:
+        touched[torch.as_tensor(list(pages), device=s.device)] = True
+    un = ~touched
+    assert bool((s.pool_k[0] == run.pool_k0[0])[un].all())
+    assert bool((s.pool_v[0] == run.pool_v0[0])[un].all())
+    same_s = (s.pool_scale[0] == run.pool_s0[0]) | (torch.isnan(s.pool_scale[0]) &
+                                                    torch.isnan(run.pool_s0[0]))
+    assert bool(same_s[un].all())
+    return len(pages)

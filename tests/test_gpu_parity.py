@@ -94,3 +94,27 @@ def test_large_configs_sampled(name, n_req):
     for r in sorted(rng.choice(len(wl.requests), n_req, replace=False).tolist()):
         check_request(run, r, kv_heads=[int(rng.integers(wl.model.n_kv_heads))])
     assert run.pool_after_attn_ok
+
+
+def test_fp8_small():
+    _full_check(workloads.generate("small_fp8"))
+
+
+def test_fp8_small_all_miss_and_g8():
+    _full_check(workloads.make_workload(workloads.get_config("small_fp8").with_(hit_prob=0.0)))
+    cfg = workloads.get_config("small_fp8")
+    shape = cfg.model.__class__(**{**vars(cfg.model), "n_q_heads": 64})
+    _full_check(workloads.make_workload(cfg.with_(model=shape)))
+
+
+@pytest.mark.slow
+def test_fp8rag_full_size():
+    """The fp8 RAG batch at full size: every request's codes and page scales
+    bit-exact; attention on two sampled KV heads of every request."""
+    wl = workloads.generate("fp8rag")
+    run = GpuRun(wl)
+    assert run.pool_after_compose_ok and run.pool_after_attn_ok
+    heads = np.random.default_rng(202).choice(wl.model.n_kv_heads, 2, replace=False)
+    for r in range(0, len(wl.requests), 3):
+        check_request(run, r, kv_heads=sorted(heads.tolist()))
+    assert check_retained(run) > 0

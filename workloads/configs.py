@@ -139,6 +139,14 @@ SMALL_BF16_G8 = _reg(WorkloadConfig(
     query_tokens=13,
     description="small bf16, 64q/8kv (GQA group 8)"))
 
+SMALL_FP8 = _reg(WorkloadConfig(
+    name="small_fp8", seed=14, model=replace(_RAG_SMALL_SHAPE, kv_dtype="e4m3"),
+    n_requests=3, units_per_request=(3, 5), unit_tokens=(2, 9), pool_units=10,
+    zipf_s=1.0, hit_prob=0.6, n_recompute=16, instruction_tokens=32,
+    query_tokens=20, extra={"unit_tokens_multiple": 16},
+    description="small e4m3 pool: page-aligned units of 32..144 tokens, "
+                "ragged final page"))
+
 SMALL_F32 = _reg(WorkloadConfig(
     name="small_f32", seed=13,
     model=ModelShape(n_q_heads=8, n_kv_heads=2, head_dim=128, kv_dtype="f32",

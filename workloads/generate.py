@@ -112,7 +112,10 @@ class Workload:
         per-page power-of-two scales (k_scale, v_scale) float32 [pages].
 
         Codes are torch's e4m3fn encoding of N(0,1)/scale draws clamped to the
-        finite range, so code * scale is distributed like N(0,1).
+        finite range, so code * scale is distributed like N(0,1).  As in any
+        pool written by the retention quantizer, each page's scale is the
+        smallest power of two that covers the page: the first element of
+        every page holds the largest finite code (+448).
         """
         m = self.model
         n = int(self.unit_len[unit_id])
@@ -127,6 +130,7 @@ class Workload:
             tok_scale = np.repeat(scale, m.page_size)[:n]
             x = np.clip(x / tok_scale[:, None, None], -448.0, 448.0)
             codes = torch.from_numpy(x).to(torch.float8_e4m3fn).view(torch.uint8).numpy()
+            codes[::m.page_size, 0, 0] = 0x7E
             out.append((codes, scale))
         (kc, ks), (vc, vs) = out
         return kc, vc, ks, vs
@@ -169,6 +173,7 @@ def make_workload(cfg: WorkloadConfig) -> Workload:
         lrng = np.random.default_rng((cfg.seed, _TAG_LEN))
         lo, hi = cfg.unit_tokens
         unit_len = lrng.integers(lo, hi + 1, size=cfg.pool_units).astype(np.int32)
+        unit_len *= int(cfg.extra.get("unit_tokens_multiple", 1))
     else:
         unit_len = np.full(cfg.pool_units, cfg.unit_tokens, dtype=np.int32)
 
