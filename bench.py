@@ -38,6 +38,28 @@ def kv_elem_bytes(dtype):
     return {"f32": 4, "bf16": 2, "e4m3": 1}[dtype]
 
 
+def profiled_traffic(workload: str, kernel: str):
+    """HBM bytes per launch of `kernel` from the committed rocprofv3 counter
+    summary (FETCH_SIZE and WRITE_SIZE scaled against a plain copy), or None
+    if there is none or the kernel's source changed since it was taken."""
+    import hashlib
+    import re
+    path = os.path.join(ROOT, "profiles", f"{workload}_kernels.md")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    m = re.search(r"```json\n(.*?)\n```", text, re.S)
+    if not m:
+        return None
+    for name, rec in json.loads(m.group(1)).items():
+        if name != kernel:
+            continue
+        src = os.path.join(ROOT, rec["source"])
+        digest = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+        return rec["traffic_bytes"] if digest == rec["source_sha256_16"] else None
+    return None
+
+
 def cpu_baseline(wl, n_req):
     """Time the CPU oracle on the first n_req requests of the same batch."""
     import threadpoolctl
@@ -177,6 +199,10 @@ def main():
     attn_tflops = attn_flops / (attn_ms * 1e-3) / 1e12
     compose_gbs = gather_bytes / (compose_ms * 1e-3) / 1e9
     peak = PEAK_E4M3_BLEND if m.kv_dtype == "e4m3" else PEAK_MFMA_TFLOPS[m.act_dtype]
+    G = m.n_q_heads // m.n_kv_heads
+    attn_kernel = f"attn_fp8_kernel<{G}>" if m.kv_dtype == "e4m3" else f"attn_mfma_kernel<{G}>"
+    compose_kernel = ("page_fp8_kernel<0>" if m.kv_dtype == "e4m3" else
+                      f"kv_move_kernel<{m.head_dim}, unsigned short, 0>")
     value = wl.prompt_tokens / (ms * 1e-3)
 
     rec = {
@@ -201,13 +227,14 @@ def main():
         "kernel_us": {"compose": compose_ms * 1e3, "append": append_ms * 1e3,
                       "attention": attn_ms * 1e3, "retain_side_stream": retain_ms * 1e3},
         "roofline": {"bound": "mfma", "achieved": attn_tflops, "peak": peak,
-                     "unit": "TFLOP/s", "frac": attn_tflops / peak, "traffic": None,
-                     "kernel": ("attn_fp8_kernel" if m.kv_dtype == "e4m3"
-                                else "attn_mfma_kernel"),
-                     "flops_per_launch": attn_flops},
+                     "unit": "TFLOP/s", "frac": attn_tflops / peak,
+                     "traffic": profiled_traffic(args.workload, attn_kernel),
+                     "kernel": attn_kernel, "flops_per_launch": attn_flops},
         "roofline_compose": {"bound": "hbm", "achieved": compose_gbs, "peak": PEAK_HBM_GBS,
                              "unit": "GB/s", "frac": compose_gbs / PEAK_HBM_GBS,
-                             "bytes_per_launch": gather_bytes},
+                             "bytes_per_launch": gather_bytes,
+                             "traffic": profiled_traffic(args.workload, compose_kernel),
+                             "kernel": compose_kernel},
         "append_gbps": append_bytes / (append_ms * 1e-3) / 1e9,
         "retain_gbps": retain_bytes / (retain_ms * 1e-3) / 1e9 if retain_ms > 0 else None,
     }
