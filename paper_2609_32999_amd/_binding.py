@@ -15,7 +15,8 @@ from ctypes import POINTER, c_double, c_float, c_int32, c_int64, c_size_t, c_uin
 import numpy as np
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "libtsr.so")
+# TSR_LIBRARY overrides the library path (to compare builds side by side).
+LIB_PATH = os.environ.get("TSR_LIBRARY") or os.path.join(HERE, "libtsr.so")
 
 TSR_OK, TSR_ERR_INVALID_ARG, TSR_ERR_UNSUPPORTED, TSR_ERR_OUT_OF_RANGE, TSR_ERR_DEVICE = range(5)
 STATUS_NAMES = {0: "OK", 1: "INVALID_ARG", 2: "UNSUPPORTED", 3: "OUT_OF_RANGE", 4: "DEVICE"}

@@ -124,6 +124,9 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+constexpr f16x2 kOnes2 = {(_Float16)1.0f, (_Float16)1.0f};
+
 union Frag {
   uint4 u;
   uint32_t w[4];
@@ -149,14 +152,14 @@ __device__ __forceinline__ uint32_t pack_f16x2(float a, float b) {
 }
 
 template <int G>
-__global__ __launch_bounds__(256, (G > 4 ? 1 : 2)) void attn_mfma_kernel(
+__global__ __launch_bounds__(256, 2) void attn_mfma_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc,
     const uint16_t* __restrict__ vc, const AttnItem* __restrict__ items,
     const int32_t* __restrict__ bts, const RowDesc* __restrict__ rows,
     const float* __restrict__ rope_cos, const float* __restrict__ rope_sin,
     uint16_t* __restrict__ out, float* __restrict__ lse, int n_q_heads,
     int n_kv_heads, int log2_page, float scale, float scale_log2e) {
-  constexpr int HPW = (G + 3) / 4;  // query heads per wave
+  constexpr int HPW = 1;  // query heads per wave
   __shared__ __attribute__((aligned(16))) uint16_t smem[2 * kStage];
 
   const AttnItem it = items[blockIdx.x];
@@ -177,7 +180,9 @@ __global__ __launch_bounds__(256, (G > 4 ? 1 : 2)) void attn_mfma_kernel(
   bf16x8 qf[HPW][8];
 #pragma unroll
   for (int i = 0; i < HPW; ++i) {
-    const int hl = min(w + 4 * i, G - 1);
+    // wave w owns query head head0 + w of the group; with G < 4 the spare
+    // waves recompute head G-1 and store nothing
+    const int hl = G >= 4 ? it.head0 + w + 4 * i : min(w + 4 * i, G - 1);
     const uint16_t* qp = q + ((int64_t)row * n_q_heads + g * G + hl) * kD;
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
@@ -214,7 +219,7 @@ __global__ __launch_bounds__(256, (G > 4 ? 1 : 2)) void attn_mfma_kernel(
   // G-1 (branch-free MFMA code) and store nothing.
   bool wave_active[HPW];
 #pragma unroll
-  for (int i = 0; i < HPW; ++i) wave_active[i] = (w + 4 * i) < G;
+  for (int i = 0; i < HPW; ++i) wave_active[i] = G >= 4 || (w + 4 * i) < G;
 
   // ---- global -> register staging of one K/V tile
   // The tile's 64 keys form four 16-key blocks; with B >= 16 each block lies
@@ -346,22 +351,26 @@ __global__ __launch_bounds__(256, (G > 4 ? 1 : 2)) void attn_mfma_kernel(
           for (int r = 0; r < 16; ++r) o[i][db][r] *= alpha;
       }
       const float mc = m[i] * scale_log2e;
-      float ls = 0.0f;
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const float p = __builtin_amdgcn_exp2f(fmaf(s[i][kb][r], scale_log2e, -mc));
-          s[i][kb][r] = p;
-          ls += p;
-        }
-      l[i] += ls;
+        for (int r = 0; r < 16; ++r)
+          s[i][kb][r] = __builtin_amdgcn_exp2f(fmaf(s[i][kb][r], scale_log2e, -mc));
+      // P^T fragments in fp16; the row sum is taken from the same fp16 values
+      // that enter the PV product (two per v_dot2_f32_f16)
+      float ls = 0.0f;
 #pragma unroll
       for (int k2 = 0; k2 < 4; ++k2) {
         const int kb = k2 >> 1, base = 8 * (k2 & 1);
 #pragma unroll
         for (int e = 0; e < 8; ++e) pf[i][k2][e] = (_Float16)s[i][kb][base + e];
+#pragma unroll
+        for (int e = 0; e < 8; e += 2) {
+          const f16x2 pair = {pf[i][k2][e], pf[i][k2][e + 1]};
+          ls = __builtin_amdgcn_fdot2(pair, kOnes2, ls, false);
+        }
       }
+      l[i] += ls;
     }
 
     // O^T[d][row] += V^T[d][keys] P^T[keys][row]
@@ -409,7 +418,7 @@ __global__ __launch_bounds__(256, (G > 4 ? 1 : 2)) void attn_mfma_kernel(
     const float lt = l[i] + __shfl_xor(l[i], 32);
     if (lrow >= it.n_rows) continue;
     const float inv = 1.0f / lt;
-    const int hq = g * G + w + 4 * i;
+    const int hq = g * G + (G >= 4 ? it.head0 : 0) + w + 4 * i;
     uint16_t* op = out + ((int64_t)row * n_q_heads + hq) * kD;
 #pragma unroll
     for (int db = 0; db < 4; ++db)

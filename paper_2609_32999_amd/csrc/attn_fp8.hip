@@ -49,7 +49,7 @@ __device__ __forceinline__ int page_scale_exp(float amax) {
 }
 
 template <int G>
-__global__ __launch_bounds__(256, (G > 4 ? 1 : 2)) void attn_fp8_kernel(
+__global__ __launch_bounds__(256, 2) void attn_fp8_kernel(
     const uint16_t* __restrict__ q, const uint8_t* __restrict__ kc,
     const uint8_t* __restrict__ vc, const float* __restrict__ scales,
     const AttnItem* __restrict__ items, const int32_t* __restrict__ bts,
@@ -57,7 +57,7 @@ __global__ __launch_bounds__(256, (G > 4 ? 1 : 2)) void attn_fp8_kernel(
     const float* __restrict__ rope_sin, uint16_t* __restrict__ out,
     float* __restrict__ lse, int n_q_heads, int n_kv_heads, int log2_page,
     float scale_log2e) {
-  constexpr int HPW = (G + 3) / 4;
+  constexpr int HPW = 1;  // query heads per wave
   __shared__ __attribute__((aligned(16))) uint8_t kmem[2][kKBytes];
   __shared__ __attribute__((aligned(16))) uint16_t vmem[2][kVElems];
 
@@ -81,7 +81,9 @@ __global__ __launch_bounds__(256, (G > 4 ? 1 : 2)) void attn_fp8_kernel(
   float qs[HPW];
 #pragma unroll
   for (int i = 0; i < HPW; ++i) {
-    const int hl = min(w + 4 * i, G - 1);
+    // wave w owns query head head0 + w of the group; with G < 4 the spare
+    // waves recompute head G-1 and store nothing
+    const int hl = G >= 4 ? it.head0 + w + 4 * i : min(w + 4 * i, G - 1);
     const uint16_t* qp = q + ((int64_t)row * n_q_heads + g * G + hl) * kD;
     float lo[32], hi[32];
 #pragma unroll
@@ -129,7 +131,7 @@ __global__ __launch_bounds__(256, (G > 4 ? 1 : 2)) void attn_fp8_kernel(
   }
   bool wave_active[HPW];
 #pragma unroll
-  for (int i = 0; i < HPW; ++i) wave_active[i] = (w + 4 * i) < G;
+  for (int i = 0; i < HPW; ++i) wave_active[i] = G >= 4 || (w + 4 * i) < G;
 
   // ---- global -> register staging.  16-key blocks of a tile lie in one page.
   // K: two 16-byte chunks per thread; chunk c covers block c/128, key
@@ -334,7 +336,7 @@ __global__ __launch_bounds__(256, (G > 4 ? 1 : 2)) void attn_fp8_kernel(
     const float lt = l[i] + __shfl_xor(l[i], 32);
     if (lrow >= it.n_rows) continue;
     const float inv = 1.0f / lt;
-    const int hq = g * G + w + 4 * i;
+    const int hq = g * G + (G >= 4 ? it.head0 : 0) + w + 4 * i;
     uint16_t* op = out + ((int64_t)row * n_q_heads + hq) * kD;
 #pragma unroll
     for (int db = 0; db < 4; ++db)

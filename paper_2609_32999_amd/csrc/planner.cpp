@@ -306,6 +306,11 @@ tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
   }
 
   // attention items: tiles of kTileRows consecutive rows x KV heads
+  // The MFMA kernels give each of their 4 waves one query head; a larger
+  // GQA group is split over several items that read the same K/V tiles
+  // (adjacent in the launch order, so the repeat reads hit L2).
+  const int G = m.n_q_heads / Hkv;
+  const int hsplit = (m.act_dtype == TSR_BF16 && G > 4) ? G / 4 : 1;
   struct Item { AttnItem it; int64_t cost; int group; };
   std::vector<Item> items;
   int32_t max_kv = 0;
@@ -314,16 +319,19 @@ tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
       const int32_t n = std::min(kTileRows, req_row0[r + 1] - t0);
       const int32_t lo = p->row_pos[t0], hi = p->row_pos[t0 + n - 1];
       max_kv = std::max(max_kv, hi + 1);
-      for (int g = 0; g < Hkv; ++g) {
-        AttnItem a{t0, n, hi + 1, lo, g, bt_off[r], bt_len[r], r};
-        items.push_back({a, (int64_t)(hi + 1), r * Hkv + g});
-      }
+      for (int g = 0; g < Hkv; ++g)
+        for (int hs = 0; hs < hsplit; ++hs) {
+          AttnItem a{t0, n, hi + 1, lo, g, bt_off[r], bt_len[r], 4 * hs};
+          items.push_back({a, (int64_t)(hi + 1), r * Hkv + g});
+        }
     }
   }
   // XCD-aware order: (request, KV head) groups share K/V, so each group is
   // bound to one XCD bin (workgroup w runs on XCD w % kNumXcd); bins are
   // balanced by cost (longest group first onto the lightest bin) and each
-  // bin is issued longest item first.  Short bins are padded with empty items.
+  // bin is issued longest item first (measured: issuing a bin group by
+  // group for L2 locality lost more to the tail than it gained).  Short bins
+  // are padded with empty items.
   std::vector<int64_t> gcost((size_t)std::max(1, n_req * Hkv), 0);
   for (const Item& x : items) gcost[x.group] += x.cost;
   std::vector<int> gorder(gcost.size());
@@ -350,7 +358,7 @@ tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
   for (size_t i = 0; i < per_bin; ++i)
     for (int b = 0; b < kNumXcd; ++b)
       order.push_back(i < bins[b].size() ? bins[b][i]
-                                         : AttnItem{0, 0, 0, 0, 0, 0, 0, -1});
+                                         : AttnItem{0, 0, 0, 0, 0, 0, 0, 0});
 
   p->T = (int32_t)rows.size();
   p->n_gather = (int32_t)gather.size();

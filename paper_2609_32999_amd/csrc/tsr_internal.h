@@ -55,7 +55,9 @@ struct alignas(16) PageDesc {
 };
 
 // One attention work item: up to kTileRows consecutive computed rows of one
-// request against one KV head.  n_rows == 0 marks padding.
+// request against one KV head, for query heads head0 .. head0+3 of that KV
+// head's group (MFMA kernels; a group of G > 4 heads is split over G/4
+// items).  n_rows == 0 marks padding.
 struct alignas(16) AttnItem {
   int32_t row0;      // first computed row (plan order)
   int32_t n_rows;    // rows in the tile (<= kTileRows)
@@ -64,7 +66,7 @@ struct alignas(16) AttnItem {
   int32_t kv_head;
   int32_t bt_off;    // offset of the request's block table in the plan
   int32_t n_pages;   // entries of that block table
-  int32_t req;
+  int32_t head0;     // first query head of the group handled by the item
 };
 
 // Device-side view of a plan (pointers into the caller's workspace).
