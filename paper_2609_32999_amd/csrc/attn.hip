@@ -127,12 +127,21 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
 constexpr f16x2 kOnes2 = {(_Float16)1.0f, (_Float16)1.0f};
 
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+typedef i32x4 __attribute__((aligned(4))) i32x4u;
+
 union Frag {
   uint4 u;
   uint32_t w[4];
   bf16x8 b;
   f16x8 h;
 };
+
+// Wave-priority hooks around MFMA blocks (see s_setprio); empty by default.
+#ifndef TSR_PRIO_MFMA
+#define TSR_PRIO_MFMA() ((void)0)
+#define TSR_PRIO_VALU() ((void)0)
+#endif
 
 constexpr int kD = 128;
 constexpr int kKT = kKvTile;           // keys per tile
@@ -241,11 +250,19 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(
   auto load_tile = [&](int j) {
     const int key0 = j * kKT;
     int64_t base[4];
+    int page[4];
+    const int idx0 = key0 >> log2_page;
+    if (log2_page == 4 && idx0 + 3 < it.n_pages) {   // one 16-byte scalar load
+      const i32x4u p4 = *reinterpret_cast<const i32x4u*>(bt + idx0);
+      page[0] = p4[0]; page[1] = p4[1]; page[2] = p4[2]; page[3] = p4[3];
+    } else {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) page[q] = bt[min((key0 + 16 * q) >> log2_page, it.n_pages - 1)];
+    }
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const int kq = key0 + 16 * q;
-      const int page = bt[min(kq >> log2_page, it.n_pages - 1)];
-      base[q] = ((((int64_t)page * n_kv_heads + g) << log2_page) + (kq & page_mask)) * kD;
+      base[q] = ((((int64_t)page[q] * n_kv_heads + g) << log2_page) + (kq & page_mask)) * kD;
     }
     const int64_t vbase = vq == 0 ? base[0] : vq == 1 ? base[1] : vq == 2 ? base[2] : base[3];
 #pragma unroll
@@ -294,6 +311,7 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(
     const uint16_t* vs = ks + kKElems;
 
     // S^T[key][row] for two 32-key blocks
+    TSR_PRIO_MFMA();
     f32x16 s[HPW][2];
 #pragma unroll
     for (int i = 0; i < HPW; ++i)
@@ -312,7 +330,17 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(
           s[i][kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a.b, qf[i][kst], s[i][kb], 0, 0, 0);
       }
     }
+    // keep four LDS fragment reads in flight ahead of the MFMAs
+    // (scheduling groups: 0x100 = LDS read, 0x008 = MFMA)
+    __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+#pragma unroll
+    for (int t = 0; t < 12; ++t) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
 
+    TSR_PRIO_VALU();
     if constexpr (MASK) {
       const int kbase = j * kKT;
 #pragma unroll
@@ -327,66 +355,68 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(
     }
 
     // Online softmax with a lazily updated running max: the max (and with
-    // it O and l) is only rescaled when a row's tile max exceeds it by more
+    // it O and l) is only rescaled when a row's block max exceeds it by more
     // than 2^kLazy in probability units, so P stays <= 2^kLazy (exact range
-    // for fp16) and the rescale is skipped on almost every tile.
-    f16x8 pf[HPW][4];
+    // for fp16) and the rescale is skipped almost always.  The tile is
+    // processed as two 32-key halves (softmax, then its PV MFMAs) so that the
+    // second half's VALU work can issue while the first half's MFMAs run.
 #pragma unroll
-    for (int i = 0; i < HPW; ++i) {
-      float mt = -INFINITY;
+    for (int kb = 0; kb < 2; ++kb) {
+      f16x8 pf[HPW][2];
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
+      for (int i = 0; i < HPW; ++i) {
+        float mt = -INFINITY;
 #pragma unroll
         for (int r = 0; r < 16; ++r) mt = fmaxf(mt, s[i][kb][r]);
-      mt = fmaxf(mt, __shfl_xor(mt, 32));
-      const bool grow = mt * scale_log2e > m[i] * scale_log2e + kLazy;
-      if (__builtin_amdgcn_ballot_w64(grow)) {
-        const float mn = fmaxf(m[i], mt);
-        const float alpha = __builtin_amdgcn_exp2f((m[i] - mn) * scale_log2e);
-        m[i] = mn;
-        l[i] *= alpha;
+        mt = fmaxf(mt, __shfl_xor(mt, 32));
+        const bool grow = mt * scale_log2e > m[i] * scale_log2e + kLazy;
+        if (__builtin_amdgcn_ballot_w64(grow)) {
+          const float mn = fmaxf(m[i], mt);
+          const float alpha = __builtin_amdgcn_exp2f((m[i] - mn) * scale_log2e);
+          m[i] = mn;
+          l[i] *= alpha;
 #pragma unroll
-        for (int db = 0; db < 4; ++db)
+          for (int db = 0; db < 4; ++db)
 #pragma unroll
-          for (int r = 0; r < 16; ++r) o[i][db][r] *= alpha;
-      }
-      const float mc = m[i] * scale_log2e;
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
+            for (int r = 0; r < 16; ++r) o[i][db][r] *= alpha;
+        }
+        const float mc = m[i] * scale_log2e;
 #pragma unroll
         for (int r = 0; r < 16; ++r)
           s[i][kb][r] = __builtin_amdgcn_exp2f(fmaf(s[i][kb][r], scale_log2e, -mc));
-      // P^T fragments in fp16; the row sum is taken from the same fp16 values
-      // that enter the PV product (two per v_dot2_f32_f16)
-      float ls = 0.0f;
+        // P^T fragments in fp16; the row sum is taken from the same fp16
+        // values that enter the PV product (two per v_dot2_f32_f16)
+        float ls = 0.0f;
 #pragma unroll
-      for (int k2 = 0; k2 < 4; ++k2) {
-        const int kb = k2 >> 1, base = 8 * (k2 & 1);
+        for (int h = 0; h < 2; ++h) {
 #pragma unroll
-        for (int e = 0; e < 8; ++e) pf[i][k2][e] = (_Float16)s[i][kb][base + e];
+          for (int e = 0; e < 8; ++e) pf[i][h][e] = (_Float16)s[i][kb][8 * h + e];
 #pragma unroll
-        for (int e = 0; e < 8; e += 2) {
-          const f16x2 pair = {pf[i][k2][e], pf[i][k2][e + 1]};
-          ls = __builtin_amdgcn_fdot2(pair, kOnes2, ls, false);
+          for (int e = 0; e < 8; e += 2) {
+            const f16x2 pair = {pf[i][h][e], pf[i][h][e + 1]};
+            ls = __builtin_amdgcn_fdot2(pair, kOnes2, ls, false);
+          }
+        }
+        l[i] += ls;
+      }
+      // O^T[d][row] += V^T[d][keys] P^T[keys][row] for this half's 32 keys
+      TSR_PRIO_MFMA();
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int k2 = 2 * kb + h;
+#pragma unroll
+        for (int db = 0; db < 4; ++db) {
+          const uint16_t* vp = vs + (32 * db + lrow) * kVStr + 16 * k2 + 4 * lh;
+          Frag a;
+          const uint2 lo = *reinterpret_cast<const uint2*>(vp);
+          const uint2 hi = *reinterpret_cast<const uint2*>(vp + 8);
+          a.w[0] = lo.x; a.w[1] = lo.y; a.w[2] = hi.x; a.w[3] = hi.y;
+#pragma unroll
+          for (int i = 0; i < HPW; ++i)
+            o[i][db] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a.h, pf[i][h], o[i][db], 0, 0, 0);
         }
       }
-      l[i] += ls;
-    }
-
-    // O^T[d][row] += V^T[d][keys] P^T[keys][row]
-#pragma unroll
-    for (int k2 = 0; k2 < 4; ++k2) {
-#pragma unroll
-      for (int db = 0; db < 4; ++db) {
-        const uint16_t* vp = vs + (32 * db + lrow) * kVStr + 16 * k2 + 4 * lh;
-        Frag a;
-        const uint2 lo = *reinterpret_cast<const uint2*>(vp);
-        const uint2 hi = *reinterpret_cast<const uint2*>(vp + 8);
-        a.w[0] = lo.x; a.w[1] = lo.y; a.w[2] = hi.x; a.w[3] = hi.y;
-#pragma unroll
-        for (int i = 0; i < HPW; ++i)
-          o[i][db] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a.h, pf[i][k2], o[i][db], 0, 0, 0);
-      }
+      TSR_PRIO_VALU();
     }
   };
 
