@@ -124,8 +124,6 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
-typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
-constexpr f16x2 kOnes2 = {(_Float16)1.0f, (_Float16)1.0f};
 
 typedef int i32x4 __attribute__((ext_vector_type(4)));
 typedef i32x4 __attribute__((aligned(4))) i32x4u;
@@ -146,7 +144,11 @@ union Frag {
 constexpr int kD = 128;
 constexpr int kKT = kKvTile;           // keys per tile
 constexpr int kKStr = kD + 8;          // bf16 elements per K row in LDS
-constexpr int kVStr = kKT + 4;         // fp16 elements per V^T row in LDS
+// V^T rows (fp16) are 16-byte aligned and hold each 16-key step permuted as
+// keys [0..3, 8..11, 4..7, 12..15], so that the eight keys a lane feeds to
+// the PV MFMA (4h .. 4h+3 and 8+4h .. 8+4h+3 for half-wave h, the order in
+// which the S^T accumulators hand out P^T) are one 16-byte LDS read.
+constexpr int kVStr = kKT + 8;         // fp16 elements per V^T row in LDS
 constexpr int kKElems = kKT * kKStr;
 constexpr int kVElems = kD * kVStr;
 constexpr int kStage = kKElems + kVElems;
@@ -237,9 +239,9 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(
   // K: thread owns 16 bytes (dims 8*(tid%16) ..) of key 16*pb + tid/16 of
   //    block pb; the K tile is stored row-major.
   // V: thread owns 16 bytes (dims 8*(tid/16) ..) of keys 4*(tid%16) + pb, so
-  //    it writes four consecutive keys of each of its 8 dims to the
-  //    transposed V tile, and the 16 lanes of a group fill one 128-byte row
-  //    segment (no LDS bank conflicts).
+  //    it writes four consecutive keys (at their permuted place) of each of
+  //    its 8 dims to the transposed V tile, and the 16 lanes of a group fill
+  //    one 128-byte row segment (no LDS bank conflicts).
   uint4 kr[4], vr[4];
   const int kc8 = (tid & 15) * 8;
   const int vkg = tid & 15;
@@ -247,6 +249,7 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(
   const int koff = (tid >> 4) * kD + kc8;
   const int voff = 4 * (vkg & 3) * kD + vc8;
   const int vq = vkg >> 2;
+  const int vcol = 16 * vq + ((vkg & 1) << 3) + ((vkg & 2) << 1);
   auto load_tile = [&](int j) {
     const int key0 = j * kKT;
     int64_t base[4];
@@ -297,7 +300,7 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(
       const float f1 = bf16_to_f32((v1[e >> 1] >> sh) & 0xffffu);
       const float f2 = bf16_to_f32((v2[e >> 1] >> sh) & 0xffffu);
       const float f3 = bf16_to_f32((v3[e >> 1] >> sh) & 0xffffu);
-      *reinterpret_cast<uint2*>(vs + (vc8 + e) * kVStr + 4 * vkg) =
+      *reinterpret_cast<uint2*>(vs + (vc8 + e) * kVStr + vcol) =
           make_uint2(pack_f16x2(f0, f1), pack_f16x2(f2, f3));
     }
   };
@@ -384,20 +387,16 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(
 #pragma unroll
         for (int r = 0; r < 16; ++r)
           s[i][kb][r] = __builtin_amdgcn_exp2f(fmaf(s[i][kb][r], scale_log2e, -mc));
-        // P^T fragments in fp16; the row sum is taken from the same fp16
-        // values that enter the PV product (two per v_dot2_f32_f16)
-        float ls = 0.0f;
+        // row sum in fp32 from the unrounded P, as four independent chains
+        // of plain adds (v_dot2_f32_f16 stalls behind the matrix core)
+        float ls[4] = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-        for (int h = 0; h < 2; ++h) {
+        for (int r = 0; r < 16; ++r) ls[r & 3] += s[i][kb][r];
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
 #pragma unroll
           for (int e = 0; e < 8; ++e) pf[i][h][e] = (_Float16)s[i][kb][8 * h + e];
-#pragma unroll
-          for (int e = 0; e < 8; e += 2) {
-            const f16x2 pair = {pf[i][h][e], pf[i][h][e + 1]};
-            ls = __builtin_amdgcn_fdot2(pair, kOnes2, ls, false);
-          }
-        }
-        l[i] += ls;
+        l[i] += (ls[0] + ls[1]) + (ls[2] + ls[3]);
       }
       // O^T[d][row] += V^T[d][keys] P^T[keys][row] for this half's 32 keys
       TSR_PRIO_MFMA();
@@ -406,11 +405,8 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(
         const int k2 = 2 * kb + h;
 #pragma unroll
         for (int db = 0; db < 4; ++db) {
-          const uint16_t* vp = vs + (32 * db + lrow) * kVStr + 16 * k2 + 4 * lh;
           Frag a;
-          const uint2 lo = *reinterpret_cast<const uint2*>(vp);
-          const uint2 hi = *reinterpret_cast<const uint2*>(vp + 8);
-          a.w[0] = lo.x; a.w[1] = lo.y; a.w[2] = hi.x; a.w[3] = hi.y;
+          a.u = *reinterpret_cast<const uint4*>(vs + (32 * db + lrow) * kVStr + 16 * k2 + 8 * lh);
 #pragma unroll
           for (int i = 0; i < HPW; ++i)
             o[i][db] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a.h, pf[i][h], o[i][db], 0, 0, 0);
