@@ -368,13 +368,14 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(
       f16x8 pf[HPW][2];
 #pragma unroll
       for (int i = 0; i < HPW; ++i) {
+        // each half-wave holds half of every row's keys: the halves
+        // exchange their maxima only on the rare rescale path
         float mt = -INFINITY;
 #pragma unroll
         for (int r = 0; r < 16; ++r) mt = fmaxf(mt, s[i][kb][r]);
-        mt = fmaxf(mt, __shfl_xor(mt, 32));
         const bool grow = mt * scale_log2e > m[i] * scale_log2e + kLazy;
         if (__builtin_amdgcn_ballot_w64(grow)) {
-          const float mn = fmaxf(m[i], mt);
+          const float mn = fmaxf(m[i], fmaxf(mt, __shfl_xor(mt, 32)));
           const float alpha = __builtin_amdgcn_exp2f((m[i] - mn) * scale_log2e);
           m[i] = mn;
           l[i] *= alpha;

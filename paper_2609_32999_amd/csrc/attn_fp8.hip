@@ -36,7 +36,10 @@ union Frag8 {
 constexpr int kD = 128;
 constexpr int kKT = kKvTile;           // keys per tile
 constexpr int kKStr = kD + 16;         // bytes per e4m3 K row in LDS
-constexpr int kVStr = kKT + 4;         // fp16 elements per V^T row in LDS
+// V^T rows (fp16) are 16-byte aligned and hold each 16-key step permuted as
+// keys [0..3, 8..11, 4..7, 12..15], so that the eight keys a lane feeds to
+// the PV MFMA are one 16-byte LDS read (as in the bf16 kernel).
+constexpr int kVStr = kKT + 8;         // fp16 elements per V^T row in LDS
 constexpr int kKBytes = kKT * kKStr;
 constexpr int kVElems = kD * kVStr;
 constexpr float kLazy = 8.0f;          // lazy-rescale threshold (log2 units)
@@ -142,6 +145,7 @@ __global__ __launch_bounds__(256, 2) void attn_fp8_kernel(
   const int vkg = tid & 15;
   const int vc8 = (tid >> 4) * 8;
   const int vq = vkg >> 2;
+  const int vcol = 16 * vq + ((vkg & 1) << 3) + ((vkg & 2) << 1);   // permuted
   float nks[4], nvs[4];   // page scales of the staged tile (uniform)
   float tks[4];           // K page scales of the tile being computed
   auto load_tile = [&](int j) {
@@ -204,9 +208,9 @@ __global__ __launch_bounds__(256, 2) void attn_fp8_kernel(
         const f16x2 h01 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(p01, s, true);
         const f16x2 h23 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(p23, s, true);
         const int d = vc8 + 4 * half + 2 * e2;
-        *reinterpret_cast<uint2*>(vs + d * kVStr + 4 * vkg) =
+        *reinterpret_cast<uint2*>(vs + d * kVStr + vcol) =
             make_uint2(__builtin_bit_cast(uint32_t, l01), __builtin_bit_cast(uint32_t, l23));
-        *reinterpret_cast<uint2*>(vs + (d + 1) * kVStr + 4 * vkg) =
+        *reinterpret_cast<uint2*>(vs + (d + 1) * kVStr + vcol) =
             make_uint2(__builtin_bit_cast(uint32_t, h01), __builtin_bit_cast(uint32_t, h23));
       }
     }
@@ -228,27 +232,27 @@ __global__ __launch_bounds__(256, 2) void attn_fp8_kernel(
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
         const uint8_t* kp = ks + (32 * kb + lrow) * kKStr + 64 * kst + 32 * lh;
-        const uint4 x0 = *reinterpret_cast<const uint4*>(kp);
-        const uint4 x1 = *reinterpret_cast<const uint4*>(kp + 16);
-        const i32x8 a = {(int)x0.x, (int)x0.y, (int)x0.z, (int)x0.w,
-                         (int)x1.x, (int)x1.y, (int)x1.z, (int)x1.w};
+        // both 16-byte halves land in adjacent registers of the operand
+        union { uint4 u[2]; i32x8 v; } x;
+        x.u[0] = *reinterpret_cast<const uint4*>(kp);
+        x.u[1] = *reinterpret_cast<const uint4*>(kp + 16);
+        const i32x8 a = x.v;
 #pragma unroll
         for (int i = 0; i < HPW; ++i)
           s[i][kb] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
               a, qf[i][kst], s[i][kb], 0, 0, 0, 127, 0, 127);
       }
     }
-    // page of S register r of key block kb: 2*kb + r/8 within the tile
+    // page of S register r of key block kb: 2*kb + r/8 within the tile; its
+    // factor f (Q scale x K page scale x softmax scale x log2 e) is > 0, so
+    // each page's row max is f times the max of its raw scores, and P =
+    // exp2(f s - m) is one fma and one exp2 per score
     f16x8 pf[HPW][4];
 #pragma unroll
     for (int i = 0; i < HPW; ++i) {
       float f[4];
 #pragma unroll
       for (int b = 0; b < 4; ++b) f[b] = qs[i] * tks[b] * scale_log2e;
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) s[i][kb][r] *= f[2 * kb + (r >> 3)];
       if constexpr (MASK) {
         const int kbase = j * kKT;
 #pragma unroll
@@ -259,15 +263,21 @@ __global__ __launch_bounds__(256, 2) void attn_fp8_kernel(
             s[i][kb][r] = key > pos ? -INFINITY : s[i][kb][r];
           }
       }
-      float mt = -INFINITY;
+      float mb[4];
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
+      for (int b = 0; b < 4; ++b) {
+        const int kb = b >> 1, r0 = 8 * (b & 1);
+        float x = s[i][kb][r0];
 #pragma unroll
-        for (int r = 0; r < 16; ++r) mt = fmaxf(mt, s[i][kb][r]);
-      mt = fmaxf(mt, __shfl_xor(mt, 32));
-      // scores are in log2 units here; see attn.hip for the lazy rescale
+        for (int r = 1; r < 8; ++r) x = fmaxf(x, s[i][kb][r0 + r]);
+        mb[b] = x * f[b];
+      }
+      // each half-wave holds half of every row's keys: the halves exchange
+      // their maxima only on the rare rescale path (scores are in log2 units
+      // here; see attn.hip for the lazy rescale)
+      const float mt = fmaxf(fmaxf(mb[0], mb[1]), fmaxf(mb[2], mb[3]));
       if (__builtin_amdgcn_ballot_w64(mt > m[i] + kLazy)) {
-        const float mn = fmaxf(m[i], mt);
+        const float mn = fmaxf(m[i], fmaxf(mt, __shfl_xor(mt, 32)));
         const float alpha = __builtin_amdgcn_exp2f(m[i] - mn);
         m[i] = mn;
         l[i] *= alpha;
@@ -276,16 +286,17 @@ __global__ __launch_bounds__(256, 2) void attn_fp8_kernel(
 #pragma unroll
           for (int r = 0; r < 16; ++r) o[i][db][r] *= alpha;
       }
-      float ls = 0.0f;
+      // row sum in fp32 as four independent chains of plain adds
+      float ls[4] = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const float p = __builtin_amdgcn_exp2f(s[i][kb][r] - m[i]);
+          const float p = __builtin_amdgcn_exp2f(fmaf(s[i][kb][r], f[2 * kb + (r >> 3)], -m[i]));
           s[i][kb][r] = p;
-          ls += p;
+          ls[r & 3] += p;
         }
-      l[i] += ls;
+      l[i] += (ls[0] + ls[1]) + (ls[2] + ls[3]);
 #pragma unroll
       for (int k2 = 0; k2 < 4; ++k2) {
         const int kb = k2 >> 1, base = 8 * (k2 & 1);
@@ -297,11 +308,8 @@ __global__ __launch_bounds__(256, 2) void attn_fp8_kernel(
     for (int k2 = 0; k2 < 4; ++k2) {
 #pragma unroll
       for (int db = 0; db < 4; ++db) {
-        const uint16_t* vp = vs + (32 * db + lrow) * kVStr + 16 * k2 + 4 * lh;
         Frag8 a;
-        const uint2 lo = *reinterpret_cast<const uint2*>(vp);
-        const uint2 hi = *reinterpret_cast<const uint2*>(vp + 8);
-        a.w[0] = lo.x; a.w[1] = lo.y; a.w[2] = hi.x; a.w[3] = hi.y;
+        a.u = *reinterpret_cast<const uint4*>(vs + (32 * db + lrow) * kVStr + 16 * k2 + 8 * lh);
 #pragma unroll
         for (int i = 0; i < HPW; ++i)
           o[i][db] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a.h, pf[i][k2], o[i][db], 0, 0, 0);
