@@ -118,3 +118,75 @@ def test_fp8rag_full_size():
     for r in range(0, len(wl.requests), 3):
         check_request(run, r, kv_heads=sorted(heads.tolist()))
     assert check_retained(run) > 0
+
+
+@pytest.mark.parametrize("name", ["small_bf16", "small_fp8"])
+def test_compose_all_layers(name):
+    """One compose launch over three layers (the layer strides of the ABI).
+    Layer 0 holds the workload's pool, layer 1 its negation (sign bits
+    flipped: rotation, rounding and e4m3 re-quantization are odd functions,
+    so layer 1's composed pages are exactly the negation of layer 0's), layer
+    2 a second copy of layer 0.  Layer 0 is checked against the oracle at
+    every position compose writes."""
+    from oracle.compose import assemble_request_kv, assemble_request_kv_e4m3
+    from oracle.numerics import e4m3_decode
+    from paper_2609_32999_amd import staging
+    from paper_2609_32999_amd.session import Session
+    wl = workloads.generate(name)
+    s = Session(wl.model, wl.n_pool_pages, wl.n_req_pages, n_layers=3)
+    staging.upload_pool(s, wl, layer=0)
+    for src in (s.pool_k, s.pool_v):
+        if s.e4m3:
+            src[1].copy_(src[0] ^ 0x80)
+        else:
+            src[1].view(torch.int16).copy_(src[0].view(torch.int16) ^ -0x8000)
+        src[2].copy_(src[0])
+    if s.e4m3:
+        s.pool_scale[1].copy_(s.pool_scale[0])
+        s.pool_scale[2].copy_(s.pool_scale[0])
+    plan = s.plan(wl.requests)
+    s.compose(plan, layer="all")
+    torch.cuda.synchronize()
+    for r in range(len(wl.requests)):
+        cached = _gathered_positions(wl, r)
+        got = [staging.request_kv(s, wl, r, layer=l) for l in range(3)]
+        if s.e4m3:
+            want = assemble_request_kv_e4m3(wl, r)
+            dec = [lambda x: e4m3_decode(x), lambda x: e4m3_decode(x), None, None]
+            for f in range(4):
+                a, b = got[0][f][cached], want[f][cached]
+                if dec[f]:
+                    a, b = dec[f](a), dec[f](b)
+                assert np.array_equal(a, b), f"request {r} field {f} differs from the oracle"
+            for l, sg in ((1, -1.0), (2, 1.0)):
+                for f in range(2):
+                    assert np.array_equal(e4m3_decode(got[l][f][cached]),
+                                          sg * e4m3_decode(got[0][f][cached])), f"layer {l}"
+                for f in range(2, 4):
+                    assert np.array_equal(got[l][f][cached], got[0][f][cached]), f"layer {l} scales"
+        else:
+            K, V, source = assemble_request_kv(wl, r)
+            assert np.array_equal(cached, source == "gather")
+            k0, v0 = got[0]
+            assert np.array_equal(k0[cached].view(np.uint32), K[cached].view(np.uint32)), "K"
+            assert np.array_equal(v0[cached].view(np.uint32), V[cached].view(np.uint32)), "V"
+            for l, sg in ((1, -1.0), (2, 1.0)):
+                kl, vl = got[l]
+                assert np.array_equal(kl[cached], sg * k0[cached]), f"layer {l} K"
+                assert np.array_equal(vl[cached], sg * v0[cached]), f"layer {l} V"
+    say(f"[gpu] {name}: three-layer compose matches")
+
+
+def _gathered_positions(wl, r):
+    """Prompt positions of request r that compose writes (HIT tokens past the
+    recompute window)."""
+    from oracle import layout as L
+    req = wl.requests[r]
+    computed = set(int(p) for p in L.compute_positions(req))
+    cached = np.zeros(req.prompt_len, dtype=bool)
+    for u in req.units:
+        if u.residency == 1:
+            for j in range(u.n_tokens):
+                if u.position + j not in computed:
+                    cached[u.position + j] = True
+    return cached
