@@ -34,6 +34,40 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
+def measured_peaks(torch):
+    """Achievable rates on this GPU, as context for the published peaks: a
+    1 GiB device-to-device copy (read + write bytes) and a bf16 8192^3
+    matrix product (the vendor GEMM library through torch.matmul)."""
+    ev = lambda: torch.cuda.Event(enable_timing=True)
+    a = torch.empty(1 << 30, dtype=torch.uint8, device="cuda").fill_(1)
+    b = torch.empty_like(a)
+    b.copy_(a)
+    t0, t1 = ev(), ev()
+    t0.record()
+    for _ in range(5):
+        b.copy_(a)
+    t1.record()
+    torch.cuda.synchronize()
+    copy_gbps = 5 * 2 * a.numel() / (t0.elapsed_time(t1) * 1e-3) / 1e9
+    del a, b
+    n = 8192
+    x = torch.randn(n, n, device="cuda", dtype=torch.bfloat16)
+    y = torch.randn(n, n, device="cuda", dtype=torch.bfloat16)
+    z = x @ y
+    t0, t1 = ev(), ev()
+    t0.record()
+    for _ in range(5):
+        z = x @ y
+    t1.record()
+    torch.cuda.synchronize()
+    gemm_tflops = 5 * 2.0 * n ** 3 / (t0.elapsed_time(t1) * 1e-3) / 1e12
+    del x, y, z
+    torch.cuda.empty_cache()
+    log(f"[bench] measured peaks: copy {copy_gbps:.0f} GB/s, bf16 GEMM {gemm_tflops:.0f} TFLOP/s")
+    return {"copy_gbps": copy_gbps, "bf16_gemm_tflops": gemm_tflops,
+            "how": "1 GiB device copy x5 (read+write bytes); torch.matmul bf16 8192^3 x5"}
+
+
 def kv_elem_bytes(dtype):
     return {"f32": 4, "bf16": 2, "e4m3": 1}[dtype]
 
@@ -89,6 +123,12 @@ def main():
     ap.add_argument("--workload", default="rag8b")
     ap.add_argument("--layers", type=int, default=8)
     ap.add_argument("--cpu-requests", type=int, default=6)
+    ap.add_argument("--scope", choices=["global", "local"], default="global",
+                    help="miss scope: global (every missing-unit token attends to the "
+                         "whole prompt) or local (missing units attend within themselves "
+                         "past their recompute window)")
+    ap.add_argument("--no-peaks", dest="peaks", action="store_false",
+                    help="skip measuring the achievable copy and bf16 GEMM rates")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="run one plain device copy of this size first (to scale "
@@ -104,6 +144,8 @@ def main():
     from paper_2609_32999_amd import staging
     from paper_2609_32999_amd.session import Session
 
+    measured = measured_peaks(torch) if args.peaks else None
+
     if args.calib_copy_mib:
         n = args.calib_copy_mib << 20
         a = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)
@@ -114,7 +156,7 @@ def main():
         log(f"[bench] calibration copy of {args.calib_copy_mib} MiB done")
         del a, b
 
-    wl = workloads.generate(args.workload)
+    wl = workloads.make_workload(workloads.get_config(args.workload).with_(miss_scope=args.scope))
     m = wl.model
     L = args.layers
     log(f"[bench] workload={wl.name} layers={L} prompt_tokens={wl.prompt_tokens}")
@@ -207,7 +249,8 @@ def main():
     gather_bytes = 2 * plan.num_gather_tokens * row_bytes   # read + write
     append_bytes = 2 * T * row_bytes
     retain_bytes = 2 * plan.num_retain_tokens * row_bytes
-    visible = int((pos.astype(np.int64) + 1).sum())
+    kv_lo = plan.row_kv_lo()
+    visible = int((pos.astype(np.int64) - kv_lo + 1).sum())
     attn_flops = 4.0 * m.head_dim * m.n_q_heads * visible
     attn_tflops = attn_flops / (attn_ms * 1e-3) / 1e12
     compose_gbs = gather_bytes / (compose_ms * 1e-3) / 1e9
@@ -232,6 +275,7 @@ def main():
             "requests": len(wl.requests), "prompt_tokens": wl.prompt_tokens,
             "computed_tokens": T, "gathered_tokens": plan.num_gather_tokens,
             "retained_tokens": plan.num_retain_tokens, "layer_buffer_sets": L,
+            "miss_scope": args.scope,
             "seed": wl.seed,
         },
         "computed_tokens_per_s": T / (ms * 1e-3),
@@ -254,6 +298,10 @@ def main():
         "append_gbps": append_bytes / (append_ms * 1e-3) / 1e9,
         "retain_gbps": retain_bytes / (retain_ms * 1e-3) / 1e9 if retain_ms > 0 else None,
     }
+    if measured:
+        rec["measured_peaks"] = measured
+        rec["roofline"]["frac_of_measured"] = attn_tflops / measured["bf16_gemm_tflops"]
+        rec["roofline_compose"]["frac_of_measured"] = compose_gbs / measured["copy_gbps"]
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle baseline")
         rec["cpu_baseline"] = cpu_baseline(wl, min(args.cpu_requests, len(wl.requests)))

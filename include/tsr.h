@@ -48,7 +48,7 @@
 extern "C" {
 #endif
 
-#define TSR_ABI_VERSION 1
+#define TSR_ABI_VERSION 2
 
 typedef enum {
   TSR_OK = 0,
@@ -63,6 +63,19 @@ typedef enum { TSR_F32 = 0, TSR_BF16 = 1, TSR_E4M3 = 2 } tsr_dtype;
 /* Preparation of a unit (Section 5.1, per-unit plan): a state used from a
  * cache tier is a HIT; a state computed from text is a MISS. */
 typedef enum { TSR_MISS = 0, TSR_HIT = 1 } tsr_residency;
+
+/* Which keys the rows of a MISS unit see (Section 5.3).
+ *   TSR_SCOPE_GLOBAL  every token of a MISS unit is a row of the final pass
+ *                     and sees the whole assembled prompt up to itself.
+ *   TSR_SCOPE_LOCAL   the paper's preparation of a miss: the unit is
+ *                     prefilled on its own and then composed like a hit.
+ *                     Its first min(n_recompute, n) tokens (the recompute
+ *                     window) are rows of the final pass over the whole
+ *                     prompt; its remaining tokens are rows that see only
+ *                     the keys of their own unit (evaluated at their final
+ *                     positions, which RoPE's relative property makes equal
+ *                     to a prefill from position 0). */
+typedef enum { TSR_SCOPE_GLOBAL = 0, TSR_SCOPE_LOCAL = 1 } tsr_miss_scope;
 
 /* Shape and numerics of one attention layer.
  *   (kv_dtype, act_dtype) in {(F32, F32), (BF16, BF16), (E4M3, BF16)}.
@@ -95,9 +108,10 @@ typedef struct {
  *   n_tokens     unit length n > 0.
  *   residency    TSR_HIT: its cached state (keys before RoPE, values) is in
  *                pool_pages; TSR_MISS: it is computed in this pass.
- *   n_recompute  HIT only: the composition policy recomputes the first
- *                min(n_recompute, n) tokens (a fixed chunk-initial window,
- *                Section 7); they become computed rows.
+ *   n_recompute  the composition policy recomputes the first
+ *                min(n_recompute, n) tokens of a HIT (a fixed chunk-initial
+ *                window, Section 7); they become computed rows.  Under
+ *                TSR_SCOPE_LOCAL the same window applies to a MISS unit.
  *   retain       MISS only: 1 writes the computed state into pool_pages.
  *   pool_pages   host array of ceil(n / page_size) pool page ids: the source
  *                of a HIT, the destination of a retained MISS, else unused
@@ -115,6 +129,8 @@ typedef struct {
 
 /* One request: an ordered prompt tiled exactly once by its units and text
  * segments (instruction, separators, query), and its request KV pages.
+ *   miss_scope   a tsr_miss_scope value; 0 (the global scope) for structs
+ *                that are zero-initialised.
  *   text_segs    host array [n_text][2] of {start, length}, length > 0.
  *   block_table  host array of ceil(prompt_len / page_size) request page ids,
  *                not shared with any other request of the batch. */
@@ -123,7 +139,7 @@ typedef struct {
   int32_t n_units;
   const tsr_unit* units;
   int32_t n_text;
-  int32_t reserved;
+  int32_t miss_scope;
   const int32_t* text_segs;
   const int32_t* block_table;
 } tsr_request;
@@ -185,6 +201,11 @@ tsr_status tsr_plan_compute_positions(const tsr_plan* plan,
                                       int32_t* host_positions,
                                       int32_t* host_requests);
 
+/* First visible key position of every computed row, in plan order
+ * (host_kv_lo [T]): 0, or under TSR_SCOPE_LOCAL the first position of the
+ * unit of a MISS token past its recompute window. */
+tsr_status tsr_plan_row_kv_lo(const tsr_plan* plan, int32_t* host_kv_lo);
+
 void tsr_plan_destroy(tsr_plan* plan);
 
 /* ------------------------------------------------------------ hot path */
@@ -212,9 +233,11 @@ tsr_status tsr_compose_kv(const tsr_plan* plan, const void* pool_k,
 /* Final extend pass (Section 5.3, "Completing prefill"):
  *   1. for every computed row t at position p_t: k_rot = RoPE(k_t, p_t) and
  *      v_t are written to the request pages at p_t;
- *   2. o_t,h = softmax(scale * q_rot . K_req[0..p_t, g]^T) V_req[0..p_t, g],
+ *   2. o_t,h = softmax(scale * q_rot . K_req[lo_t..p_t, g]^T) V_req[lo_t..p_t, g],
  *      q_rot = RoPE(q_t,h, p_t) rounded to act_dtype, g = h / (H_q / H_kv),
- *      causal by absolute position (a key at p_t itself is visible).
+ *      causal by absolute position (a key at p_t itself is visible); lo_t
+ *      is 0 except for the unit-local rows of TSR_SCOPE_LOCAL (see
+ *      tsr_plan_row_kv_lo).
  *   q    device [T][H_q][d], k/v device [T][H_kv][d]: pre-RoPE, act dtype.
  *   out  device [T][H_q][d] of act_dtype.
  *   lse  device [T][H_q] fp32 natural-log sum of exp(scale * s), or NULL.

@@ -7,7 +7,8 @@ Definition used (readings for what the paper leaves unstated):
 
 * query head h uses KV head g = floor(h / G), G = H_q / H_kv (contiguous
   grouping, as in Llama-family GQA);
-* a token at prompt position p sees keys at positions 0 .. p inclusive;
+* a token at prompt position p sees keys at positions lo .. p inclusive,
+  lo = 0 except for the unit-local rows of LOCAL miss scope (layout.py);
 * s_j = scale * <q, k_j>, scale = 1/sqrt(d) unless given;
 * o = sum_j softmax(s)_j v_j, lse = logsumexp(s) (natural log);
 * everything in fp64, on operands already rounded to the dtypes the GPU
@@ -25,8 +26,11 @@ import math
 import numpy as np
 
 
-def causal_gqa_attention(q, positions, K, V, scale=None, row_block: int = 1024):
+def causal_gqa_attention(q, positions, K, V, scale=None, row_block: int = 1024,
+                         kv_lo=None):
     """q [T][H_q][d], positions [T], K/V [P][H_kv][d] -> out [T][H_q][d], lse [T][H_q].
+
+    kv_lo [T] (optional): first visible key of every row (default 0).
 
     All arithmetic in fp64.  Rows are evaluated in blocks of `row_block`
     only to bound memory; every row is independent.
@@ -46,12 +50,15 @@ def causal_gqa_attention(q, positions, K, V, scale=None, row_block: int = 1024):
     lse = np.zeros((T, Hq), dtype=np.float64)
     if T == 0:
         return out, lse
+    lo_all = (np.zeros(T, dtype=np.int64) if kv_lo is None
+              else np.asarray(kv_lo, dtype=np.int64))
     P = int(positions.max()) + 1
     key_pos = np.arange(P)
     for r0 in range(0, T, row_block):
         rows = slice(r0, min(T, r0 + row_block))
         pr = positions[rows]
-        visible = key_pos[None, :] <= pr[:, None]          # [t][P]
+        visible = ((key_pos[None, :] <= pr[:, None]) &
+                   (key_pos[None, :] >= lo_all[rows][:, None]))   # [t][P]
         for h in range(Hq):
             g = h // G
             s = scale * (q[rows, h, :] @ K[:P, g, :].T)      # [t][P]
@@ -64,7 +71,7 @@ def causal_gqa_attention(q, positions, K, V, scale=None, row_block: int = 1024):
     return out, lse
 
 
-def brute_force_attention(q, positions, K, V, scale=None):
+def brute_force_attention(q, positions, K, V, scale=None, kv_lo=None):
     """Same definition with explicit Python loops (tiny inputs only)."""
     T, Hq, d = len(q), len(q[0]), len(q[0][0])
     Hkv = len(K[0])
@@ -75,10 +82,12 @@ def brute_force_attention(q, positions, K, V, scale=None):
     lse = [[0.0] * Hq for _ in range(T)]
     for t in range(T):
         p = int(positions[t])
+        lo = 0 if kv_lo is None else int(kv_lo[t])
+        keys = list(range(lo, p + 1))
         for h in range(Hq):
             g = h // G
             scores = []
-            for j in range(p + 1):
+            for j in keys:
                 acc = 0.0
                 for c in range(d):
                     acc += float(q[t][h][c]) * float(K[j][g][c])
@@ -87,6 +96,6 @@ def brute_force_attention(q, positions, K, V, scale=None):
             w = [math.exp(s - mx) for s in scores]
             tot = sum(w)
             for c in range(d):
-                out[t][h][c] = sum(w[j] * float(V[j][g][c]) for j in range(p + 1)) / tot
+                out[t][h][c] = sum(w[i] * float(V[j][g][c]) for i, j in enumerate(keys)) / tot
             lse[t][h] = mx + math.log(tot)
     return np.array(out), np.array(lse)

@@ -13,7 +13,14 @@ Readings (the paper does not spell these out):
 * the composition policy is EPIC's fixed chunk-initial window (Section 7):
   the first min(r, n) tokens of every reused unit are recomputed;
 * with GLOBAL miss scope, every token of a computed (MISS) unit is a row of
-  the final causal pass over the whole assembled prompt.
+  the final causal pass over the whole assembled prompt;
+* with LOCAL miss scope (the paper's own semantics, Section 5.3: missing
+  units are prefilled independently, then composed like hits), a MISS
+  unit's tokens past its recompute window see only the keys of their own
+  unit; the window (the first min(r, n) tokens, as for a HIT) and the text
+  tokens are rows of the final pass over the whole prompt.  The unit's
+  independent prefill is evaluated at its final positions: by the relative
+  property of RoPE this equals a prefill from position 0 (pinned).
 
 Pins: the worked example of Section 2.2 (Doc B at positions 150-249 in one
 prompt and 50-149 in the other), ceil(n/B) page counts, and set algebra
@@ -76,6 +83,33 @@ def compute_positions(req) -> np.ndarray:
         else:
             pos.extend(range(s, s + recompute_count(u)))
     return np.asarray(sorted(pos), dtype=np.int64)
+
+
+GLOBAL = 0
+LOCAL = 1
+
+
+def miss_scope(req) -> int:
+    """GLOBAL (default) or LOCAL miss scope of a request."""
+    return int(getattr(req, "miss_scope", GLOBAL))
+
+
+def row_kv_lo(req) -> np.ndarray:
+    """First visible key position of every computed row (compute_positions
+    order): 0, except under LOCAL scope for a MISS unit's tokens past its
+    recompute window, which see only their own unit."""
+    pos = compute_positions(req)
+    lo = np.zeros(len(pos), dtype=np.int64)
+    if miss_scope(req) != LOCAL:
+        return lo
+    for u in req.units:
+        if u.residency != MISS:
+            continue
+        r = min(int(u.n_recompute), int(u.n_tokens))
+        start, end = int(u.position) + r, int(u.position) + int(u.n_tokens)
+        sel = (pos >= start) & (pos < end)
+        lo[sel] = int(u.position)
+    return lo
 
 
 def gather_tokens(req) -> list[tuple[int, int, int]]:

@@ -33,6 +33,7 @@ class RequestResult:
     lse: np.ndarray            # fp64 [T_r][h_q]
     kv_heads: np.ndarray
     q_heads: np.ndarray
+    kv_lo: np.ndarray          # first visible key of every row
 
 
 def run_request(wl, r: int, kv_heads=None, scale=None) -> RequestResult:
@@ -49,8 +50,9 @@ def run_request(wl, r: int, kv_heads=None, scale=None) -> RequestResult:
     else:
         K, V, src = assemble_request_kv(wl, r, kvh)
         cpos, q = rotated_queries(wl, r, qh)
-    out, lse = causal_gqa_attention(q, cpos, K, V, scale=scale)
-    return RequestResult(cpos, K, V, src, q, out, lse, kvh, qh)
+    lo = L.row_kv_lo(wl.requests[r])
+    out, lse = causal_gqa_attention(q, cpos, K, V, scale=scale, kv_lo=lo)
+    return RequestResult(cpos, K, V, src, q, out, lse, kvh, qh, lo)
 
 
 def run(wl, requests=None, kv_heads=None, scale=None):
@@ -77,6 +79,20 @@ def full_prefill(wl, r: int, scale=None):
     return causal_gqa_attention(qr, pos, kr, v, scale=scale)
 
 
+def unit_prefill(wl, r: int, ui: int, scale=None):
+    """Independent causal prefill of unit ui of request r from position 0
+    (its tokens only, rotated at 0 .. n-1), as the paper prepares a missing
+    unit (Section 5.3); used to pin the LOCAL miss scope."""
+    m = wl.model
+    u = wl.requests[r].units[ui]
+    n = int(u.n_tokens)
+    q, k, v = wl.fresh(r, np.arange(u.position, u.position + n))
+    pos = np.arange(n)
+    qr = round_storage(rope_fp32(q, pos, m.rope_theta), m.act_dtype)
+    kr = round_storage(rope_fp32(k, pos, m.rope_theta), m.kv_dtype)
+    return causal_gqa_attention(qr, pos, kr, v, scale=scale)
+
+
 def counts(wl):
     """Algorithmic counts of the path on a workload (per layer).
 
@@ -88,7 +104,7 @@ def counts(wl):
         g += len(L.gather_tokens(req))
         cp = L.compute_positions(req)
         c += len(cp)
-        vis += int((cp + 1).sum())
+        vis += int((cp - L.row_kv_lo(req) + 1).sum())
         rt += len(L.retain_tokens(req, wl.model.page_size))
     return dict(gather_tokens=g, compute_tokens=c, retain_tokens=rt,
                 prompt_tokens=wl.prompt_tokens, visible_pairs=vis)

@@ -23,6 +23,7 @@ STATUS_NAMES = {0: "OK", 1: "INVALID_ARG", 2: "UNSUPPORTED", 3: "OUT_OF_RANGE", 
 TSR_F32, TSR_BF16, TSR_E4M3 = 0, 1, 2
 DTYPE_CODES = {"f32": TSR_F32, "bf16": TSR_BF16, "e4m3": TSR_E4M3}
 TSR_MISS, TSR_HIT = 0, 1
+TSR_SCOPE_GLOBAL, TSR_SCOPE_LOCAL = 0, 1
 
 # Every symbol include/tsr.h declares.
 EXPORTS = (
@@ -30,7 +31,7 @@ EXPORTS = (
     "tsr_rope_table_init", "tsr_plan_workspace_size", "tsr_plan_create",
     "tsr_plan_num_compute_tokens", "tsr_plan_num_gather_tokens",
     "tsr_plan_num_retain_tokens", "tsr_plan_num_attn_items",
-    "tsr_plan_compute_positions", "tsr_plan_destroy", "tsr_compose_kv",
+    "tsr_plan_compute_positions", "tsr_plan_row_kv_lo", "tsr_plan_destroy", "tsr_compose_kv",
     "tsr_prefill_attn", "tsr_append_kv", "tsr_attn", "tsr_retain_kv",
 )
 
@@ -60,7 +61,7 @@ class tsr_unit(ctypes.Structure):
 class tsr_request(ctypes.Structure):
     _fields_ = [("prompt_len", c_int32), ("n_units", c_int32),
                 ("units", POINTER(tsr_unit)), ("n_text", c_int32),
-                ("reserved", c_int32), ("text_segs", POINTER(c_int32)),
+                ("miss_scope", c_int32), ("text_segs", POINTER(c_int32)),
                 ("block_table", POINTER(c_int32))]
 
 
@@ -91,6 +92,7 @@ def lib():
             "tsr_plan_num_retain_tokens": (c_int32, [P]),
             "tsr_plan_num_attn_items": (c_int32, [P]),
             "tsr_plan_compute_positions": (c_int32, [P, POINTER(c_int32), POINTER(c_int32)]),
+            "tsr_plan_row_kv_lo": (c_int32, [P, POINTER(c_int32)]),
             "tsr_plan_destroy": (None, [P]),
             "tsr_compose_kv": (c_int32, [P, P, P, P, P, P, P, c_int32, c_int64, c_int64, P]),
             "tsr_prefill_attn": (c_int32, [P, P, P, P, P, P, P, P, P, P]),
@@ -148,8 +150,9 @@ class RequestBatch:
 
     Each request needs `prompt_len`, `units` (objects with unit_id, position,
     n_tokens, residency, n_recompute, retain, pool_pages), `text_segs`
-    ([(start, length)]) and `block_table`.  The arrays stay alive as long as
-    this object.
+    ([(start, length)]) and `block_table`, and may carry `miss_scope`
+    (TSR_SCOPE_GLOBAL when absent).  The arrays stay alive as long as this
+    object.
     """
 
     def __init__(self, requests):
@@ -169,7 +172,8 @@ class RequestBatch:
             segs = np.ascontiguousarray(np.asarray(r.text_segs, dtype=np.int32).reshape(-1, 2))
             bt = np.ascontiguousarray(r.block_table, dtype=np.int32)
             self._keep += [units, segs, bt]
-            arr[i] = tsr_request(int(r.prompt_len), len(r.units), units, len(segs), 0,
+            arr[i] = tsr_request(int(r.prompt_len), len(r.units), units, len(segs),
+                                 int(getattr(r, "miss_scope", TSR_SCOPE_GLOBAL)),
                                  segs.ctypes.data_as(POINTER(c_int32)),
                                  bt.ctypes.data_as(POINTER(c_int32)))
         self.array = arr
@@ -225,6 +229,13 @@ class Plan:
             self.handle, pos.ctypes.data_as(POINTER(c_int32)),
             req.ctypes.data_as(POINTER(c_int32))))
         return pos[:T], req[:T]
+
+    def row_kv_lo(self):
+        """First visible key position of every computed row (plan order)."""
+        T = self.num_compute_tokens
+        lo = np.empty(max(T, 1), dtype=np.int32)
+        _check(lib().tsr_plan_row_kv_lo(self.handle, lo.ctypes.data_as(POINTER(c_int32))))
+        return lo[:T]
 
     def destroy(self) -> None:
         if self.handle:

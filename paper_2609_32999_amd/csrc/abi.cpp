@@ -205,6 +205,15 @@ tsr_status tsr_plan_compute_positions(const tsr_plan* p, int32_t* host_positions
   return TSR_OK;
 }
 
+tsr_status tsr_plan_row_kv_lo(const tsr_plan* p, int32_t* host_kv_lo) {
+  if (!p || !host_kv_lo) {
+    set_error("plan or host_kv_lo is NULL");
+    return TSR_ERR_INVALID_ARG;
+  }
+  if (p->T) std::memcpy(host_kv_lo, p->row_lo.data(), p->T * sizeof(int32_t));
+  return TSR_OK;
+}
+
 void tsr_plan_destroy(tsr_plan* p) { delete p; }
 
 tsr_status tsr_compose_kv(const tsr_plan* p, const void* pool_k,

@@ -89,7 +89,7 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(
       }
       __syncthreads();
       float m = -INFINITY, l = 0.0f, o = 0.0f;
-      for (int k0 = 0; k0 <= pos; k0 += 256) {
+      for (int k0 = it.kv_lo; k0 <= pos; k0 += 256) {
         const int k = k0 + t;
         float s = -INFINITY;
         if (k <= pos) {
@@ -353,7 +353,7 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
             const int key = kbase + 32 * kb + 8 * (r >> 2) + 4 * lh + (r & 3);
-            s[i][kb][r] = key > pos ? -INFINITY : s[i][kb][r];
+            s[i][kb][r] = (key > pos || key < it.kv_lo) ? -INFINITY : s[i][kb][r];
           }
     }
 
@@ -384,7 +384,9 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(
 #pragma unroll
             for (int r = 0; r < 16; ++r) o[i][db][r] *= alpha;
         }
-        const float mc = m[i] * scale_log2e;
+        // a half with no visible key yet leaves m at -inf (all its scores
+        // are -inf too): exponentiate against 0 so that P = 0, not NaN
+        const float mc = m[i] == -INFINITY ? 0.0f : m[i] * scale_log2e;
 #pragma unroll
         for (int r = 0; r < 16; ++r)
           s[i][kb][r] = __builtin_amdgcn_exp2f(fmaf(s[i][kb][r], scale_log2e, -mc));
@@ -417,26 +419,27 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(
     }
   };
 
+  // keys kv_lo .. kv_len-1: tiles j0 .. ntiles-1.  A tile needs the mask
+  // when it reaches past the smallest row position or starts below kv_lo.
   const int ntiles = (it.kv_len + kKT - 1) / kKT;
-  // tiles whose last key is <= the smallest row position need no mask
-  const int nfull = min(ntiles, (it.min_pos + 1) / kKT);
-  load_tile(0);
-  store_tile(0);
+  const int j0 = it.kv_lo / kKT;
+  const int jlo = min(ntiles, (it.kv_lo + kKT - 1) / kKT);   // first tile without keys < kv_lo
+  const int nfull = min(ntiles, (it.min_pos + 1) / kKT);      // tiles ending at or before min_pos
+  auto run_tiles = [&](int ja, int jb, auto mask_tag) {
+    for (int j = ja; j < jb; ++j) {
+      const bool more = j + 1 < ntiles;
+      if (more) load_tile(j + 1);
+      tile(j, mask_tag);
+      if (more) store_tile((j + 1) & 1);
+      __syncthreads();
+    }
+  };
+  load_tile(j0);
+  store_tile(j0 & 1);
   __syncthreads();
-  for (int j = 0; j < nfull; ++j) {
-    const bool more = j + 1 < ntiles;
-    if (more) load_tile(j + 1);
-    tile(j, std::false_type{});
-    if (more) store_tile((j + 1) & 1);
-    __syncthreads();
-  }
-  for (int j = nfull; j < ntiles; ++j) {
-    const bool more = j + 1 < ntiles;
-    if (more) load_tile(j + 1);
-    tile(j, std::true_type{});
-    if (more) store_tile((j + 1) & 1);
-    __syncthreads();
-  }
+  run_tiles(j0, jlo, std::true_type{});
+  run_tiles(jlo, max(jlo, nfull), std::false_type{});
+  run_tiles(max(jlo, nfull), ntiles, std::true_type{});
 
   // ---- epilogue: normalise, round to bf16, store rows of this tile
 #pragma unroll

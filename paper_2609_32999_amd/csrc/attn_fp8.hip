@@ -260,7 +260,7 @@ __global__ __launch_bounds__(256, 2) void attn_fp8_kernel(
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
             const int key = kbase + 32 * kb + 8 * (r >> 2) + 4 * lh + (r & 3);
-            s[i][kb][r] = key > pos ? -INFINITY : s[i][kb][r];
+            s[i][kb][r] = (key > pos || key < it.kv_lo) ? -INFINITY : s[i][kb][r];
           }
       }
       float mb[4];
@@ -286,13 +286,15 @@ __global__ __launch_bounds__(256, 2) void attn_fp8_kernel(
 #pragma unroll
           for (int r = 0; r < 16; ++r) o[i][db][r] *= alpha;
       }
-      // row sum in fp32 as four independent chains of plain adds
+      // row sum in fp32 as four independent chains of plain adds; a row with
+      // no visible key yet keeps m at -inf and is exponentiated against 0
+      const float mi = m[i] == -INFINITY ? 0.0f : m[i];
       float ls[4] = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const float p = __builtin_amdgcn_exp2f(fmaf(s[i][kb][r], f[2 * kb + (r >> 3)], -m[i]));
+          const float p = __builtin_amdgcn_exp2f(fmaf(s[i][kb][r], f[2 * kb + (r >> 3)], -mi));
           s[i][kb][r] = p;
           ls[r & 3] += p;
         }
@@ -317,17 +319,21 @@ __global__ __launch_bounds__(256, 2) void attn_fp8_kernel(
     }
   };
 
+  // keys kv_lo .. kv_len-1: tiles j0 .. ntiles-1; a tile needs the mask when
+  // it reaches past the smallest row position or starts below kv_lo
   const int ntiles = (it.kv_len + kKT - 1) / kKT;
+  const int j0 = it.kv_lo / kKT;
+  const int jlo = (it.kv_lo + kKT - 1) / kKT;
   const int nfull = min(ntiles, (it.min_pos + 1) / kKT);
-  load_tile(0);
-  store_tile(0);
+  load_tile(j0);
+  store_tile(j0 & 1);
 #pragma unroll
   for (int b = 0; b < 4; ++b) tks[b] = nks[b];
   __syncthreads();
-  for (int j = 0; j < ntiles; ++j) {
+  for (int j = j0; j < ntiles; ++j) {
     const bool more = j + 1 < ntiles;
     if (more) load_tile(j + 1);
-    if (j < nfull)
+    if (j >= jlo && j < nfull)
       tile(j, std::false_type{});
     else
       tile(j, std::true_type{});

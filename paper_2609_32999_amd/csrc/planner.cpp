@@ -116,6 +116,7 @@ tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
   std::vector<int32_t> bt_off(n_req), bt_len(n_req), req_row0(n_req + 1, 0);
   p->row_pos.clear();
   p->row_req.clear();
+  p->row_lo.clear();
 
   std::vector<uint8_t> req_page_used((size_t)n_req_pages, 0);
   // pool pages: bit 1 = read by a HIT, bit 2 = written by a retained MISS
@@ -133,6 +134,11 @@ tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
           << " exceeds max_position " << m.max_position;
       return fail(TSR_ERR_OUT_OF_RANGE, err.str());
     }
+    if (q.miss_scope != TSR_SCOPE_GLOBAL && q.miss_scope != TSR_SCOPE_LOCAL) {
+      err << "request " << r << ": miss_scope must be TSR_SCOPE_GLOBAL or TSR_SCOPE_LOCAL";
+      return fail(TSR_ERR_INVALID_ARG, err.str());
+    }
+    const bool local = q.miss_scope == TSR_SCOPE_LOCAL;
     if (q.n_units < 0 || q.n_text < 0 || (q.n_units && !q.units) ||
         (q.n_text && !q.text_segs) || !q.block_table) {
       err << "request " << r << ": null or negative-size member";
@@ -219,6 +225,7 @@ tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
           rows.push_back({req_slot(s.start + j), s.start + j});
           p->row_pos.push_back(s.start + j);
           p->row_req.push_back(r);
+          p->row_lo.push_back(0);
         }
         continue;
       }
@@ -231,7 +238,7 @@ tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
         err << "request " << r << " unit " << s.unit << ": retain must be 0 or 1";
         return fail(TSR_ERR_INVALID_ARG, err.str());
       }
-      if (u.residency == TSR_HIT && u.n_recompute < 0) {
+      if ((u.residency == TSR_HIT || local) && u.n_recompute < 0) {
         err << "request " << r << " unit " << s.unit << ": n_recompute < 0";
         return fail(TSR_ERR_INVALID_ARG, err.str());
       }
@@ -277,10 +284,14 @@ tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
             rpages.push_back({row0 + j, u.pool_pages[j / B], u.position + j,
                               std::min(B, u.n_tokens - j)});
       }
+      // under the local scope a MISS unit's tokens past its recompute window
+      // see only their own unit
+      const int32_t wnd = (!hit && local) ? std::min(u.n_recompute, u.n_tokens) : ncomp;
       for (int32_t j = 0; j < ncomp; ++j) {
         rows.push_back({req_slot(u.position + j), u.position + j});
         p->row_pos.push_back(u.position + j);
         p->row_req.push_back(r);
+        p->row_lo.push_back(j < wnd ? 0 : u.position);
       }
       if (hit) {
         for (int32_t j = ncomp; j < u.n_tokens; ++j)
@@ -315,15 +326,22 @@ tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
   std::vector<Item> items;
   int32_t max_kv = 0;
   for (int r = 0; r < n_req; ++r) {
-    for (int32_t t0 = req_row0[r]; t0 < req_row0[r + 1]; t0 += kTileRows) {
-      const int32_t n = std::min(kTileRows, req_row0[r + 1] - t0);
-      const int32_t lo = p->row_pos[t0], hi = p->row_pos[t0 + n - 1];
-      max_kv = std::max(max_kv, hi + 1);
-      for (int g = 0; g < Hkv; ++g)
-        for (int hs = 0; hs < hsplit; ++hs) {
-          AttnItem a{t0, n, hi + 1, lo, g, bt_off[r], bt_len[r], 4 * hs};
-          items.push_back({a, (int64_t)(hi + 1), r * Hkv + g});
-        }
+    // runs of consecutive rows with the same first visible key
+    for (int32_t a0 = req_row0[r]; a0 < req_row0[r + 1];) {
+      int32_t a1 = a0 + 1;
+      while (a1 < req_row0[r + 1] && p->row_lo[a1] == p->row_lo[a0]) ++a1;
+      const int32_t kv_lo = p->row_lo[a0];
+      for (int32_t t0 = a0; t0 < a1; t0 += kTileRows) {
+        const int32_t n = std::min(kTileRows, a1 - t0);
+        const int32_t lo = p->row_pos[t0], hi = p->row_pos[t0 + n - 1];
+        max_kv = std::max(max_kv, hi + 1);
+        for (int g = 0; g < Hkv; ++g)
+          for (int hs = 0; hs < hsplit; ++hs) {
+            AttnItem a{t0, n, hi + 1, lo, g, bt_off[r], bt_len[r], 4 * hs, kv_lo, {0, 0, 0}};
+            items.push_back({a, (int64_t)(hi + 1 - kv_lo), r * Hkv + g});
+          }
+      }
+      a0 = a1;
     }
   }
   // XCD-aware order: (request, KV head) groups share K/V, so each group is
@@ -358,7 +376,7 @@ tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
   for (size_t i = 0; i < per_bin; ++i)
     for (int b = 0; b < kNumXcd; ++b)
       order.push_back(i < bins[b].size() ? bins[b][i]
-                                         : AttnItem{0, 0, 0, 0, 0, 0, 0, 0});
+                                         : AttnItem{0, 0, 0, 0, 0, 0, 0, 0, 0, {0, 0, 0}});
 
   p->T = (int32_t)rows.size();
   p->n_gather = (int32_t)gather.size();

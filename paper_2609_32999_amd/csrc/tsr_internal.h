@@ -55,18 +55,20 @@ struct alignas(16) PageDesc {
 };
 
 // One attention work item: up to kTileRows consecutive computed rows of one
-// request against one KV head, for query heads head0 .. head0+3 of that KV
-// head's group (MFMA kernels; a group of G > 4 heads is split over G/4
-// items).  n_rows == 0 marks padding.
+// request, all with the same first visible key, against one KV head, for
+// query heads head0 .. head0+3 of that KV head's group (MFMA kernels; a
+// group of G > 4 heads is split over G/4 items).  n_rows == 0 marks padding.
 struct alignas(16) AttnItem {
   int32_t row0;      // first computed row (plan order)
   int32_t n_rows;    // rows in the tile (<= kTileRows)
-  int32_t kv_len;    // keys 0 .. kv_len-1 are visible to some row (max pos + 1)
+  int32_t kv_len;    // keys kv_lo .. kv_len-1 are visible to some row (max pos + 1)
   int32_t min_pos;   // smallest position among the rows
   int32_t kv_head;
   int32_t bt_off;    // offset of the request's block table in the plan
   int32_t n_pages;   // entries of that block table
   int32_t head0;     // first query head of the group handled by the item
+  int32_t kv_lo;     // first visible key of every row (0 unless unit-local)
+  int32_t pad[3];
 };
 
 // Device-side view of a plan (pointers into the caller's workspace).
@@ -97,7 +99,7 @@ struct tsr_plan {
   int32_t n_items;          // attention items incl. padding
   int32_t max_kv_len;
   int32_t n_gpages, n_apages, n_rpages;   // e4m3 plans only
-  std::vector<int32_t> row_pos, row_req;
+  std::vector<int32_t> row_pos, row_req, row_lo;
   std::vector<char> image;  // host copy of the device image
   size_t off_gather, off_rows, off_retain, off_items, off_bt, ws_bytes;
   size_t off_gpages, off_apages, off_rpages;

@@ -39,7 +39,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_abi_version():
-    assert P.tsr_abi_version() == 1
+    assert P.tsr_abi_version() == 2
 
 
 @pytest.mark.parametrize("name", ["tiny", "small_bf16", "small_f32", "small_bf16_g8",
@@ -173,3 +173,35 @@ def test_edge_requests_plan():
     r1 = NS(prompt_len=1, units=[], text_segs=[(0, 1)], block_table=np.array([5], np.int32))
     plan = _plan(wl, [r1])
     assert plan.num_compute_tokens == 1 and plan.num_attn_items == 8
+
+
+@pytest.mark.parametrize("name", ["tiny", "small_bf16", "rag8b", "agent8b"])
+def test_host_plan_row_kv_lo_matches_oracle_local_scope(name):
+    cfg = workloads.get_config(name).with_(miss_scope="local")
+    wl = workloads.make_workload(cfg)
+    plan = _plan(wl)
+    want = np.concatenate([L.row_kv_lo(r) for r in wl.requests])
+    got = plan.row_kv_lo()
+    assert np.array_equal(got, want)
+    assert (got > 0).any()
+    # the global scope of the same batch: every row sees the whole prefix
+    assert not _plan(workloads.make_workload(cfg.with_(miss_scope="global"))).row_kv_lo().any()
+
+
+def test_bad_miss_scope_and_negative_local_window_are_rejected():
+    wl = workloads.generate("tiny")
+    req = wl.requests[0]
+    bad = NS(**{**vars(req), "miss_scope": 2})
+    with pytest.raises(P.TsrError) as e:
+        _plan(wl, [bad])
+    assert e.value.status == P.TSR_ERR_INVALID_ARG
+    units = [NS(**vars(u)) for u in req.units]
+    units[0].n_recompute = -1                     # a MISS unit
+    assert units[0].residency == 0
+    loc = NS(**{**vars(req), "units": units, "miss_scope": 1})
+    with pytest.raises(P.TsrError) as e:
+        _plan(wl, [loc])
+    assert e.value.status == P.TSR_ERR_INVALID_ARG
+    # under the global scope a MISS unit's n_recompute is not used
+    glob = NS(**{**vars(req), "units": units, "miss_scope": 0})
+    _plan(wl, [glob]).destroy()

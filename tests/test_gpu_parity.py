@@ -190,3 +190,32 @@ def _gathered_positions(wl, r):
                 if u.position + j not in computed:
                     cached[u.position + j] = True
     return cached
+
+
+@pytest.mark.parametrize("name", ["tiny", "small_f32", "small_bf16", "small_bf16_g8", "small_fp8"])
+def test_local_miss_scope(name):
+    """LOCAL miss scope: a MISS unit's tokens past its window attend only to
+    their own unit (first visible key not a multiple of the tile in the
+    ragged configs)."""
+    _full_check(workloads.make_workload(workloads.get_config(name).with_(miss_scope="local")))
+
+
+@pytest.mark.parametrize("G", [1, 2])
+def test_local_miss_scope_small_groups(G):
+    cfg = workloads.get_config("small_bf16").with_(miss_scope="local")
+    shape = cfg.model.__class__(**{**vars(cfg.model), "n_q_heads": 8 * G})
+    _full_check(workloads.make_workload(cfg.with_(model=shape)))
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("name", ["rag8b", "agent8b"])
+def test_local_miss_scope_large(name):
+    """Full-size batches under the LOCAL scope; attention checked on one
+    sampled KV head of sampled requests."""
+    wl = workloads.make_workload(workloads.get_config(name).with_(miss_scope="local"))
+    run = GpuRun(wl)
+    rng = np.random.default_rng(31)
+    reqs = sorted(rng.choice(len(wl.requests), min(3, len(wl.requests)), replace=False).tolist())
+    for r in reqs:
+        check_request(run, r, kv_heads=[int(rng.integers(wl.model.n_kv_heads))])
+    assert run.pool_after_attn_ok

@@ -51,6 +51,10 @@ class WorkloadConfig:
     unit_order: tuple[tuple[int, ...], ...] | None = None
     # retain newly computed units into the pool
     retain_misses: bool = True
+    # miss scope of every request: "global" (missing units are rows of the
+    # final pass over the whole prompt) or "local" (prefilled alone, then
+    # composed with a recompute window like hits)
+    miss_scope: str = "global"
     description: str = ""
     extra: dict = field(default_factory=dict)
 

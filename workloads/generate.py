@@ -33,6 +33,7 @@ _TAG_FRESH = 0x51F
 _TAG_UNIT = 0xCAC4E
 _TAG_LEN = 0x1E4
 _TAG_SCALE = 0x5CA1E
+_SCOPES = {"global": 0, "local": 1}
 
 
 @dataclass
@@ -52,6 +53,7 @@ class RequestSpec:
     units: list[UnitRef]
     text_segs: list[tuple[int, int]]   # (start, length), length > 0
     block_table: np.ndarray            # int32 [ceil(prompt_len / B)]
+    miss_scope: int = 0                # 0: global, 1: local
 
 
 def _round_to(x: np.ndarray, dtype: str) -> np.ndarray:
@@ -241,7 +243,8 @@ def make_workload(cfg: WorkloadConfig) -> Workload:
             text.append((pos, cfg.query_tokens))
             pos += cfg.query_tokens
         requests.append(RequestSpec(prompt_len=pos, units=units, text_segs=text,
-                                    block_table=np.empty(0, dtype=np.int32)))
+                                    block_table=np.empty(0, dtype=np.int32),
+                                    miss_scope=_SCOPES[cfg.miss_scope]))
         req_page_counts.append(-(-pos // B))
 
     n_req_pages = int(sum(req_page_counts))
