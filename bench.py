@@ -115,6 +115,51 @@ def cpu_baseline(wl, n_req):
                       f"{dt:.1f} s on {cores} BLAS threads (os.cpu_count()={os.cpu_count()})"}
 
 
+def host_tier(torch, wl, plan, k, v, row_bytes, reps=5):
+    """Compose and retain against a pool held in pinned host memory (the host
+    tier): the same kernels read the cached pages, and write the retained
+    ones, across the host link.  Reported beside a plain pinned-host <->
+    device copy of similar size, the link's achievable rate."""
+    from paper_2609_32999_amd import staging
+    from paper_2609_32999_amd.session import Session
+    m = wl.model
+    hs = Session(m, wl.n_pool_pages, wl.n_req_pages, n_layers=1, pool="host")
+    staging.upload_pool(hs, wl, layer=0)
+    s = torch.cuda.current_stream()
+    E = lambda: torch.cuda.Event(enable_timing=True)
+
+    def timed(fn):
+        fn()
+        a, b = E(), E()
+        a.record(s)
+        for _ in range(reps):
+            fn()
+        b.record(s)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / reps
+
+    compose_ms = timed(lambda: hs.compose(plan, layer=0, stream=s))
+    retain_ms = timed(lambda: hs.retain(plan, k, v, layer=0, stream=s))
+    nb = max(plan.num_gather_tokens * row_bytes, 64 << 20)
+    h = torch.empty(nb, dtype=torch.uint8, pin_memory=True)
+    d = torch.empty(nb, dtype=torch.uint8, device="cuda")
+    h2d_ms = timed(lambda: d.copy_(h, non_blocking=True))
+    d2h_ms = timed(lambda: h.copy_(d, non_blocking=True))
+    read = plan.num_gather_tokens * row_bytes       # crosses the link once
+    written = plan.num_retain_tokens * row_bytes
+    log(f"[bench] host tier: compose {compose_ms * 1e3:.1f} us, retain {retain_ms * 1e3:.1f} us")
+    del hs, h, d
+    return {
+        "compose_us": compose_ms * 1e3,
+        "compose_link_gbps": read / (compose_ms * 1e-3) / 1e9,
+        "retain_us": retain_ms * 1e3,
+        "retain_link_gbps": written / (retain_ms * 1e-3) / 1e9 if written else None,
+        "copy_h2d_gbps": nb / (h2d_ms * 1e-3) / 1e9,
+        "copy_d2h_gbps": nb / (d2h_ms * 1e-3) / 1e9,
+        "copy_bytes": nb,
+    }
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -130,6 +175,8 @@ def main():
     ap.add_argument("--no-peaks", dest="peaks", action="store_false",
                     help="skip measuring the achievable copy and bf16 GEMM rates")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-host-tier", dest="host_tier", action="store_false",
+                    help="skip timing compose and retain against a pool in pinned host memory")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="run one plain device copy of this size first (to scale "
                          "HBM byte counters against a kernel of known traffic)")
@@ -246,6 +293,7 @@ def main():
 
     w = kv_elem_bytes(m.kv_dtype)
     row_bytes = 2 * m.n_kv_heads * m.head_dim * w           # K + V of one token
+    host = host_tier(torch, wl, plan, ks[0], vs[0], row_bytes) if args.host_tier else None
     gather_bytes = 2 * plan.num_gather_tokens * row_bytes   # read + write
     append_bytes = 2 * T * row_bytes
     retain_bytes = 2 * plan.num_retain_tokens * row_bytes
@@ -298,6 +346,8 @@ def main():
         "append_gbps": append_bytes / (append_ms * 1e-3) / 1e9,
         "retain_gbps": retain_bytes / (retain_ms * 1e-3) / 1e9 if retain_ms > 0 else None,
     }
+    if host:
+        rec["host_tier"] = host
     if measured:
         rec["measured_peaks"] = measured
         rec["roofline"]["frac_of_measured"] = attn_tflops / measured["bf16_gemm_tflops"]

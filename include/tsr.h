@@ -216,7 +216,10 @@ void tsr_plan_destroy(tsr_plan* plan);
  * (Section 5.3, "Preparing cache hits").  The pool is read only.
  * Rotation: fp32 table values, fp32 products and one fp32 add each, no
  * fused multiply-add; bf16 results rounded to nearest even.
- *   pool_k/pool_v  device, [n_pool_pages][H_kv][B][d] of kv_dtype.
+ *   pool_k/pool_v  device, [n_pool_pages][H_kv][B][d] of kv_dtype; or, for
+ *                  a pool held in host memory (Section 5.2's local tier),
+ *                  the device address of pinned host memory
+ *                  (hipHostGetDevicePointer), read across the host link.
  *   req_k/req_v    device, [n_req_pages][H_kv][B][d] of kv_dtype.
  *   pool_scale, req_scale  e4m3 only (else NULL): [n_layers][pages][2] fp32.
  *   e4m3: V codes and V scale are copied; K is dequantized, rotated in fp32
@@ -273,7 +276,9 @@ tsr_status tsr_attn(const tsr_plan* plan, const void* q, const void* req_k,
  * beyond n are left untouched.  k/v are the same inputs as
  * tsr_prefill_attn's and must stay alive until the stream reaches this work
  * (Section 5.4: sources stay valid until their copies complete).  A caller
- * may publish the units as HITs only after observing its completion. */
+ * may publish the units as HITs only after observing its completion.
+ * pool_k/pool_v/pool_scale: as for tsr_compose_kv (device memory, or the
+ * device address of pinned host memory). */
 tsr_status tsr_retain_kv(const tsr_plan* plan, const void* k, const void* v,
                          void* pool_k, void* pool_v, float* pool_scale,
                          void* stream);

@@ -3,7 +3,9 @@
 PyTorch provides device memory and streams only; every step of the path runs
 in libtsr's kernels through the C ABI.  A Session owns, for one layer shape:
 
-* the pool arena     [n_pool_pages][H_kv][B][d] for K (pre-RoPE) and V;
+* the pool arena     [n_pool_pages][H_kv][B][d] for K (pre-RoPE) and V, in
+                     device memory or, for the host tier, in pinned host
+                     memory that the kernels read and write over the bus;
 * the request arena  [n_req_pages][H_kv][B][d] for the assembled K and V;
 * the RoPE table     built once per model by tsr_rope_table_init;
 * for e4m3 pools, page scales [n_layers][pages][2] fp32 ({K, V}) for both
@@ -25,11 +27,26 @@ def _require_device():
         raise RuntimeError("libtsr needs a ROCm GPU; none is visible")
 
 
+def _host_device_pointer(t: torch.Tensor) -> int:
+    """Device-visible address of a pinned host tensor (hipHostGetDevicePointer
+    on the HIP runtime torch has loaded)."""
+    import ctypes
+    if not t.is_pinned():
+        raise RuntimeError("host-tier pools must be pinned host memory")
+    hip = ctypes.CDLL("libamdhip64.so.7")
+    dptr = ctypes.c_void_p()
+    err = hip.hipHostGetDevicePointer(ctypes.byref(dptr), ctypes.c_void_p(t.data_ptr()), 0)
+    if err != 0 or not dptr.value:
+        raise RuntimeError(f"hipHostGetDevicePointer failed ({err})")
+    return int(dptr.value)
+
+
 class Session:
     def __init__(self, shape, n_pool_pages: int, n_req_pages: int,
-                 device: str = "cuda", n_layers: int = 1, stream=None):
+                 device: str = "cuda", n_layers: int = 1, stream=None, pool: str = "device"):
         """`shape` has n_q_heads, n_kv_heads, head_dim, page_size, kv_dtype,
-        act_dtype, rope_theta, max_position (workloads.ModelShape)."""
+        act_dtype, rope_theta, max_position (workloads.ModelShape).  `pool`
+        is "device" (HBM) or "host" (pinned host memory: the host tier)."""
         _require_device()
         B.lib()
         self.shape = shape
@@ -47,9 +64,14 @@ class Session:
         self.n_pool_pages = n_pool_pages
         self.n_req_pages = n_req_pages
         page = (shape.n_kv_heads, shape.page_size, shape.head_dim)
+        if pool not in ("device", "host"):
+            raise ValueError(f"pool must be 'device' or 'host', not {pool!r}")
+        self.pool_tier = pool
+        pool_dev = dict(device=self.device) if pool == "device" else dict(pin_memory=True)
         self.pool_k = torch.empty((n_layers, n_pool_pages, *page), dtype=self.kv_dtype,
-                                  device=self.device)
-        self.pool_v = torch.empty_like(self.pool_k)
+                                  **pool_dev)
+        self.pool_v = torch.empty((n_layers, n_pool_pages, *page), dtype=self.kv_dtype,
+                                  **pool_dev)
         self.req_k = torch.empty((n_layers, n_req_pages, *page), dtype=self.kv_dtype,
                                  device=self.device)
         self.req_v = torch.empty_like(self.req_k)
@@ -57,9 +79,16 @@ class Session:
         self.pool_scale = self.req_scale = None
         if self.e4m3:
             self.pool_scale = torch.empty((n_layers, n_pool_pages, 2), dtype=torch.float32,
-                                          device=self.device)
+                                          **pool_dev)
             self.req_scale = torch.empty((n_layers, n_req_pages, 2), dtype=torch.float32,
                                          device=self.device)
+        # addresses the kernels use for the pool arenas
+        self._pool_base = {}
+        for name in ("pool_k", "pool_v", "pool_scale"):
+            t = getattr(self, name)
+            if t is not None:
+                self._pool_base[name] = (t.data_ptr() if pool == "device"
+                                         else _host_device_pointer(t))
         nbytes = B.tsr_rope_table_bytes(self.model)
         if nbytes == 0:
             raise B.TsrError(B.TSR_ERR_INVALID_ARG, B.tsr_last_error())
@@ -84,17 +113,28 @@ class Session:
         """Compose one layer (default 0), or all layers when layer == 'all'."""
         s = stream or self.stream
         if layer == "all":
-            B.tsr_compose_kv(plan, self.pool_k, self.pool_v, self.pool_scale, self.req_k,
+            B.tsr_compose_kv(plan, self._pk(0), self._pv(0), self._ps(0), self.req_k,
                              self.req_v, self.req_scale, self.n_layers,
                              self.pool_k[0].nbytes if self.n_layers > 1 else 0,
                              self.req_k[0].nbytes if self.n_layers > 1 else 0, s)
             return
         li = layer or 0
-        B.tsr_compose_kv(plan, self.pool_k[li], self.pool_v[li], self._ps(li), self.req_k[li],
+        B.tsr_compose_kv(plan, self._pk(li), self._pv(li), self._ps(li), self.req_k[li],
                          self.req_v[li], self._rs(li), 1, 0, 0, s)
 
+    # kernel-visible addresses of one layer of the pool arenas
+    def _pool_addr(self, name, layer):
+        t = getattr(self, name)
+        return self._pool_base[name] + layer * t[0].nbytes
+
+    def _pk(self, layer):
+        return self._pool_addr("pool_k", layer)
+
+    def _pv(self, layer):
+        return self._pool_addr("pool_v", layer)
+
     def _ps(self, layer):
-        return self.pool_scale[layer] if self.e4m3 else None
+        return self._pool_addr("pool_scale", layer) if self.e4m3 else None
 
     def _rs(self, layer):
         return self.req_scale[layer] if self.e4m3 else None
@@ -120,5 +160,5 @@ class Session:
                    stream or self.stream)
 
     def retain(self, plan, k, v, layer: int = 0, stream=None):
-        B.tsr_retain_kv(plan, k, v, self.pool_k[layer], self.pool_v[layer], self._ps(layer),
+        B.tsr_retain_kv(plan, k, v, self._pk(layer), self._pv(layer), self._ps(layer),
                         stream or self.stream)

@@ -26,16 +26,16 @@ def upload_pool(sess, wl, unit_ids=None, layer: int = 0) -> None:
     B = wl.model.page_size
     ids = wl.hit_unit_ids() if unit_ids is None else unit_ids
     for uid in ids:
-        pages = torch.as_tensor(np.asarray(wl.unit_pages[uid], dtype=np.int64),
-                                device=sess.device)
+        dev = sess.pool_k.device          # the GPU, or the host for a host-tier pool
+        pages = torch.as_tensor(np.asarray(wl.unit_pages[uid], dtype=np.int64), device=dev)
         if sess.e4m3:
             k, v, ks, vs = wl.unit_state_e4m3(uid)
-            sc = torch.from_numpy(np.stack([ks, vs], axis=1)).to(sess.device)
+            sc = torch.from_numpy(np.stack([ks, vs], axis=1)).to(dev)
             sess.pool_scale[layer][pages] = sc
         else:
             k, v = wl.unit_state(uid)
         for src, dst in ((k, sess.pool_k[layer]), (v, sess.pool_v[layer])):
-            t = torch.from_numpy(_pages_from_tokens(src, B)).to(sess.device)
+            t = torch.from_numpy(_pages_from_tokens(src, B)).to(dev)
             dst[pages] = t.to(dst.dtype)
 
 

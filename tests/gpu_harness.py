@@ -49,12 +49,12 @@ def say(msg: str) -> None:
 class GpuRun:
     """Runs compose -> prefill_attn -> retain on a workload (one layer)."""
 
-    def __init__(self, wl, with_lse=True):
+    def __init__(self, wl, with_lse=True, pool="device"):
         self.wl = wl
         m = wl.model
         say(f"[gpu] workload={wl.name} seed={wl.seed} H={m.n_q_heads}/{m.n_kv_heads} "
-            f"d={m.head_dim} {m.kv_dtype} prompt_tokens={wl.prompt_tokens}")
-        s = Session(m, wl.n_pool_pages, wl.n_req_pages)
+            f"d={m.head_dim} {m.kv_dtype} prompt_tokens={wl.prompt_tokens} pool={pool}")
+        s = Session(m, wl.n_pool_pages, wl.n_req_pages, pool=pool)
         self.sess = s
         for t in (s.pool_k, s.pool_v, s.req_k, s.req_v):
             fill_sentinel(t)
@@ -175,12 +175,12 @@ def check_retained(run: GpuRun):
         assert np.array_equal(gk[:, filled].view(np.uint32), kref[:, filled].view(np.uint32))
         assert np.array_equal(gv[:, filled].view(np.uint32), vref[:, filled].view(np.uint32))
         if (~filled).any():
-            sk = is_sentinel(s.pool_k[0, pg])[:, torch.as_tensor(~filled, device=s.device)]
+            sk = is_sentinel(s.pool_k[0, pg])[:, torch.as_tensor(~filled, device=s.pool_k.device)]
             assert bool(sk.all()), "retain wrote past the unit's last token"
     # every other pool page is untouched
-    touched = torch.zeros(wl.n_pool_pages, dtype=torch.bool, device=s.device)
+    touched = torch.zeros(wl.n_pool_pages, dtype=torch.bool, device=s.pool_k.device)
     if pages:
-        touched[torch.as_tensor(list(pages), device=s.device)] = True
+        touched[torch.as_tensor(list(pages), device=s.pool_k.device)] = True
     same_k = (s.pool_k[0].view(torch.uint8) == run.pool_k0[0].view(torch.uint8))
     same_v = (s.pool_v[0].view(torch.uint8) == run.pool_v0[0].view(torch.uint8))
     untouched = ~touched
@@ -206,7 +206,7 @@ def _check_retained_e4m3(run: GpuRun):
     s = run.sess
     pages = retained_pages_e4m3(wl)
     for pg, (kref, vref, ks, vs, filled) in pages.items():
-        f = torch.as_tensor(filled, device=s.device)
+        f = torch.as_tensor(filled, device=s.pool_k.device)
         gk = s.pool_k[0, pg][:, f].cpu().numpy()
         gv = s.pool_v[0, pg][:, f].cpu().numpy()
         assert np.array_equal(e4m3_decode(gk), e4m3_decode(kref[:, filled]))
@@ -215,9 +215,9 @@ def _check_retained_e4m3(run: GpuRun):
         assert sc[0] == ks and sc[1] == vs, (pg, sc, ks, vs)
         if (~filled).any():
             assert bool(is_sentinel(s.pool_k[0, pg][:, ~f]).all())
-    touched = torch.zeros(wl.n_pool_pages, dtype=torch.bool, device=s.device)
+    touched = torch.zeros(wl.n_pool_pages, dtype=torch.bool, device=s.pool_k.device)
     if pages:
-        touched[torch.as_tensor(list(pages), device=s.device)] = True
+        touched[torch.as_tensor(list(pages), device=s.pool_k.device)] = True
     un = ~touched
     assert bool((s.pool_k[0] == run.pool_k0[0])[un].all())
     assert bool((s.pool_v[0] == run.pool_v0[0])[un].all())

@@ -219,3 +219,22 @@ def test_local_miss_scope_large(name):
     for r in reqs:
         check_request(run, r, kv_heads=[int(rng.integers(wl.model.n_kv_heads))])
     assert run.pool_after_attn_ok
+
+
+@pytest.mark.parametrize("name", ["small_bf16", "small_fp8", "small_f32"])
+def test_host_tier_pool(name):
+    """The pool in pinned host memory (the host tier): compose gathers cached
+    pages over the bus, retain writes new units back to host memory; both
+    bit-exact, attention as with a device pool."""
+    run = _full_check_pool(workloads.generate(name), "host")
+    assert run.sess.pool_k.device.type == "cpu"
+
+
+def _full_check_pool(wl, pool):
+    run = GpuRun(wl, pool=pool)
+    assert run.pool_after_compose_ok and run.pool_after_attn_ok, "pool modified"
+    for r in range(len(wl.requests)):
+        check_request(run, r)
+        check_request_sentinels(run, r)
+    check_retained(run)
+    return run
