@@ -48,14 +48,18 @@
 extern "C" {
 #endif
 
-#define TSR_ABI_VERSION 2
+#define TSR_ABI_VERSION 3
 
 typedef enum {
   TSR_OK = 0,
   TSR_ERR_INVALID_ARG = 1,   /* malformed request, null pointer, bad size */
   TSR_ERR_UNSUPPORTED = 2,   /* valid but not implemented (dtype, shape)  */
   TSR_ERR_OUT_OF_RANGE = 3,  /* page id, position or arena bound exceeded */
-  TSR_ERR_DEVICE = 4         /* a HIP call failed (message in last error) */
+  TSR_ERR_DEVICE = 4,        /* a HIP call failed (message in last error) */
+  TSR_ERR_STATE = 5,         /* cache entry not in the state the call needs
+                                (exists, absent, PENDING, leased, stale
+                                storage epoch, different block set)        */
+  TSR_ERR_NO_SPACE = 6       /* not enough free blocks in the cache arena  */
 } tsr_status;
 
 typedef enum { TSR_F32 = 0, TSR_BF16 = 1, TSR_E4M3 = 2 } tsr_dtype;
@@ -282,6 +286,95 @@ tsr_status tsr_attn(const tsr_plan* plan, const void* q, const void* req_k,
 tsr_status tsr_retain_kv(const tsr_plan* plan, const void* k, const void* v,
                          void* pool_k, void* pool_v, float* pool_scale,
                          void* stream);
+
+/* -------------------------------------------------- context-unit cache */
+
+/* Directory of a node's context-unit cache (Section 5.2: a cache of unit
+ * states in pinned host memory on every generation node; Section 5.4: its
+ * entry life cycle).  It records which units hold a complete reusable state
+ * in a caller-owned arena of fixed-size blocks (one block = one KV page of
+ * every layer), in which blocks and under which storage epoch, and how many
+ * transfers still read them.  Host metadata only: the directory never
+ * touches the blocks' bytes and makes no HIP call.  Every function is
+ * thread-safe (one mutex per directory).
+ *
+ * Entry life cycle:
+ *   reserve  ABSENT -> PENDING.  Takes n free blocks (lowest ids first) and a
+ *            new storage epoch, the version that tells successive
+ *            allocations of one unit apart; only the holder of that epoch may
+ *            publish or cancel.  A PENDING entry is not a hit: acquire fails,
+ *            so other requests compute the unit for themselves.
+ *   publish  PENDING -> READY, once the writer has observed the completion
+ *            of every block write.  The epoch and the exact block list are
+ *            checked, so a stale writer or a partial write cannot publish.
+ *   cancel   PENDING -> ABSENT for a failed or abandoned writeback.  The
+ *            entry is never published; its blocks are "draining" and return
+ *            to the free set only when the writer calls tsr_cache_reclaim
+ *            for that epoch, after its outstanding transfers completed.
+ *   acquire  READY only: takes a read lease and returns the blocks.  This is
+ *            the revalidation of a planned hit before its transfer; any
+ *            other state returns TSR_ERR_STATE and the caller prepares the
+ *            unit from text instead (Section 5.3, preparation failures).
+ *   release  drops one lease, after the transfer that read the blocks ended.
+ *   evict    READY with no lease -> ABSENT; blocks freed.  A leased entry is
+ *            not evicted (TSR_ERR_STATE). */
+typedef struct tsr_cache tsr_cache;
+
+typedef enum {
+  TSR_ENTRY_ABSENT = 0,
+  TSR_ENTRY_PENDING = 1,
+  TSR_ENTRY_READY = 2
+} tsr_entry_state;
+
+/* A directory over blocks [0, n_blocks), all free. */
+tsr_status tsr_cache_create(int32_t n_blocks, tsr_cache** out);
+void tsr_cache_destroy(tsr_cache* cache);
+
+/* blocks: host [n_blocks] output; epoch: output.  NO_SPACE if fewer than
+ * n_blocks are free; STATE if the unit has an entry. */
+tsr_status tsr_cache_reserve(tsr_cache* cache, uint64_t unit_id, int32_t n_blocks,
+                             uint64_t* epoch, int32_t* blocks);
+/* blocks: host [n_blocks], the list reserve returned, in its order. */
+tsr_status tsr_cache_publish(tsr_cache* cache, uint64_t unit_id, uint64_t epoch,
+                             const int32_t* blocks, int32_t n_blocks);
+tsr_status tsr_cache_cancel(tsr_cache* cache, uint64_t unit_id, uint64_t epoch);
+tsr_status tsr_cache_reclaim(tsr_cache* cache, uint64_t epoch);
+/* blocks: host [max_blocks] output; n_blocks: the unit's block count (set
+ * also when it exceeds max_blocks, which returns OUT_OF_RANGE, no lease). */
+tsr_status tsr_cache_acquire(tsr_cache* cache, uint64_t unit_id, int32_t max_blocks,
+                             uint64_t* epoch, int32_t* blocks, int32_t* n_blocks);
+tsr_status tsr_cache_release(tsr_cache* cache, uint64_t unit_id, uint64_t epoch);
+tsr_status tsr_cache_evict(tsr_cache* cache, uint64_t unit_id);
+/* state (required), epoch, n_blocks, leases (each may be NULL); an absent
+ * unit reads as TSR_ENTRY_ABSENT with zeros. */
+tsr_status tsr_cache_query(const tsr_cache* cache, uint64_t unit_id, int32_t* state,
+                           uint64_t* epoch, int32_t* n_blocks, int32_t* leases);
+/* Blocks neither held by an entry nor draining; -1 for NULL. */
+int32_t tsr_cache_free_blocks(const tsr_cache* cache);
+
+/* Copy whole blocks between two block arenas on `stream` with
+ * hipMemcpyAsync (between pinned host memory and device memory the copy
+ * engines carry it, leaving the compute units to the kernels):
+ *   dst block dst_blocks[i] <- src block src_blocks[i] for i < n, in each
+ *   of n_layers layers (layer l of an arena starts l * layer_stride bytes
+ *   after its base; strides are ignored when n_layers == 1).
+ * Pairs whose ids both continue the previous pair's are merged into one
+ * copy.  Staging a cached unit into device memory before compose (Section
+ * 5.3, local hits copied from the pinned host cache into bounded GPU
+ * staging) and writing retained blocks back to the cache (Section 5.4) are
+ * both this call.
+ *   dst/src      device pointers or pinned host pointers to arenas of
+ *                n_dst_blocks / n_src_blocks blocks of block_bytes.
+ *   dst_blocks, src_blocks  host arrays [n].
+ * Every id is checked against its arena before anything is enqueued
+ * (OUT_OF_RANGE).  If a HIP call fails midway (DEVICE), the copies before
+ * it stay enqueued.  Source blocks must not be modified, and destination
+ * blocks not read, until the stream reaches this work. */
+tsr_status tsr_copy_blocks(void* dst, int32_t n_dst_blocks, const int32_t* dst_blocks,
+                           const void* src, int32_t n_src_blocks,
+                           const int32_t* src_blocks, int32_t n, int64_t block_bytes,
+                           int32_t n_layers, int64_t dst_layer_stride,
+                           int64_t src_layer_stride, void* stream);
 
 /* Thread-local message of the last failure on this thread ("" if none). */
 const char* tsr_last_error(void);

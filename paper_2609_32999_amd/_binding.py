@@ -18,8 +18,11 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 # TSR_LIBRARY overrides the library path (to compare builds side by side).
 LIB_PATH = os.environ.get("TSR_LIBRARY") or os.path.join(HERE, "libtsr.so")
 
-TSR_OK, TSR_ERR_INVALID_ARG, TSR_ERR_UNSUPPORTED, TSR_ERR_OUT_OF_RANGE, TSR_ERR_DEVICE = range(5)
-STATUS_NAMES = {0: "OK", 1: "INVALID_ARG", 2: "UNSUPPORTED", 3: "OUT_OF_RANGE", 4: "DEVICE"}
+(TSR_OK, TSR_ERR_INVALID_ARG, TSR_ERR_UNSUPPORTED, TSR_ERR_OUT_OF_RANGE, TSR_ERR_DEVICE,
+ TSR_ERR_STATE, TSR_ERR_NO_SPACE) = range(7)
+STATUS_NAMES = {0: "OK", 1: "INVALID_ARG", 2: "UNSUPPORTED", 3: "OUT_OF_RANGE", 4: "DEVICE",
+                5: "STATE", 6: "NO_SPACE"}
+TSR_ENTRY_ABSENT, TSR_ENTRY_PENDING, TSR_ENTRY_READY = 0, 1, 2
 TSR_F32, TSR_BF16, TSR_E4M3 = 0, 1, 2
 DTYPE_CODES = {"f32": TSR_F32, "bf16": TSR_BF16, "e4m3": TSR_E4M3}
 TSR_MISS, TSR_HIT = 0, 1
@@ -33,6 +36,9 @@ EXPORTS = (
     "tsr_plan_num_retain_tokens", "tsr_plan_num_attn_items",
     "tsr_plan_compute_positions", "tsr_plan_row_kv_lo", "tsr_plan_destroy", "tsr_compose_kv",
     "tsr_prefill_attn", "tsr_append_kv", "tsr_attn", "tsr_retain_kv",
+    "tsr_cache_create", "tsr_cache_destroy", "tsr_cache_reserve", "tsr_cache_publish",
+    "tsr_cache_cancel", "tsr_cache_reclaim", "tsr_cache_acquire", "tsr_cache_release",
+    "tsr_cache_evict", "tsr_cache_query", "tsr_cache_free_blocks", "tsr_copy_blocks",
 )
 
 
@@ -99,6 +105,23 @@ def lib():
             "tsr_retain_kv": (c_int32, [P, P, P, P, P, P, P]),
             "tsr_append_kv": (c_int32, [P, P, P, P, P, P, P]),
             "tsr_attn": (c_int32, [P, P, P, P, P, P, P, P]),
+            "tsr_cache_create": (c_int32, [c_int32, POINTER(c_void_p)]),
+            "tsr_cache_destroy": (None, [P]),
+            "tsr_cache_reserve": (c_int32, [P, c_uint64, c_int32, POINTER(c_uint64),
+                                            POINTER(c_int32)]),
+            "tsr_cache_publish": (c_int32, [P, c_uint64, c_uint64, POINTER(c_int32), c_int32]),
+            "tsr_cache_cancel": (c_int32, [P, c_uint64, c_uint64]),
+            "tsr_cache_reclaim": (c_int32, [P, c_uint64]),
+            "tsr_cache_acquire": (c_int32, [P, c_uint64, c_int32, POINTER(c_uint64),
+                                            POINTER(c_int32), POINTER(c_int32)]),
+            "tsr_cache_release": (c_int32, [P, c_uint64, c_uint64]),
+            "tsr_cache_evict": (c_int32, [P, c_uint64]),
+            "tsr_cache_query": (c_int32, [P, c_uint64, POINTER(c_int32), POINTER(c_uint64),
+                                          POINTER(c_int32), POINTER(c_int32)]),
+            "tsr_cache_free_blocks": (c_int32, [P]),
+            "tsr_copy_blocks": (c_int32, [P, c_int32, POINTER(c_int32), P, c_int32,
+                                          POINTER(c_int32), c_int32, c_int64, c_int32,
+                                          c_int64, c_int64, P]),
         }
         for name, (res, args) in sig.items():
             f = getattr(L, name)
@@ -287,3 +310,85 @@ def tsr_append_kv(plan: Plan, k, v, req_k, req_v, req_scale=None, stream=None) -
 def tsr_attn(plan: Plan, q, req_k, req_v, req_scale, out, lse=None, stream=None) -> None:
     _check(lib().tsr_attn(plan.handle, _ptr(q), _ptr(req_k), _ptr(req_v), _ptr(req_scale),
                           _ptr(out), _ptr(lse), _stream(stream)))
+
+
+def _i32(a) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(a, dtype=np.int32))
+
+
+def _i32p(a: np.ndarray):
+    return a.ctypes.data_as(POINTER(c_int32))
+
+
+class UnitCache:
+    """A context-unit cache directory (tsr_cache_*): entries PENDING/READY
+    under storage epochs, read leases, draining blocks of cancelled writes."""
+
+    def __init__(self, n_blocks: int):
+        out = c_void_p()
+        _check(lib().tsr_cache_create(n_blocks, ctypes.byref(out)))
+        self.handle = out.value
+        self.n_blocks = n_blocks
+
+    def close(self) -> None:
+        if self.handle:
+            lib().tsr_cache_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def reserve(self, unit_id: int, n_blocks: int) -> tuple[int, np.ndarray]:
+        ep = c_uint64()
+        blocks = np.empty(max(n_blocks, 0), dtype=np.int32)
+        _check(lib().tsr_cache_reserve(self.handle, unit_id, n_blocks, ctypes.byref(ep),
+                                       _i32p(blocks)))
+        return ep.value, blocks
+
+    def publish(self, unit_id: int, epoch: int, blocks) -> None:
+        b = _i32(blocks)
+        _check(lib().tsr_cache_publish(self.handle, unit_id, epoch, _i32p(b), len(b)))
+
+    def cancel(self, unit_id: int, epoch: int) -> None:
+        _check(lib().tsr_cache_cancel(self.handle, unit_id, epoch))
+
+    def reclaim(self, epoch: int) -> None:
+        _check(lib().tsr_cache_reclaim(self.handle, epoch))
+
+    def acquire(self, unit_id: int, max_blocks: int) -> tuple[int, np.ndarray]:
+        ep, n = c_uint64(), c_int32()
+        blocks = np.empty(max(max_blocks, 0), dtype=np.int32)
+        _check(lib().tsr_cache_acquire(self.handle, unit_id, max_blocks, ctypes.byref(ep),
+                                       _i32p(blocks), ctypes.byref(n)))
+        return ep.value, blocks[:n.value].copy()
+
+    def release(self, unit_id: int, epoch: int) -> None:
+        _check(lib().tsr_cache_release(self.handle, unit_id, epoch))
+
+    def evict(self, unit_id: int) -> None:
+        _check(lib().tsr_cache_evict(self.handle, unit_id))
+
+    def query(self, unit_id: int) -> dict:
+        st, ep, nb, ls = c_int32(), c_uint64(), c_int32(), c_int32()
+        _check(lib().tsr_cache_query(self.handle, unit_id, ctypes.byref(st), ctypes.byref(ep),
+                                     ctypes.byref(nb), ctypes.byref(ls)))
+        return {"state": st.value, "epoch": ep.value, "n_blocks": nb.value,
+                "leases": ls.value}
+
+    @property
+    def free_blocks(self) -> int:
+        return lib().tsr_cache_free_blocks(self.handle)
+
+
+def tsr_copy_blocks(dst, n_dst_blocks: int, dst_blocks, src, n_src_blocks: int, src_blocks,
+                    block_bytes: int, n_layers: int = 1, dst_layer_stride: int = 0,
+                    src_layer_stride: int = 0, stream=None) -> None:
+    d, sb = _i32(dst_blocks), _i32(src_blocks)
+    if len(d) != len(sb):
+        raise ValueError("dst_blocks and src_blocks differ in length")
+    _check(lib().tsr_copy_blocks(_ptr(dst), n_dst_blocks, _i32p(d), _ptr(src), n_src_blocks,
+                                 _i32p(sb), len(d), block_bytes, n_layers, dst_layer_stride,
+                                 src_layer_stride, _stream(stream)))

@@ -15,12 +15,6 @@ namespace tsr {
 namespace {
 thread_local std::string g_error;
 
-tsr_status device_fail(const char* what, hipError_t e) {
-  set_error(std::string(what) + ": " + hipGetErrorName(e) + " (" +
-            hipGetErrorString(e) + ")");
-  return TSR_ERR_DEVICE;
-}
-
 tsr_status check_exec(const tsr_plan* p) {
   if (!p) {
     set_error("plan is NULL");
@@ -52,21 +46,6 @@ tsr_status check_scales(const tsr_plan* p, const float* a, const float* b,
   return TSR_OK;
 }
 
-template <typename F>
-tsr_status guarded(F&& f) {
-  try {
-    return f();
-  } catch (const std::bad_alloc&) {
-    set_error("host allocation failed");
-    return TSR_ERR_INVALID_ARG;
-  } catch (const std::exception& e) {
-    set_error(std::string("internal error: ") + e.what());
-    return TSR_ERR_INVALID_ARG;
-  } catch (...) {
-    set_error("internal error");
-    return TSR_ERR_INVALID_ARG;
-  }
-}
 }  // namespace
 
 void set_error(const std::string& msg) { g_error = msg; }

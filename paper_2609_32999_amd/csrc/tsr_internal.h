@@ -6,6 +6,8 @@
 
 #include <cstddef>
 #include <cstdint>
+#include <exception>
+#include <new>
 #include <string>
 #include <vector>
 
@@ -112,6 +114,30 @@ namespace tsr {
 
 // Thread-local error text, set by every failing entry point.
 void set_error(const std::string& msg);
+
+// A failed HIP call: record its name and message, return TSR_ERR_DEVICE.
+inline tsr_status device_fail(const char* what, hipError_t e) {
+  set_error(std::string(what) + ": " + hipGetErrorName(e) + " (" +
+            hipGetErrorString(e) + ")");
+  return TSR_ERR_DEVICE;
+}
+
+// Run an entry point's body so that no exception crosses the C ABI.
+template <typename F>
+tsr_status guarded(F&& f) {
+  try {
+    return f();
+  } catch (const std::bad_alloc&) {
+    set_error("host allocation failed");
+    return TSR_ERR_INVALID_ARG;
+  } catch (const std::exception& e) {
+    set_error(std::string("internal error: ") + e.what());
+    return TSR_ERR_INVALID_ARG;
+  } catch (...) {
+    set_error("internal error");
+    return TSR_ERR_INVALID_ARG;
+  }
+}
 
 // Validate a model; on failure returns a status and sets the error.
 tsr_status check_model(const tsr_model* m);

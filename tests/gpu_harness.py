@@ -225,3 +225,139 @@ def _check_retained_e4m3(run: GpuRun):
                                                     torch.isnan(run.pool_s0[0]))
     assert bool(same_s[un].all())
     return len(pages)
+
+
+# ------------------------------------------------------------ host tier
+def unit_pages_all_layers(wl, uid, n_layers):
+    """Host-cache contents of a unit: K and V pages [n_layers][pages][H][B][d]
+    (and e4m3 scales [n_layers][pages][2]).  Layer 0 holds the unit's
+    cached state; every later layer holds it with K and V swapped, so a
+    copy that mixes up layers is caught."""
+    m = wl.model
+    if m.kv_dtype == "e4m3":
+        kc, vc, ks, vs = wl.unit_state_e4m3(uid)
+        kp = torch.from_numpy(staging._pages_from_tokens(kc, m.page_size))
+        vp = torch.from_numpy(staging._pages_from_tokens(vc, m.page_size))
+        sc = torch.from_numpy(np.stack([ks, vs], axis=1))
+        sw = torch.from_numpy(np.stack([vs, ks], axis=1))
+        return (torch.stack([kp] + [vp] * (n_layers - 1)),
+                torch.stack([vp] + [kp] * (n_layers - 1)),
+                torch.stack([sc] + [sw] * (n_layers - 1)))
+    k, v = wl.unit_state(uid)
+    kp = torch.from_numpy(staging._pages_from_tokens(k, m.page_size))
+    vp = torch.from_numpy(staging._pages_from_tokens(v, m.page_size))
+    return (torch.stack([kp] + [vp] * (n_layers - 1)),
+            torch.stack([vp] + [kp] * (n_layers - 1)), None)
+
+
+def staged_pages_needed(requests, page_size):
+    from paper_2609_32999_amd import TSR_HIT
+    seen, n = set(), 0
+    for r in requests:
+        for u in r.units:
+            if (u.residency == TSR_HIT and u.unit_id not in seen) or (u.residency != TSR_HIT and u.retain):
+                n += -(-int(u.n_tokens) // page_size)
+                if u.residency == TSR_HIT:
+                    seen.add(u.unit_id)
+    return n
+
+
+class StagedRun:
+    """Runs a batch through the host tier: prepare (revalidate hits, stage
+    them into device memory with the copy engines), compose, prefill_attn,
+    retain into staging, write back, finish (release leases, publish).
+    Exposes what check_request reads, with `wl` holding the requests as
+    prepared (fallbacks downgraded to MISS, pages renamed to staging)."""
+
+    def __init__(self, wl, tier=None, n_layers=2, n_staging=None, n_blocks=None,
+                 fail_units=(), fail_retain=(), insert=True, with_lse=True):
+        import dataclasses
+        from paper_2609_32999_amd.host_tier import HostTier
+        m = wl.model
+        if tier is None:
+            n_staging = n_staging or staged_pages_needed(wl.requests, m.page_size)
+            n_blocks = n_blocks or wl.n_pool_pages
+            say(f"[gpu] host tier: workload={wl.name} seed={wl.seed} {m.kv_dtype} "
+                f"blocks={n_blocks} staging={n_staging} layers={n_layers}")
+            tier = HostTier(m, n_blocks, n_staging, wl.n_req_pages, n_layers=n_layers)
+            s = tier.sess
+            for t in (s.pool_k, s.pool_v, s.req_k, s.req_v, tier.host_k, tier.host_v):
+                fill_sentinel(t)
+            if s.e4m3:
+                for t in (s.pool_scale, s.req_scale, tier.host_scale):
+                    t.fill_(float("nan"))
+        self.tier = tier
+        s = self.sess = tier.sess
+        if insert:
+            for uid in wl.hit_unit_ids():
+                if tier.cache.query(uid)["state"] == 0:
+                    tier.insert(uid, *unit_pages_all_layers(wl, uid, tier.n_layers))
+        self.prep = tier.prepare(wl.requests, fail_units=fail_units)
+        self.wl = dataclasses.replace(wl, requests=self.prep.requests)
+        self.plan = s.plan(self.wl.requests)
+        self.q, self.k, self.v = staging.fresh_inputs(s, self.wl, self.plan)
+        self.pos, self.req = self.plan.compute_positions()
+        s.compose(self.plan, layer=0)
+        self.out, self.lse = s.new_outputs(self.plan, with_lse)
+        s.prefill_attn(self.plan, self.q, self.k, self.v, self.out, self.lse)
+        s.retain(self.plan, self.k, self.v)
+        self.reservations = list(self.prep.reservations)
+        tier.writeback(self.prep, fail_units=fail_retain)
+        tier.finish(self.prep)
+        torch.cuda.synchronize()
+        say(f"[gpu] staged={len(self.prep.stage_src)} fallbacks={len(self.prep.fallbacks)} "
+            f"declined={len(self.prep.declined)} published={len(self.prep.published)} "
+            f"cancelled={len(self.prep.cancelled)} T={self.plan.num_compute_tokens}")
+
+    def request_kv(self, r):
+        return staging.request_kv(self.sess, self.wl, r)
+
+    def rows_of(self, r):
+        return np.nonzero(self.req == r)[0]
+
+    def check_staged_bytes(self):
+        """Every staged slot holds its host block's bytes, in every layer."""
+        t = self.tier
+        src = torch.as_tensor(self.prep.stage_src.astype(np.int64))
+        dst = torch.as_tensor(self.prep.stage_dst.astype(np.int64), device=self.sess.device)
+        for host, stg in t._arenas():
+            for l in range(t.n_layers):
+                a = stg[l][dst].cpu().view(torch.uint8)
+                b = host[l][src].view(torch.uint8)
+                assert torch.equal(a, b), f"staged layer {l} differs from the host blocks"
+
+    def check_published(self):
+        """Published units are READY under their epoch and their host blocks
+        hold the retained state (layer 0) in the slots the unit covers."""
+        t = self.tier
+        m = self.wl.model
+        if m.kv_dtype == "e4m3":
+            pages = retained_pages_e4m3(self.wl)
+        else:
+            pages = retained_pages(self.wl)
+        n = 0
+        for uid, epoch, blocks, slots in self.reservations:
+            q = t.cache.query(uid)
+            if uid in self.prep.cancelled:
+                assert q["state"] == 0, f"a failed writeback of unit {uid} is visible"
+                continue
+            assert q["state"] == 2 and q["epoch"] == epoch and q["leases"] == 0, q
+            for b, sl in zip(blocks, slots):
+                ref = pages[int(sl)]
+                filled = ref[-1]
+                if m.kv_dtype == "e4m3":
+                    kref, vref, ks, vs, _ = ref
+                    gk = t.host_k[0, b][:, torch.as_tensor(filled)].numpy()
+                    gv = t.host_v[0, b][:, torch.as_tensor(filled)].numpy()
+                    assert np.array_equal(e4m3_decode(gk), e4m3_decode(kref[:, filled]))
+                    assert np.array_equal(e4m3_decode(gv), e4m3_decode(vref[:, filled]))
+                    sc = t.host_scale[0, b].numpy()
+                    assert sc[0] == ks and sc[1] == vs
+                else:
+                    kref, vref, _ = ref
+                    gk = t.host_k[0, b].float().numpy()
+                    gv = t.host_v[0, b].float().numpy()
+                    assert np.array_equal(gk[:, filled].view(np.uint32), kref[:, filled].view(np.uint32))
+                    assert np.array_equal(gv[:, filled].view(np.uint32), vref[:, filled].view(np.uint32))
+                n += 1
+        return n

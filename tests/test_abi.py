@@ -39,7 +39,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_abi_version():
-    assert P.tsr_abi_version() == 2
+    assert P.tsr_abi_version() == 3
 
 
 @pytest.mark.parametrize("name", ["tiny", "small_bf16", "small_f32", "small_bf16_g8",
