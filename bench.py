@@ -160,6 +160,123 @@ def host_tier(torch, wl, plan, k, v, row_bytes, reps=5):
     }
 
 
+def host_tier_staged(torch, wl, reps=5, warmup=2):
+    """One layer of a batch through the host tier with device staging (the
+    paper's path for local hits): the hits' blocks are copied from the
+    pinned host cache into a bounded staging arena by the copy engines,
+    compose places them, and retained units are written back to the cache
+    through staging.  Timed two ways: in order (stage, then append, compose,
+    attention), and overlapped (append and the attention items that read no
+    composed key run while the copies are in flight; compose and the other
+    items follow).  Retain and the writeback are in both."""
+    from paper_2609_32999_amd import TSR_ATTN_AFTER_COMPOSE, TSR_ATTN_BEFORE_COMPOSE, staging
+    from paper_2609_32999_amd.host_tier import HostTier, plan_preparation
+    m = wl.model
+    B = m.page_size
+    hits = wl.hit_unit_ids()
+    hit_pages = sum(-(-int(wl.unit_len[u]) // B) for u in hits)
+    ret_pages = sum(-(-int(u.n_tokens) // B) for r in wl.requests for u in r.units
+                    if u.residency == 0 and u.retain)
+    n = hit_pages + ret_pages
+    # the cache also holds other units: one 32-page entry after every hit
+    # unit, so that no two hit units are adjacent and each is its own copy
+    gap = 32
+    tier = HostTier(m, n + gap * len(hits), n, wl.n_req_pages)
+    for i, uid in enumerate(hits):
+        if m.kv_dtype == "e4m3":
+            kc, vc, ks, vs = wl.unit_state_e4m3(uid)
+            sc = torch.from_numpy(np.stack([ks, vs], axis=1))[None]
+        else:
+            kc, vc = wl.unit_state(uid)
+            sc = None
+        kp = torch.from_numpy(staging._pages_from_tokens(kc, B))[None]
+        vp = torch.from_numpy(staging._pages_from_tokens(vc, B))[None]
+        tier.insert(uid, kp, vp, sc)
+        ep, blocks = tier.cache.reserve((1 << 40) + i, gap)
+        tier.cache.publish((1 << 40) + i, ep, blocks)
+    s = tier.sess
+    main = s.stream
+    prep0 = plan_preparation(tier.cache, wl.requests, n, B)
+    tier.stage(prep0, main)
+    plan = s.plan(prep0.requests)
+    q, k, v = staging.fresh_inputs(s, wl, plan)
+    out, lse = s.new_outputs(plan, with_lse=True)
+    E = lambda: torch.cuda.Event(enable_timing=True)
+
+    def close(prep):
+        tier.finish(prep)
+        for uid in prep.published:       # keep every step's directory state alike
+            tier.cache.evict(uid)
+
+    n_res0 = len(prep0.reservations)
+    tier.writeback(prep0, main)
+    torch.cuda.synchronize()
+    close(prep0)
+
+    def step(overlap):
+        prep = plan_preparation(tier.cache, wl.requests, n, B)
+        assert np.array_equal(prep.stage_dst, prep0.stage_dst) and \
+            len(prep.reservations) == n_res0
+        a, b, c = E(), E(), E()
+        a.record(main)
+        tier.stage(prep, main, wait=not overlap)
+        s.append(plan, k, v, stream=main)
+        if overlap:
+            s.attn(plan, q, out, lse, stream=main, part=TSR_ATTN_BEFORE_COMPOSE)
+            tier.wait_staged(prep, main)
+            s.compose(plan, stream=main)
+            s.attn(plan, q, out, lse, stream=main, part=TSR_ATTN_AFTER_COMPOSE)
+        else:
+            s.compose(plan, stream=main)
+            s.attn(plan, q, out, lse, stream=main)
+        b.record(main)
+        s.retain(plan, k, v, stream=main)
+        tier.writeback(prep, main)
+        c.record(main)
+        torch.cuda.synchronize()
+        close(prep)
+        return a.elapsed_time(b), a.elapsed_time(c)
+
+    def stage_only():
+        prep = plan_preparation(tier.cache, wl.requests, n, B)
+        a, b = E(), E()
+        a.record(main)
+        tier.stage(prep, main)
+        b.record(main)
+        torch.cuda.synchronize()
+        for uid, epoch, _, _ in prep.reservations:      # nothing was retained
+            tier.cache.cancel(uid, epoch)
+            tier.cache.reclaim(epoch)
+        prep.reservations = []
+        tier.finish(prep)
+        return a.elapsed_time(b)
+
+    for _ in range(warmup):
+        step(False), step(True), stage_only()
+    t_in, t_ov, t_st = [], [], []
+    for _ in range(reps):                  # alternate, so neither runs colder
+        t_in.append(step(False))
+        t_ov.append(step(True))
+        t_st.append(stage_only())
+    res = {}
+    for key, t in (("in_order", np.array(t_in)), ("overlapped", np.array(t_ov))):
+        res[key] = {"through_attention_us": float(t[:, 0].mean() * 1e3),
+                    "with_writeback_us": float(t[:, 1].mean() * 1e3)}
+    src, dst = prep0.stage_src, prep0.stage_dst
+    runs = 1 + int(((np.diff(src) != 1) | (np.diff(dst) != 1)).sum()) if len(src) else 0
+    res["stage_only_us"] = float(np.mean(t_st) * 1e3)
+    res["copies_per_arena"] = runs
+    row_bytes = 2 * m.n_kv_heads * m.head_dim * kv_elem_bytes(m.kv_dtype)
+    res["staged_bytes"] = int(len(prep0.stage_src)) * B * row_bytes
+    res["stage_link_gbps"] = res["staged_bytes"] / (res["stage_only_us"] * 1e-6) / 1e9
+    res["written_back_bytes"] = ret_pages * B * row_bytes
+    res["items_before_compose"] = plan.num_attn_items_part(TSR_ATTN_BEFORE_COMPOSE)
+    res["items_after_compose"] = plan.num_attn_items_part(TSR_ATTN_AFTER_COMPOSE)
+    log(f"[bench] host tier staged: {res}")
+    del tier
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -294,6 +411,8 @@ def main():
     w = kv_elem_bytes(m.kv_dtype)
     row_bytes = 2 * m.n_kv_heads * m.head_dim * w           # K + V of one token
     host = host_tier(torch, wl, plan, ks[0], vs[0], row_bytes) if args.host_tier else None
+    if host:
+        host["staged"] = host_tier_staged(torch, wl)
     gather_bytes = 2 * plan.num_gather_tokens * row_bytes   # read + write
     append_bytes = 2 * T * row_bytes
     retain_bytes = 2 * plan.num_retain_tokens * row_bytes

@@ -199,6 +199,30 @@ int32_t tsr_plan_num_retain_tokens(const tsr_plan* plan);
 /* Number of attention work items (row tile x KV head). */
 int32_t tsr_plan_num_attn_items(const tsr_plan* plan);
 
+/* The attention items in two parts, so that attention can start while the
+ * cached states are still on their way (Section 5.3: cache hits transfer
+ * while missing units are prefilled, and the request completes once every
+ * state is ready):
+ *   TSR_ATTN_BEFORE_COMPOSE  items none of whose loaded key tiles (masked
+ *                            keys included) holds a position tsr_compose_kv
+ *                            fills: they read only keys that tsr_append_kv
+ *                            writes, so they may run before compose (under
+ *                            TSR_SCOPE_LOCAL: the unit-local rows of missing
+ *                            units, among others);
+ *   TSR_ATTN_AFTER_COMPOSE   every other item.
+ * The two parts together compute exactly what TSR_ATTN_ALL computes; each
+ * is scheduled over the XCDs on its own.  Items of both parts write
+ * disjoint rows and heads of `out` and `lse`. */
+typedef enum {
+  TSR_ATTN_ALL = 0,
+  TSR_ATTN_BEFORE_COMPOSE = 1,
+  TSR_ATTN_AFTER_COMPOSE = 2
+} tsr_attn_part_id;
+
+/* Items of one part (padding to whole XCD rounds included); -1 for a NULL
+ * plan or an unknown part. */
+int32_t tsr_plan_num_attn_items_part(const tsr_plan* plan, int32_t part);
+
 /* Prompt position and request index of every computed row, in plan order.
  * host_positions: [T] (required); host_requests: [T] or NULL. */
 tsr_status tsr_plan_compute_positions(const tsr_plan* plan,
@@ -272,6 +296,13 @@ tsr_status tsr_append_kv(const tsr_plan* plan, const void* k, const void* v,
 tsr_status tsr_attn(const tsr_plan* plan, const void* q, const void* req_k,
                     const void* req_v, const float* req_scale, void* out,
                     float* lse, void* stream);
+
+/* tsr_attn restricted to one part of the items (a tsr_attn_part_id);
+ * TSR_ATTN_ALL is tsr_attn.  BEFORE_COMPOSE needs tsr_append_kv of the
+ * plan in stream order; AFTER_COMPOSE needs append and compose. */
+tsr_status tsr_attn_part(const tsr_plan* plan, int32_t part, const void* q,
+                         const void* req_k, const void* req_v, const float* req_scale,
+                         void* out, float* lse, void* stream);
 
 /* Retain (Section 5.4): for every MISS unit with retain = 1 and token j:
  *   K_pool[block j/B][slot j%B] = k (before RoPE), V_pool[...] = v

@@ -27,6 +27,7 @@ TSR_F32, TSR_BF16, TSR_E4M3 = 0, 1, 2
 DTYPE_CODES = {"f32": TSR_F32, "bf16": TSR_BF16, "e4m3": TSR_E4M3}
 TSR_MISS, TSR_HIT = 0, 1
 TSR_SCOPE_GLOBAL, TSR_SCOPE_LOCAL = 0, 1
+TSR_ATTN_ALL, TSR_ATTN_BEFORE_COMPOSE, TSR_ATTN_AFTER_COMPOSE = 0, 1, 2
 
 # Every symbol include/tsr.h declares.
 EXPORTS = (
@@ -34,6 +35,7 @@ EXPORTS = (
     "tsr_rope_table_init", "tsr_plan_workspace_size", "tsr_plan_create",
     "tsr_plan_num_compute_tokens", "tsr_plan_num_gather_tokens",
     "tsr_plan_num_retain_tokens", "tsr_plan_num_attn_items",
+    "tsr_plan_num_attn_items_part", "tsr_attn_part",
     "tsr_plan_compute_positions", "tsr_plan_row_kv_lo", "tsr_plan_destroy", "tsr_compose_kv",
     "tsr_prefill_attn", "tsr_append_kv", "tsr_attn", "tsr_retain_kv",
     "tsr_cache_create", "tsr_cache_destroy", "tsr_cache_reserve", "tsr_cache_publish",
@@ -97,6 +99,7 @@ def lib():
             "tsr_plan_num_gather_tokens": (c_int32, [P]),
             "tsr_plan_num_retain_tokens": (c_int32, [P]),
             "tsr_plan_num_attn_items": (c_int32, [P]),
+            "tsr_plan_num_attn_items_part": (c_int32, [P, c_int32]),
             "tsr_plan_compute_positions": (c_int32, [P, POINTER(c_int32), POINTER(c_int32)]),
             "tsr_plan_row_kv_lo": (c_int32, [P, POINTER(c_int32)]),
             "tsr_plan_destroy": (None, [P]),
@@ -105,6 +108,7 @@ def lib():
             "tsr_retain_kv": (c_int32, [P, P, P, P, P, P, P]),
             "tsr_append_kv": (c_int32, [P, P, P, P, P, P, P]),
             "tsr_attn": (c_int32, [P, P, P, P, P, P, P, P]),
+            "tsr_attn_part": (c_int32, [P, c_int32, P, P, P, P, P, P, P]),
             "tsr_cache_create": (c_int32, [c_int32, POINTER(c_void_p)]),
             "tsr_cache_destroy": (None, [P]),
             "tsr_cache_reserve": (c_int32, [P, c_uint64, c_int32, POINTER(c_uint64),
@@ -243,6 +247,9 @@ class Plan:
     @property
     def num_attn_items(self) -> int:
         return lib().tsr_plan_num_attn_items(self.handle)
+
+    def num_attn_items_part(self, part: int) -> int:
+        return lib().tsr_plan_num_attn_items_part(self.handle, part)
 
     def compute_positions(self):
         T = self.num_compute_tokens
@@ -392,3 +399,9 @@ def tsr_copy_blocks(dst, n_dst_blocks: int, dst_blocks, src, n_src_blocks: int, 
     _check(lib().tsr_copy_blocks(_ptr(dst), n_dst_blocks, _i32p(d), _ptr(src), n_src_blocks,
                                  _i32p(sb), len(d), block_bytes, n_layers, dst_layer_stride,
                                  src_layer_stride, _stream(stream)))
+
+
+def tsr_attn_part(plan: Plan, part: int, q, req_k, req_v, req_scale, out, lse=None,
+                  stream=None) -> None:
+    _check(lib().tsr_attn_part(plan.handle, part, _ptr(q), _ptr(req_k), _ptr(req_v),
+                               _ptr(req_scale), _ptr(out), _ptr(lse), _stream(stream)))

@@ -153,6 +153,8 @@ tsr_status tsr_plan_create(const tsr_model* model, const tsr_request* reqs,
       p->dev.rows = reinterpret_cast<const RowDesc*>(base + p->off_rows);
       p->dev.retain = reinterpret_cast<const RetainDesc*>(base + p->off_retain);
       p->dev.items = reinterpret_cast<const AttnItem*>(base + p->off_items);
+      for (int q = 0; q < 2; ++q)
+        p->dev.items_part[q] = reinterpret_cast<const AttnItem*>(base + p->off_items_part[q]);
       p->dev.block_tables = reinterpret_cast<const int32_t*>(base + p->off_bt);
       p->dev.gpages = reinterpret_cast<const PageDesc*>(base + p->off_gpages);
       p->dev.apages = reinterpret_cast<const PageDesc*>(base + p->off_apages);
@@ -171,6 +173,11 @@ int32_t tsr_plan_num_compute_tokens(const tsr_plan* p) { return p ? p->T : -1; }
 int32_t tsr_plan_num_gather_tokens(const tsr_plan* p) { return p ? p->n_gather : -1; }
 int32_t tsr_plan_num_retain_tokens(const tsr_plan* p) { return p ? p->n_retain : -1; }
 int32_t tsr_plan_num_attn_items(const tsr_plan* p) { return p ? p->n_items : -1; }
+
+int32_t tsr_plan_num_attn_items_part(const tsr_plan* p, int32_t part) {
+  if (!p || part < TSR_ATTN_ALL || part > TSR_ATTN_AFTER_COMPOSE) return -1;
+  return part == TSR_ATTN_ALL ? p->n_items : p->n_items_part[part - 1];
+}
 
 tsr_status tsr_plan_compute_positions(const tsr_plan* p, int32_t* host_positions,
                                       int32_t* host_requests) {
@@ -252,8 +259,9 @@ tsr_status tsr_prefill_attn(const tsr_plan* p, const void* q, const void* k,
     hipError_t e = is_e4m3(p) ? launch_append_e4m3(p, k, v, req_k, req_v, req_scale, s)
                               : launch_append(p, k, v, req_k, req_v, s);
     if (e != hipSuccess) return device_fail("append launch", e);
-    e = is_e4m3(p) ? launch_attn_e4m3(p, q, req_k, req_v, req_scale, out, lse, s)
-                   : launch_attn(p, q, req_k, req_v, out, lse, s);
+    e = is_e4m3(p) ? launch_attn_e4m3(p, p->dev.items, p->n_items, q, req_k, req_v,
+                                      req_scale, out, lse, s)
+                   : launch_attn(p, p->dev.items, p->n_items, q, req_k, req_v, out, lse, s);
     if (e != hipSuccess) return device_fail("attention launch", e);
     return TSR_OK;
   });
@@ -279,24 +287,37 @@ tsr_status tsr_append_kv(const tsr_plan* p, const void* k, const void* v,
   });
 }
 
-tsr_status tsr_attn(const tsr_plan* p, const void* q, const void* req_k,
-                    const void* req_v, const float* req_scale, void* out,
-                    float* lse, void* stream) {
+tsr_status tsr_attn_part(const tsr_plan* p, int32_t part, const void* q,
+                         const void* req_k, const void* req_v, const float* req_scale,
+                         void* out, float* lse, void* stream) {
   return guarded([&]() -> tsr_status {
     tsr_status st = check_exec(p);
     if (st != TSR_OK) return st;
+    if (part < TSR_ATTN_ALL || part > TSR_ATTN_AFTER_COMPOSE) {
+      set_error("attn: part must be TSR_ATTN_ALL, _BEFORE_COMPOSE or _AFTER_COMPOSE");
+      return TSR_ERR_INVALID_ARG;
+    }
     if ((st = check_scales(p, nullptr, req_scale, false, true)) != TSR_OK) return st;
     if (p->T == 0) return TSR_OK;
     if (!q || !req_k || !req_v || !out) {
       set_error("attn: a required pointer is NULL");
       return TSR_ERR_INVALID_ARG;
     }
+    const AttnItem* items = part == TSR_ATTN_ALL ? p->dev.items : p->dev.items_part[part - 1];
+    const int32_t n = part == TSR_ATTN_ALL ? p->n_items : p->n_items_part[part - 1];
     hipStream_t s = static_cast<hipStream_t>(stream);
-    hipError_t e = is_e4m3(p) ? launch_attn_e4m3(p, q, req_k, req_v, req_scale, out, lse, s)
-                              : launch_attn(p, q, req_k, req_v, out, lse, s);
+    hipError_t e = is_e4m3(p)
+                       ? launch_attn_e4m3(p, items, n, q, req_k, req_v, req_scale, out, lse, s)
+                       : launch_attn(p, items, n, q, req_k, req_v, out, lse, s);
     if (e != hipSuccess) return device_fail("attention launch", e);
     return TSR_OK;
   });
+}
+
+tsr_status tsr_attn(const tsr_plan* p, const void* q, const void* req_k,
+                    const void* req_v, const float* req_scale, void* out,
+                    float* lse, void* stream) {
+  return tsr_attn_part(p, TSR_ATTN_ALL, q, req_k, req_v, req_scale, out, lse, stream);
 }
 
 tsr_status tsr_retain_kv(const tsr_plan* p, const void* k, const void* v,

@@ -472,18 +472,19 @@ int ilog2(int x) {
 
 }  // namespace
 
-hipError_t launch_attn(const tsr_plan* p, const void* q, const void* req_k,
+hipError_t launch_attn(const tsr_plan* p, const AttnItem* items, int32_t n_items,
+                       const void* q, const void* req_k,
                        const void* req_v, void* out, float* lse, hipStream_t s) {
-  if (p->n_items == 0 || p->T == 0) return hipSuccess;
+  if (n_items == 0 || p->T == 0) return hipSuccess;
   const tsr_model& m = p->model;
   const int lp = ilog2(m.page_size);
   const int G = m.n_q_heads / m.n_kv_heads;
-  const dim3 grid(p->n_items), block(256);
+  const dim3 grid(n_items), block(256);
   if (m.act_dtype == TSR_F32) {
 #define TSR_F32K(DIM)                                                             \
   hipLaunchKernelGGL(attn_f32_kernel<DIM>, grid, block, 0, s,                     \
                      static_cast<const float*>(q), static_cast<const float*>(req_k), \
-                     static_cast<const float*>(req_v), p->dev.items,               \
+                     static_cast<const float*>(req_v), items,                       \
                      p->dev.block_tables, p->dev.rows, p->dev.rope_cos,            \
                      p->dev.rope_sin, static_cast<float*>(out), lse, m.n_q_heads,  \
                      m.n_kv_heads, lp, p->scale)
@@ -500,7 +501,7 @@ hipError_t launch_attn(const tsr_plan* p, const void* q, const void* req_k,
 #define TSR_MFMA(GG)                                                               \
   hipLaunchKernelGGL(attn_mfma_kernel<GG>, grid, block, 0, s,                      \
                      static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(req_k), \
-                     static_cast<const uint16_t*>(req_v), p->dev.items,             \
+                     static_cast<const uint16_t*>(req_v), items,                     \
                      p->dev.block_tables, p->dev.rows, p->dev.rope_cos,             \
                      p->dev.rope_sin, static_cast<uint16_t*>(out), lse,             \
                      m.n_q_heads, m.n_kv_heads, lp, p->scale, sl2e)

@@ -376,18 +376,19 @@ int ilog2(int x) {
 
 }  // namespace
 
-hipError_t launch_attn_e4m3(const tsr_plan* p, const void* q, const void* req_k,
+hipError_t launch_attn_e4m3(const tsr_plan* p, const AttnItem* items, int32_t n_items,
+                            const void* q, const void* req_k,
                             const void* req_v, const float* req_scale, void* out,
                             float* lse, hipStream_t s) {
-  if (p->n_items == 0 || p->T == 0) return hipSuccess;
+  if (n_items == 0 || p->T == 0) return hipSuccess;
   const tsr_model& m = p->model;
   const int lp = ilog2(m.page_size);
   const int G = m.n_q_heads / m.n_kv_heads;
   const float sl2e = (float)((double)p->scale * 1.4426950408889634);
 #define TSR_FP8(GG)                                                                   \
-  hipLaunchKernelGGL(attn_fp8_kernel<GG>, dim3(p->n_items), dim3(256), 0, s,          \
+  hipLaunchKernelGGL(attn_fp8_kernel<GG>, dim3(n_items), dim3(256), 0, s,             \
                      static_cast<const uint16_t*>(q), static_cast<const uint8_t*>(req_k), \
-                     static_cast<const uint8_t*>(req_v), req_scale, p->dev.items,     \
+                     static_cast<const uint8_t*>(req_v), req_scale, items,            \
                      p->dev.block_tables, p->dev.rows, p->dev.rope_cos,               \
                      p->dev.rope_sin, static_cast<uint16_t*>(out), lse, m.n_q_heads,  \
                      m.n_kv_heads, lp, sl2e)

@@ -114,6 +114,8 @@ tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
   std::vector<RetainDesc> retain;
   std::vector<int32_t> bts;
   std::vector<int32_t> bt_off(n_req), bt_len(n_req), req_row0(n_req + 1, 0);
+  // per request, the position ranges [a, b) that compose fills
+  std::vector<std::vector<std::pair<int32_t, int32_t>>> gathered(n_req);
   p->row_pos.clear();
   p->row_req.clear();
   p->row_lo.clear();
@@ -294,6 +296,8 @@ tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
         p->row_lo.push_back(j < wnd ? 0 : u.position);
       }
       if (hit) {
+        if (ncomp < u.n_tokens)
+          gathered[r].push_back({u.position + ncomp, u.position + u.n_tokens});
         for (int32_t j = ncomp; j < u.n_tokens; ++j)
           gather.push_back({u.pool_pages[j / B] * B + j % B,
                             req_slot(u.position + j), u.position + j, 0});
@@ -322,7 +326,7 @@ tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
   // (adjacent in the launch order, so the repeat reads hit L2).
   const int G = m.n_q_heads / Hkv;
   const int hsplit = (m.act_dtype == TSR_BF16 && G > 4) ? G / 4 : 1;
-  struct Item { AttnItem it; int64_t cost; int group; };
+  struct Item { AttnItem it; int64_t cost; int group; int part; };
   std::vector<Item> items;
   int32_t max_kv = 0;
   for (int r = 0; r < n_req; ++r) {
@@ -335,10 +339,18 @@ tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
         const int32_t n = std::min(kTileRows, a1 - t0);
         const int32_t lo = p->row_pos[t0], hi = p->row_pos[t0 + n - 1];
         max_kv = std::max(max_kv, hi + 1);
+        // part 1 if a gathered position lies in the key tiles the kernels
+        // load for this item (masked keys included): [tile of kv_lo, end of
+        // the tile of hi]
+        const int32_t klo = kv_lo / kKvTile * kKvTile;
+        const int32_t khi = (hi / kKvTile + 1) * kKvTile;
+        int part = 0;
+        for (const auto& iv : gathered[r])
+          if (iv.first < khi && iv.second > klo) part = 1;
         for (int g = 0; g < Hkv; ++g)
           for (int hs = 0; hs < hsplit; ++hs) {
             AttnItem a{t0, n, hi + 1, lo, g, bt_off[r], bt_len[r], 4 * hs, kv_lo, {0, 0, 0}};
-            items.push_back({a, (int64_t)(hi + 1 - kv_lo), r * Hkv + g});
+            items.push_back({a, (int64_t)(hi + 1 - kv_lo), r * Hkv + g, part});
           }
       }
       a0 = a1;
@@ -349,39 +361,48 @@ tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
   // balanced by cost (longest group first onto the lightest bin) and each
   // bin is issued longest item first (measured: issuing a bin group by
   // group for L2 locality lost more to the tail than it gained).  Short bins
-  // are padded with empty items.
-  std::vector<int64_t> gcost((size_t)std::max(1, n_req * Hkv), 0);
-  for (const Item& x : items) gcost[x.group] += x.cost;
-  std::vector<int> gorder(gcost.size());
-  std::iota(gorder.begin(), gorder.end(), 0);
-  std::stable_sort(gorder.begin(), gorder.end(),
-                   [&](int a, int b) { return gcost[a] > gcost[b]; });
-  std::vector<int> gbin(gcost.size(), 0);
-  int64_t bin_load[kNumXcd] = {0};
-  for (int g : gorder) {
-    int best = 0;
-    for (int b = 1; b < kNumXcd; ++b)
-      if (bin_load[b] < bin_load[best]) best = b;
-    gbin[g] = best;
-    bin_load[best] += gcost[g];
-  }
-  std::vector<std::vector<AttnItem>> bins(kNumXcd);
+  // are padded with empty items.  The full schedule and each part's are
+  // built the same way.
   std::stable_sort(items.begin(), items.end(),
                    [](const Item& a, const Item& b) { return a.cost > b.cost; });
-  for (const Item& x : items) bins[gbin[x.group]].push_back(x.it);
-  size_t per_bin = 0;
-  for (auto& b : bins) per_bin = std::max(per_bin, b.size());
-  std::vector<AttnItem> order;
-  order.reserve(per_bin * kNumXcd);
-  for (size_t i = 0; i < per_bin; ++i)
-    for (int b = 0; b < kNumXcd; ++b)
-      order.push_back(i < bins[b].size() ? bins[b][i]
-                                         : AttnItem{0, 0, 0, 0, 0, 0, 0, 0, 0, {0, 0, 0}});
+  auto schedule = [&](int part) {
+    std::vector<int64_t> gcost((size_t)std::max(1, n_req * Hkv), 0);
+    for (const Item& x : items)
+      if (part < 0 || x.part == part) gcost[x.group] += x.cost;
+    std::vector<int> gorder(gcost.size());
+    std::iota(gorder.begin(), gorder.end(), 0);
+    std::stable_sort(gorder.begin(), gorder.end(),
+                     [&](int a, int b) { return gcost[a] > gcost[b]; });
+    std::vector<int> gbin(gcost.size(), 0);
+    int64_t bin_load[kNumXcd] = {0};
+    for (int g : gorder) {
+      int best = 0;
+      for (int b = 1; b < kNumXcd; ++b)
+        if (bin_load[b] < bin_load[best]) best = b;
+      gbin[g] = best;
+      bin_load[best] += gcost[g];
+    }
+    std::vector<std::vector<AttnItem>> bins(kNumXcd);
+    for (const Item& x : items)
+      if (part < 0 || x.part == part) bins[gbin[x.group]].push_back(x.it);
+    size_t per_bin = 0;
+    for (auto& b : bins) per_bin = std::max(per_bin, b.size());
+    std::vector<AttnItem> order;
+    order.reserve(per_bin * kNumXcd);
+    for (size_t i = 0; i < per_bin; ++i)
+      for (int b = 0; b < kNumXcd; ++b)
+        order.push_back(i < bins[b].size() ? bins[b][i]
+                                           : AttnItem{0, 0, 0, 0, 0, 0, 0, 0, 0, {0, 0, 0}});
+    return order;
+  };
+  const std::vector<AttnItem> order = schedule(-1);
+  const std::vector<AttnItem> order_part[2] = {schedule(0), schedule(1)};
 
   p->T = (int32_t)rows.size();
   p->n_gather = (int32_t)gather.size();
   p->n_retain = (int32_t)retain.size();
   p->n_items = (int32_t)order.size();
+  for (int q = 0; q < 2; ++q) p->n_items_part[q] = (int32_t)order_part[q].size();
   p->max_kv_len = max_kv;
 
   // device image: arrays at 256-byte aligned offsets
@@ -390,6 +411,10 @@ tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
   p->off_rows = off;    off = align_up(off + rows.size() * sizeof(RowDesc), 256);
   p->off_retain = off;  off = align_up(off + retain.size() * sizeof(RetainDesc), 256);
   p->off_items = off;   off = align_up(off + order.size() * sizeof(AttnItem), 256);
+  for (int q = 0; q < 2; ++q) {
+    p->off_items_part[q] = off;
+    off = align_up(off + order_part[q].size() * sizeof(AttnItem), 256);
+  }
   p->off_bt = off;      off = align_up(off + bts.size() * sizeof(int32_t), 256);
   p->off_gpages = off;  off = align_up(off + gpages.size() * sizeof(PageDesc), 256);
   p->off_apages = off;  off = align_up(off + apages.size() * sizeof(PageDesc), 256);
@@ -406,6 +431,8 @@ tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
   put(p->off_rows, rows.data(), rows.size() * sizeof(RowDesc));
   put(p->off_retain, retain.data(), retain.size() * sizeof(RetainDesc));
   put(p->off_items, order.data(), order.size() * sizeof(AttnItem));
+  for (int q = 0; q < 2; ++q)
+    put(p->off_items_part[q], order_part[q].data(), order_part[q].size() * sizeof(AttnItem));
   put(p->off_bt, bts.data(), bts.size() * sizeof(int32_t));
   put(p->off_gpages, gpages.data(), gpages.size() * sizeof(PageDesc));
   put(p->off_apages, apages.data(), apages.size() * sizeof(PageDesc));

@@ -79,6 +79,7 @@ struct PlanDev {
   const RowDesc* rows;
   const RetainDesc* retain;
   const AttnItem* items;
+  const AttnItem* items_part[2];
   const int32_t* block_tables;
   const PageDesc* gpages;  // e4m3 plans only
   const PageDesc* apages;
@@ -99,11 +100,15 @@ struct tsr_plan {
   int32_t n_gather;
   int32_t n_retain;
   int32_t n_items;          // attention items incl. padding
+  // the items split by whether their key tiles hold a gathered position:
+  // [0] none (runnable before compose), [1] some; each scheduled on its own
+  int32_t n_items_part[2];
   int32_t max_kv_len;
   int32_t n_gpages, n_apages, n_rpages;   // e4m3 plans only
   std::vector<int32_t> row_pos, row_req, row_lo;
   std::vector<char> image;  // host copy of the device image
   size_t off_gather, off_rows, off_retain, off_items, off_bt, ws_bytes;
+  size_t off_items_part[2];
   size_t off_gpages, off_apages, off_rpages;
   const void* rope_table;   // device
   void* ws;                 // device, NULL for host-only plans
@@ -154,7 +159,10 @@ hipError_t launch_compose(const tsr_plan* p, const void* pool_k,
                           int64_t req_stride, hipStream_t s);
 hipError_t launch_append(const tsr_plan* p, const void* k, const void* v,
                          void* req_k, void* req_v, hipStream_t s);
-hipError_t launch_attn(const tsr_plan* p, const void* q, const void* req_k,
+// Attention launchers run `n_items` items from `items` (a plan's full
+// schedule or one of its parts).
+hipError_t launch_attn(const tsr_plan* p, const AttnItem* items, int32_t n_items,
+                       const void* q, const void* req_k,
                        const void* req_v, void* out, float* lse, hipStream_t s);
 hipError_t launch_retain(const tsr_plan* p, const void* k, const void* v,
                          void* pool_k, void* pool_v, hipStream_t s);
@@ -172,7 +180,8 @@ hipError_t launch_append_e4m3(const tsr_plan* p, const void* k, const void* v,
 hipError_t launch_retain_e4m3(const tsr_plan* p, const void* k, const void* v,
                               void* pool_k, void* pool_v, float* pool_scale,
                               hipStream_t s);
-hipError_t launch_attn_e4m3(const tsr_plan* p, const void* q, const void* req_k,
+hipError_t launch_attn_e4m3(const tsr_plan* p, const AttnItem* items, int32_t n_items,
+                            const void* q, const void* req_k,
                             const void* req_v, const float* req_scale, void* out,
                             float* lse, hipStream_t s);
 

@@ -53,6 +53,7 @@ class Prepared:
     published: list = field(default_factory=list)      # unit ids made READY
     cancelled: list = field(default_factory=list)      # unit ids whose writeback failed
     errors: list = field(default_factory=list)         # messages of failed enqueues
+    out_blocks: np.ndarray = None                      # cache blocks written back, in order
 
 
 class HostTier:
@@ -69,37 +70,80 @@ class HostTier:
         self.n_layers = n_layers
         self.page_size = shape.page_size
         page = (shape.n_kv_heads, shape.page_size, shape.head_dim)
-        self.host_k = torch.empty((n_layers, n_blocks, *page), dtype=s.kv_dtype, pin_memory=True)
-        self.host_v = torch.empty((n_layers, n_blocks, *page), dtype=s.kv_dtype, pin_memory=True)
-        self.host_scale = (torch.empty((n_layers, n_blocks, 2), dtype=torch.float32,
-                                       pin_memory=True) if s.e4m3 else None)
+        # [K|V][layer][block], like the staging arena: one strided copy per
+        # run of blocks moves K and V of every layer
+        self.host_kv = torch.empty((2, n_layers, n_blocks, *page), dtype=s.kv_dtype,
+                                   pin_memory=True)
+        self.host_k, self.host_v = self.host_kv[0], self.host_kv[1]
+        self.host_scale = self._bounce_in = self._bounce_out = None
+        if s.e4m3:
+            self.host_scale = torch.empty((n_layers, n_blocks, 2), dtype=torch.float32,
+                                          pin_memory=True)
+            # page scales are 8 bytes a block: gathered on the host into a
+            # pinned bounce buffer and moved in one copy, not one per run
+            self._bounce_in = torch.empty((n_layers, n_staging, 2), dtype=torch.float32,
+                                          pin_memory=True)
+            self._bounce_out = torch.empty_like(self._bounce_in)
+        self._bounce_busy = None            # event of the last copy reading _bounce_in
+        self._out_pending = None            # batch whose _bounce_out finish() has to scatter
         self.copy_stream = torch.cuda.Stream(device=s.device)
 
-    # ------------------------------------------------------------ arenas
-    def _arenas(self):
-        """(host, staging) tensor pairs: K, V and, for e4m3, the scales."""
-        s = self.sess
-        pairs = [(self.host_k, s.pool_k), (self.host_v, s.pool_v)]
-        if s.e4m3:
-            pairs.append((self.host_scale, s.pool_scale))
-        return pairs
+    # ------------------------------------------------------------ copies
+    # Slab pitch above which K/V/layers are not folded into one strided copy.
+    MAX_PITCH = 1 << 32
 
-    def _copy(self, to_staging: bool, host_blocks, slots, stream) -> None:
-        """One copy per run of consecutive blocks and layer (layer pitches of
-        a large host arena run to gigabytes, so layers are not folded into
-        one strided copy here)."""
+    def _copy_kv(self, to_staging: bool, host_blocks, slots, stream) -> None:
+        """K and V of every layer for the listed blocks: one strided copy per
+        run of consecutive (block, slot) pairs, the 2 * n_layers slabs of an
+        arena being its rows."""
         if len(slots) == 0:
             return
-        for host, stg in self._arenas():
-            blk = host[0, 0].nbytes
+        s = self.sess
+        blk = self.host_kv[0, 0, 0].nbytes
+        hp, sp = self.host_k[0].nbytes, s.pool_k[0].nbytes     # slab pitches
+        host = (self.host_kv, self.n_blocks, host_blocks)
+        stg = (s.pool_kv, self.n_staging, slots)
+        dst, src = (stg, host) if to_staging else (host, stg)
+        if max(hp, sp) <= self.MAX_PITCH:
+            B.tsr_copy_blocks(*dst, *src, blk, n_layers=2 * self.n_layers,
+                              dst_layer_stride=dst[0][0, 0].nbytes,
+                              src_layer_stride=src[0][0, 0].nbytes, stream=stream)
+            return
+        for kv in range(2):
             for l in range(self.n_layers):
-                h, g = host[l], stg[l]
-                if to_staging:
-                    B.tsr_copy_blocks(g, self.n_staging, slots, h, self.n_blocks, host_blocks,
-                                      blk, stream=stream)
-                else:
-                    B.tsr_copy_blocks(h, self.n_blocks, host_blocks, g, self.n_staging, slots,
-                                      blk, stream=stream)
+                B.tsr_copy_blocks(dst[0][kv, l], dst[1], dst[2], src[0][kv, l], src[1], src[2],
+                                  blk, stream=stream)
+
+    def _stage_scales(self, host_blocks, slots, stream) -> None:
+        """e4m3: gather the blocks' page scales into the bounce buffer on the
+        host, then one copy into the staging slots."""
+        n = len(slots)
+        if n == 0 or self.host_scale is None:
+            return
+        if self._bounce_busy is not None:
+            self._bounce_busy.synchronize()
+        idx = torch.from_numpy(np.asarray(host_blocks, dtype=np.int64))
+        for l in range(self.n_layers):
+            self._bounce_in[l, :n] = self.host_scale[l, idx]
+        st = self.sess.pool_scale
+        B.tsr_copy_blocks(st, self.n_staging, slots, self._bounce_in, self.n_staging,
+                          np.arange(n, dtype=np.int32), 8, n_layers=self.n_layers,
+                          dst_layer_stride=st[0].nbytes,
+                          src_layer_stride=self._bounce_in[0].nbytes, stream=stream)
+        self._bounce_busy = torch.cuda.Event()
+        self._bounce_busy.record(stream)
+
+    def _unstage_scales(self, slots, stream) -> None:
+        """e4m3: copy the retained slots' page scales into the outgoing bounce
+        buffer (scattered into the cache by finish())."""
+        n = len(slots)
+        if n == 0 or self.host_scale is None:
+            return
+        st = self.sess.pool_scale
+        B.tsr_copy_blocks(self._bounce_out, self.n_staging, np.arange(n, dtype=np.int32), st,
+                          self.n_staging, slots, 8, n_layers=self.n_layers,
+                          dst_layer_stride=self._bounce_out[0].nbytes,
+                          src_layer_stride=st[0].nbytes, stream=stream)
 
     # ---------------------------------------------------------- contents
     def insert(self, unit_id: int, k_pages, v_pages, scales=None) -> np.ndarray:
@@ -117,24 +161,39 @@ class HostTier:
         return blocks
 
     # ------------------------------------------------------- preparation
-    def prepare(self, requests, stream=None, fail_units=()) -> Prepared:
+    def prepare(self, requests, stream=None, fail_units=(), wait: bool = True) -> Prepared:
         """Revalidate the batch's hits and assign staging (plan_preparation),
-        then enqueue the host-to-staging copies on the copy stream; `stream`
-        (the stream compose will run on) waits for them."""
-        s = stream or self.sess.stream
+        then enqueue the host-to-staging copies on the copy stream.  With
+        `wait`, `stream` (the stream compose will run on) waits for them at
+        once; otherwise the caller calls wait_staged() before compose and may
+        enqueue work that needs no staged state (append, the attention items
+        before compose) in between."""
         prep = plan_preparation(self.cache, requests, self.n_staging, self.page_size,
                                 fail_units)
+        self.stage(prep, stream, wait)
+        return prep
+
+    def stage(self, prep: Prepared, stream=None, wait: bool = True) -> None:
+        """Enqueue a prepared batch's host-to-staging copies on the copy
+        stream, after the work already on `stream`; with `wait`, `stream`
+        waits for them."""
+        s = stream or self.sess.stream
         # the copies overwrite staging: wait for earlier work that reads it
         self.copy_stream.wait_stream(s)
         try:
-            self._copy(True, prep.stage_src, prep.stage_dst, self.copy_stream)
+            self._copy_kv(True, prep.stage_src, prep.stage_dst, self.copy_stream)
+            self._stage_scales(prep.stage_src, prep.stage_dst, self.copy_stream)
         except B.TsrError:
             _undo(self.cache, prep, self.copy_stream)
             raise
         prep.staged = torch.cuda.Event()
         prep.staged.record(self.copy_stream)
-        s.wait_event(prep.staged)
-        return prep
+        if wait:
+            s.wait_event(prep.staged)
+
+    def wait_staged(self, prep: Prepared, stream=None) -> None:
+        """Make `stream` wait for the batch's staging copies."""
+        (stream or self.sess.stream).wait_event(prep.staged)
 
     # --------------------------------------------------------- retention
     def writeback(self, prep: Prepared, stream=None, fail_units=()) -> None:
@@ -142,14 +201,20 @@ class HostTier:
         units' staging blocks into their reserved host blocks on the copy
         stream.  `fail_units` marks those units' writeback as failed."""
         s = stream or self.sess.stream
+        if self._out_pending is not None:
+            raise RuntimeError("finish() the previous batch before the next writeback")
         self.copy_stream.wait_stream(s)
         ok = [(u, e, b, sl) for (u, e, b, sl) in prep.reservations if u not in fail_units]
         prep.cancelled = [u for (u, e, b, sl) in prep.reservations if u in fail_units]
         if ok:
             hb = np.concatenate([b for (_, _, b, _) in ok])
             sl = np.concatenate([x for (_, _, _, x) in ok])
+            prep.out_blocks = hb
+            if self.host_scale is not None:
+                self._out_pending = prep
             try:
-                self._copy(False, hb, sl, self.copy_stream)
+                self._copy_kv(False, hb, sl, self.copy_stream)
+                self._unstage_scales(sl, self.copy_stream)
             except B.TsrError as e:
                 # a failed writeback only loses future reuse: nothing of this
                 # batch is published, and finish() reclaims once drained
@@ -173,6 +238,12 @@ class HostTier:
             raise RuntimeError("writeback() was not called for a batch with retained units")
         if prep.written is not None:
             prep.written.synchronize()
+        if self._out_pending is prep:
+            self._out_pending = None
+        if self.host_scale is not None and prep.out_blocks is not None and not prep.errors:
+            idx = torch.from_numpy(np.asarray(prep.out_blocks, dtype=np.int64))
+            for l in range(self.n_layers):
+                self.host_scale[l, idx] = self._bounce_out[l, :len(idx)]
         for uid, epoch, blocks, _ in prep.reservations:
             if uid in prep.cancelled:
                 self.cache.cancel(uid, epoch)
@@ -189,58 +260,55 @@ def plan_preparation(cache, requests, n_staging: int, page_size: int,
 
     For every HIT, in request order: revalidate it against the directory by
     taking a read lease (a unit staged once serves every request of the
-    batch that hits it) and give its blocks consecutive staging slots.  A
-    hit that is not READY, whose block count changed, that does not fit in
-    the staging arena, or that is listed in `fail_units` (a stand-in for a
-    failed or timed-out transfer) is released and falls back to MISS: its
-    tokens become computed rows and it is not retained.
+    batch that hits it).  A hit that is not READY, whose block count
+    changed, that does not fit in the staging arena, or that is listed in
+    `fail_units` (a stand-in for a failed or timed-out transfer) is released
+    and falls back to MISS: its tokens become computed rows and it is not
+    retained.
     For every MISS with retain = 1: reserve its cache blocks under a new
-    storage epoch and give it staging slots for the retain kernel.  If an
-    entry exists (another writer holds it PENDING, or it is READY), there is
-    no room, or the unit is already reserved in this batch, retention is
-    declined (retain = 0) and the request proceeds (Section 5.4).
-    Returns the requests rewritten so that pool pages name staging slots."""
+    storage epoch.  If an entry exists (another writer holds it PENDING, or
+    it is READY), there is no room, or the unit is already reserved in this
+    batch, retention is declined (retain = 0) and the request proceeds
+    (Section 5.4).
+    Staging slots: the staged hits first, ordered by their first cache
+    block (so that units adjacent in the cache stay adjacent in staging and
+    their copies merge), then the retained units.  Returns the requests
+    rewritten so that pool pages name staging slots."""
     prep = Prepared(requests=[])
-    staged = {}
-    src, dst = [], []
-    next_slot = 0
-    reserved_ids = set()
+    staged = {}                 # unit id -> (epoch, cache blocks)
+    retained = {}               # unit id -> (epoch, cache blocks)
+    used = 0
+    rows = []                   # per request: list of (unit copy, kind)
     for ri, r in enumerate(requests):
         units = []
         for ui, u in enumerate(r.units):
             nb = -(-int(u.n_tokens) // page_size)
             nu = copy.copy(u)
+            kind = None
             if u.residency == B.TSR_HIT:
-                if u.unit_id in staged:
-                    nu.pool_pages = staged[u.unit_id]
-                    units.append(nu)
-                    continue
-                try:
-                    got = cache.acquire(u.unit_id, nb)
-                except B.TsrError:
-                    got = None                      # not READY any more
-                if got is not None and (len(got[1]) != nb or next_slot + nb > n_staging
-                                        or u.unit_id in fail_units):
-                    cache.release(u.unit_id, got[0])
-                    got = None
-                if got is None:
-                    nu.residency = B.TSR_MISS
-                    nu.retain = 0
-                    nu.pool_pages = np.zeros(0, dtype=np.int32)
-                    prep.fallbacks.append((ri, ui))
-                    units.append(nu)
-                    continue
-                epoch, blocks = got
-                slots = np.arange(next_slot, next_slot + nb, dtype=np.int32)
-                next_slot += nb
-                prep.leases.append((u.unit_id, epoch))
-                src.append(blocks)
-                dst.append(slots)
-                staged[u.unit_id] = slots
-                nu.pool_pages = slots
+                if u.unit_id not in staged:
+                    try:
+                        got = cache.acquire(u.unit_id, nb)
+                    except B.TsrError:
+                        got = None                  # not READY any more
+                    if got is not None and (len(got[1]) != nb or used + nb > n_staging
+                                            or u.unit_id in fail_units):
+                        cache.release(u.unit_id, got[0])
+                        got = None
+                    if got is None:
+                        nu.residency = B.TSR_MISS
+                        nu.retain = 0
+                        nu.pool_pages = np.zeros(0, dtype=np.int32)
+                        prep.fallbacks.append((ri, ui))
+                        units.append((nu, None))
+                        continue
+                    staged[u.unit_id] = got
+                    prep.leases.append((u.unit_id, got[0]))
+                    used += nb
+                kind = "hit"
             elif u.retain:
                 got = None
-                if next_slot + nb <= n_staging and u.unit_id not in reserved_ids:
+                if used + nb <= n_staging and u.unit_id not in retained:
                     try:
                         got = cache.reserve(u.unit_id, nb)
                     except B.TsrError:
@@ -249,17 +317,38 @@ def plan_preparation(cache, requests, n_staging: int, page_size: int,
                     nu.retain = 0
                     nu.pool_pages = np.zeros(0, dtype=np.int32)
                     prep.declined.append((ri, ui))
-                    units.append(nu)
+                    units.append((nu, None))
                     continue
-                epoch, blocks = got
-                slots = np.arange(next_slot, next_slot + nb, dtype=np.int32)
-                next_slot += nb
-                reserved_ids.add(u.unit_id)
-                prep.reservations.append((u.unit_id, epoch, blocks, slots))
-                nu.pool_pages = slots
-            units.append(nu)
+                retained[u.unit_id] = got
+                used += nb
+                kind = "retain"
+            units.append((nu, kind))
+        rows.append((r, units))
+    # slots: staged hits by first cache block, then retained units in order
+    slots = {}
+    nxt = 0
+    src, dst = [], []
+    for uid, (epoch, blocks) in sorted(staged.items(), key=lambda kv: int(kv[1][1][0])):
+        sl = np.arange(nxt, nxt + len(blocks), dtype=np.int32)
+        nxt += len(blocks)
+        slots[uid] = sl
+        src.append(blocks)
+        dst.append(sl)
+    for uid, (epoch, blocks) in retained.items():
+        sl = np.arange(nxt, nxt + len(blocks), dtype=np.int32)
+        nxt += len(blocks)
+        slots[("r", uid)] = sl
+        prep.reservations.append((uid, epoch, blocks, sl))
+    for r, units in rows:
+        out = []
+        for nu, kind in units:
+            if kind == "hit":
+                nu.pool_pages = slots[nu.unit_id]
+            elif kind == "retain":
+                nu.pool_pages = slots[("r", nu.unit_id)]
+            out.append(nu)
         nr = copy.copy(r)
-        nr.units = units
+        nr.units = out
         prep.requests.append(nr)
     prep.stage_src = np.concatenate(src) if src else np.zeros(0, np.int32)
     prep.stage_dst = np.concatenate(dst) if dst else np.zeros(0, np.int32)

@@ -68,10 +68,12 @@ class Session:
             raise ValueError(f"pool must be 'device' or 'host', not {pool!r}")
         self.pool_tier = pool
         pool_dev = dict(device=self.device) if pool == "device" else dict(pin_memory=True)
-        self.pool_k = torch.empty((n_layers, n_pool_pages, *page), dtype=self.kv_dtype,
-                                  **pool_dev)
-        self.pool_v = torch.empty((n_layers, n_pool_pages, *page), dtype=self.kv_dtype,
-                                  **pool_dev)
+        # K and V in one allocation, [K|V][layer][page]: every (K|V, layer)
+        # slab sits a whole arena after the previous one, so one strided copy
+        # can move a run of pages for K, V and every layer at once
+        self.pool_kv = torch.empty((2, n_layers, n_pool_pages, *page), dtype=self.kv_dtype,
+                                   **pool_dev)
+        self.pool_k, self.pool_v = self.pool_kv[0], self.pool_kv[1]
         self.req_k = torch.empty((n_layers, n_req_pages, *page), dtype=self.kv_dtype,
                                  device=self.device)
         self.req_v = torch.empty_like(self.req_k)
@@ -84,11 +86,13 @@ class Session:
                                          device=self.device)
         # addresses the kernels use for the pool arenas
         self._pool_base = {}
-        for name in ("pool_k", "pool_v", "pool_scale"):
-            t = getattr(self, name)
-            if t is not None:
-                self._pool_base[name] = (t.data_ptr() if pool == "device"
-                                         else _host_device_pointer(t))
+        kv_base = (self.pool_kv.data_ptr() if pool == "device"
+                   else _host_device_pointer(self.pool_kv))
+        self._pool_base["pool_k"] = kv_base
+        self._pool_base["pool_v"] = kv_base + self.pool_k.nbytes
+        if self.pool_scale is not None:
+            self._pool_base["pool_scale"] = (self.pool_scale.data_ptr() if pool == "device"
+                                             else _host_device_pointer(self.pool_scale))
         nbytes = B.tsr_rope_table_bytes(self.model)
         if nbytes == 0:
             raise B.TsrError(B.TSR_ERR_INVALID_ARG, B.tsr_last_error())
@@ -155,9 +159,11 @@ class Session:
         B.tsr_append_kv(plan, k, v, self.req_k[layer], self.req_v[layer], self._rs(layer),
                         stream or self.stream)
 
-    def attn(self, plan, q, out, lse=None, layer: int = 0, stream=None):
-        B.tsr_attn(plan, q, self.req_k[layer], self.req_v[layer], self._rs(layer), out, lse,
-                   stream or self.stream)
+    def attn(self, plan, q, out, lse=None, layer: int = 0, stream=None, part: int = 0):
+        """Attention over the assembled pages; `part` selects all items
+        (TSR_ATTN_ALL) or the items before / after compose."""
+        B.tsr_attn_part(plan, part, q, self.req_k[layer], self.req_v[layer], self._rs(layer),
+                        out, lse, stream or self.stream)
 
     def retain(self, plan, k, v, layer: int = 0, stream=None):
         B.tsr_retain_kv(plan, k, v, self._pk(layer), self._pv(layer), self._ps(layer),

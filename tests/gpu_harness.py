@@ -320,7 +320,10 @@ class StagedRun:
         t = self.tier
         src = torch.as_tensor(self.prep.stage_src.astype(np.int64))
         dst = torch.as_tensor(self.prep.stage_dst.astype(np.int64), device=self.sess.device)
-        for host, stg in t._arenas():
+        pairs = [(t.host_k, self.sess.pool_k), (t.host_v, self.sess.pool_v)]
+        if self.sess.e4m3:
+            pairs.append((t.host_scale, self.sess.pool_scale))
+        for host, stg in pairs:
             for l in range(t.n_layers):
                 a = stg[l][dst].cpu().view(torch.uint8)
                 b = host[l][src].view(torch.uint8)
