@@ -277,6 +277,35 @@ def host_tier_staged(torch, wl, reps=5, warmup=2):
     return res
 
 
+def control_plane_replay():
+    """Replay of a RAG-shaped retrieval trace through the control plane
+    (libtsr's tsr_replay, host code): 6,000 requests of 10 units of 512
+    tokens drawn Zipf(1.1) from 2,000 units whose popular set shifts every
+    1,500 requests; 4 nodes with 200 units of local cache each; 16 requests
+    in flight.  Block hit rates per policy."""
+    import paper_2609_32999_amd._binding as B
+    from workloads.traces import zipf_trace
+    trace = zipf_trace(7, 6000, 2000, 10, zipf_s=1.1, token_range=(512, 512),
+                       drift_every=1500, drift_shift=250)
+    out = {}
+    for name, kw in (("cache_aware", {}), ("load_only", {"cache_aware": 0}),
+                     ("cache_aware_shared", {"shared_capacity_blocks": 600 * 32}),
+                     ("first_retrieval_admitted", {"theta": 0.0})):
+        base = dict(n_nodes=4, local_capacity_blocks=200 * 32, shared_capacity_blocks=0,
+                    page_size=16, theta=2.0, w_recent=1.0, w_lifetime=0.05, local_window=0,
+                    shared_window=0, concurrency=16, cache_aware=1)
+        base.update(kw)
+        t0 = time.perf_counter()
+        st = B.tsr_replay(B.tsr_replay_config(**base), trace)
+        out[name] = {"local_hit": st["local_hit_blocks"] / st["blocks"],
+                     "shared_hit": st["shared_hit_blocks"] / st["blocks"],
+                     "miss": st["miss_blocks"] / st["blocks"],
+                     "local_admitted": st["local_admitted"],
+                     "node_requests": [st["min_node_requests"], st["max_node_requests"]],
+                     "replay_ms": (time.perf_counter() - t0) * 1e3}
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -467,6 +496,7 @@ def main():
     }
     if host:
         rec["host_tier"] = host
+    rec["control_plane"] = control_plane_replay()
     if measured:
         rec["measured_peaks"] = measured
         rec["roofline"]["frac_of_measured"] = attn_tflops / measured["bf16_gemm_tflops"]

@@ -21,9 +21,11 @@ Modules and what each follows:
                 tokens that are computed (Section 5.3 "Completing prefill").
 * pipeline   -- the whole per-layer path on a workload, and a dense full
                 prefill used as a reference point.
+* control    -- retrieval-aware scoring, admission, eviction and routing,
+                and their trace replay (Section 5.2).
 
 Every function is pinned by tests/test_oracle_*.py against closed forms,
 library routines, brute force on tiny inputs, and the paper's worked
 examples.  Parity status per function is listed in each module docstring.
 """
-from . import attention, compose, layout, numerics, pipeline, rope  # noqa: F401
+from . import attention, compose, control, layout, numerics, pipeline, rope  # noqa: F401

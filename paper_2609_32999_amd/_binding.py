@@ -29,7 +29,7 @@ TSR_MISS, TSR_HIT = 0, 1
 TSR_SCOPE_GLOBAL, TSR_SCOPE_LOCAL = 0, 1
 TSR_ATTN_ALL, TSR_ATTN_BEFORE_COMPOSE, TSR_ATTN_AFTER_COMPOSE = 0, 1, 2
 
-# Every symbol include/tsr.h declares.
+# Every symbol include/*.h declares.
 EXPORTS = (
     "tsr_abi_version", "tsr_last_error", "tsr_rope_table_bytes",
     "tsr_rope_table_init", "tsr_plan_workspace_size", "tsr_plan_create",
@@ -41,6 +41,11 @@ EXPORTS = (
     "tsr_cache_create", "tsr_cache_destroy", "tsr_cache_reserve", "tsr_cache_publish",
     "tsr_cache_cancel", "tsr_cache_reclaim", "tsr_cache_acquire", "tsr_cache_release",
     "tsr_cache_evict", "tsr_cache_query", "tsr_cache_free_blocks", "tsr_copy_blocks",
+    # include/tsr_control.h
+    "tsr_scorer_create", "tsr_scorer_destroy", "tsr_scorer_observe", "tsr_scorer_score",
+    "tsr_scorer_counts", "tsr_window_for_capacity", "tsr_admitter_create",
+    "tsr_admitter_destroy", "tsr_admit", "tsr_admitter_remove", "tsr_admitter_blocks",
+    "tsr_admitter_used_blocks", "tsr_admitter_num_units", "tsr_route", "tsr_replay",
 )
 
 
@@ -71,6 +76,22 @@ class tsr_request(ctypes.Structure):
                 ("units", POINTER(tsr_unit)), ("n_text", c_int32),
                 ("miss_scope", c_int32), ("text_segs", POINTER(c_int32)),
                 ("block_table", POINTER(c_int32))]
+
+
+class tsr_replay_config(ctypes.Structure):
+    _fields_ = [("n_nodes", c_int32), ("local_capacity_blocks", c_int64),
+                ("shared_capacity_blocks", c_int64), ("page_size", c_int32),
+                ("theta", c_double), ("w_recent", c_double), ("w_lifetime", c_double),
+                ("local_window", c_int32), ("shared_window", c_int32),
+                ("concurrency", c_int32), ("cache_aware", c_int32)]
+
+
+class tsr_replay_stats(ctypes.Structure):
+    _fields_ = [(n, c_int64) for n in (
+        "requests", "unit_refs", "blocks", "local_hit_units", "local_hit_blocks",
+        "shared_hit_units", "shared_hit_blocks", "miss_units", "miss_blocks",
+        "local_admitted", "local_evicted", "shared_admitted", "shared_evicted",
+        "max_node_requests", "min_node_requests")]
 
 
 _lib = None
@@ -126,6 +147,26 @@ def lib():
             "tsr_copy_blocks": (c_int32, [P, c_int32, POINTER(c_int32), P, c_int32,
                                           POINTER(c_int32), c_int32, c_int64, c_int32,
                                           c_int64, c_int64, P]),
+            "tsr_scorer_create": (c_int32, [c_int32, c_double, c_double, POINTER(c_void_p)]),
+            "tsr_scorer_destroy": (None, [P]),
+            "tsr_scorer_observe": (c_int32, [P, POINTER(c_uint64), c_int32]),
+            "tsr_scorer_score": (c_double, [P, c_uint64]),
+            "tsr_scorer_counts": (c_int32, [P, c_uint64, POINTER(c_int32), POINTER(c_int64)]),
+            "tsr_window_for_capacity": (c_int32, [c_int64, c_double]),
+            "tsr_admitter_create": (c_int32, [c_int64, c_double, POINTER(c_void_p)]),
+            "tsr_admitter_destroy": (None, [P]),
+            "tsr_admit": (c_int32, [P, P, c_uint64, c_int32, POINTER(c_int32),
+                                    POINTER(c_uint64), c_int32, POINTER(c_int32)]),
+            "tsr_admitter_remove": (c_int32, [P, c_uint64]),
+            "tsr_admitter_blocks": (c_int32, [P, c_uint64]),
+            "tsr_admitter_used_blocks": (c_int64, [P]),
+            "tsr_admitter_num_units": (c_int32, [P]),
+            "tsr_route": (c_int32, [POINTER(c_void_p), POINTER(c_int32), c_int32,
+                                    POINTER(c_uint64), c_int32, POINTER(ctypes.c_uint32),
+                                    POINTER(c_int32)]),
+            "tsr_replay": (c_int32, [POINTER(tsr_replay_config), POINTER(c_int32),
+                                     POINTER(c_uint64), POINTER(c_int32), c_int32,
+                                     POINTER(tsr_replay_stats), POINTER(c_int32)]),
         }
         for name, (res, args) in sig.items():
             f = getattr(L, name)
@@ -405,3 +446,111 @@ def tsr_attn_part(plan: Plan, part: int, q, req_k, req_v, req_scale, out, lse=No
                   stream=None) -> None:
     _check(lib().tsr_attn_part(plan.handle, part, _ptr(q), _ptr(req_k), _ptr(req_v),
                                _ptr(req_scale), _ptr(out), _ptr(lse), _stream(stream)))
+
+
+# ------------------------------------------------------------ control plane
+TSR_ADMIT_BELOW_THRESHOLD, TSR_ADMIT_ADMITTED, TSR_ADMIT_RESIDENT, TSR_ADMIT_NO_ROOM, \
+    TSR_ADMIT_TOO_LARGE = range(5)
+
+
+def _u64(a) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(a, dtype=np.uint64))
+
+
+def _u64p(a: np.ndarray):
+    return a.ctypes.data_as(POINTER(c_uint64))
+
+
+class Scorer:
+    """Reuse score s(u,t) = w_recent f_W + w_lifetime f_inf (tsr_scorer_*)."""
+
+    def __init__(self, window: int, w_recent: float = 1.0, w_lifetime: float = 0.05):
+        out = c_void_p()
+        _check(lib().tsr_scorer_create(window, w_recent, w_lifetime, ctypes.byref(out)))
+        self.handle = out.value
+
+    def __del__(self):
+        if getattr(self, "handle", None):
+            lib().tsr_scorer_destroy(self.handle)
+            self.handle = None
+
+    def observe(self, unit_ids) -> None:
+        u = _u64(unit_ids)
+        _check(lib().tsr_scorer_observe(self.handle, _u64p(u), len(u)))
+
+    def score(self, unit_id: int) -> float:
+        return lib().tsr_scorer_score(self.handle, unit_id)
+
+    def counts(self, unit_id: int) -> tuple[int, int]:
+        r, l = c_int32(), c_int64()
+        _check(lib().tsr_scorer_counts(self.handle, unit_id, ctypes.byref(r), ctypes.byref(l)))
+        return r.value, l.value
+
+
+def tsr_window_for_capacity(capacity_blocks: int, mean_blocks_per_request: float) -> int:
+    return lib().tsr_window_for_capacity(capacity_blocks, mean_blocks_per_request)
+
+
+class Admitter:
+    """A cache's resident set with threshold admission (tsr_admitter_*)."""
+
+    def __init__(self, capacity_blocks: int, theta: float):
+        out = c_void_p()
+        _check(lib().tsr_admitter_create(capacity_blocks, theta, ctypes.byref(out)))
+        self.handle = out.value
+
+    def __del__(self):
+        if getattr(self, "handle", None):
+            lib().tsr_admitter_destroy(self.handle)
+            self.handle = None
+
+    def admit(self, scorer: Scorer, unit_id: int, n_blocks: int, max_victims: int = 4096):
+        res, nv = c_int32(), c_int32()
+        v = np.zeros(max(max_victims, 1), dtype=np.uint64)
+        _check(lib().tsr_admit(self.handle, scorer.handle, unit_id, n_blocks, ctypes.byref(res),
+                               _u64p(v), max_victims, ctypes.byref(nv)))
+        return res.value, [int(x) for x in v[:nv.value]]
+
+    def remove(self, unit_id: int) -> None:
+        _check(lib().tsr_admitter_remove(self.handle, unit_id))
+
+    def blocks(self, unit_id: int) -> int:
+        return lib().tsr_admitter_blocks(self.handle, unit_id)
+
+    @property
+    def used_blocks(self) -> int:
+        return lib().tsr_admitter_used_blocks(self.handle)
+
+    @property
+    def num_units(self) -> int:
+        return lib().tsr_admitter_num_units(self.handle)
+
+
+def tsr_route(node_caches, inflight, unit_ids, rr_cursor: int = 0) -> tuple[int, int]:
+    """Returns (chosen node, next round-robin cursor)."""
+    n = len(inflight)
+    nodes = (c_void_p * n)(*[(c.handle if c is not None else None) for c in node_caches])
+    inf = _i32(inflight)
+    u = _u64(unit_ids)
+    rr = ctypes.c_uint32(rr_cursor)
+    ch = c_int32()
+    _check(lib().tsr_route(nodes, _i32p(inf), n, _u64p(u), len(u), ctypes.byref(rr),
+                           ctypes.byref(ch)))
+    return ch.value, rr.value
+
+
+def tsr_replay(cfg: tsr_replay_config, requests, return_routes: bool = False):
+    """requests: list of (unit_ids, unit_tokens) pairs.  Returns the stats
+    as a dict (and the node of every request)."""
+    offs = np.zeros(len(requests) + 1, dtype=np.int32)
+    offs[1:] = np.cumsum([len(r[0]) for r in requests])
+    ids = _u64(np.concatenate([np.asarray(r[0], np.uint64) for r in requests])
+               if requests else np.zeros(0, np.uint64))
+    toks = _i32(np.concatenate([np.asarray(r[1], np.int32) for r in requests])
+                if requests else np.zeros(0, np.int32))
+    st = tsr_replay_stats()
+    routes = np.zeros(max(len(requests), 1), dtype=np.int32)
+    _check(lib().tsr_replay(ctypes.byref(cfg), _i32p(offs), _u64p(ids), _i32p(toks),
+                            len(requests), ctypes.byref(st), _i32p(routes)))
+    stats = {n: getattr(st, n) for n, _ in tsr_replay_stats._fields_}
+    return (stats, routes[:len(requests)].copy()) if return_routes else stats

@@ -29,8 +29,11 @@ def _plan(wl, reqs=None, **kw):
 
 
 def test_library_exports_every_declared_symbol():
-    with open(os.path.join(ROOT, "include", "tsr.h")) as f:
-        header = f.read()
+    header = ""
+    for name in sorted(os.listdir(os.path.join(ROOT, "include"))):
+        if name.endswith(".h"):
+            with open(os.path.join(ROOT, "include", name)) as f:
+                header += f.read()
     declared = set(re.findall(r"^\s*(?:[\w\*]+\s+)+\**(tsr_\w+)\s*\(", header, re.M))
     assert declared == set(P.EXPORTS), declared ^ set(P.EXPORTS)
     lib = P.lib()
