@@ -277,6 +277,44 @@ def host_tier_staged(torch, wl, reps=5, warmup=2):
     return res
 
 
+def alias_v_leg(torch, sess, wl, qs, ks, vs, out, lse, L, steps, warmup):
+    """The same step with V aliasing (attention reads V of whole gathered
+    pages from the pool; compose writes only their K), timed like the main
+    step: compose, append, attention on one stream, layers rotating."""
+    plan = sess.plan(wl.requests, alias_v=True)
+    main_s = torch.cuda.current_stream()
+    E = lambda: torch.cuda.Event(enable_timing=True)
+    ev = [[E() for _ in range(4)] for _ in range(steps)]
+
+    def step(i, rec=None):
+        l = i % L
+        if rec:
+            rec[0].record(main_s)
+        sess.compose(plan, layer=l, stream=main_s)
+        if rec:
+            rec[1].record(main_s)
+        sess.append(plan, ks[l], vs[l], layer=l, stream=main_s)
+        if rec:
+            rec[2].record(main_s)
+        sess.attn(plan, qs[l], out, lse, layer=l, stream=main_s)
+        if rec:
+            rec[3].record(main_s)
+
+    for i in range(warmup):
+        step(i)
+    torch.cuda.synchronize()
+    for i in range(steps):
+        step(i, ev[i])
+    torch.cuda.synchronize()
+    t = np.array([[e[0].elapsed_time(e[1]), e[2].elapsed_time(e[3]), e[0].elapsed_time(e[3])]
+                  for e in ev])
+    res = {"aliased_pages": plan.num_aliased_pages,
+           "compose_us": float(t[:, 0].mean() * 1e3), "attention_us": float(t[:, 1].mean() * 1e3),
+           "compose_append_attention_us": float(t[:, 2].mean() * 1e3)}
+    log(f"[bench] alias_v: {res}")
+    return res
+
+
 def control_plane_replay():
     """Replay of a RAG-shaped retrieval trace through the control plane
     (libtsr's tsr_replay, host code): 6,000 requests of 10 units of 512
@@ -437,6 +475,9 @@ def main():
     torch.cuda.synchronize()
     compose_all_ms = ev_a.elapsed_time(ev_b) / reps
 
+    alias = alias_v_leg(torch, sess, wl, qs, ks, vs, out, lse, L, args.steps, args.warmup) \
+        if m.kv_dtype == "bf16" else None
+
     w = kv_elem_bytes(m.kv_dtype)
     row_bytes = 2 * m.n_kv_heads * m.head_dim * w           # K + V of one token
     host = host_tier(torch, wl, plan, ks[0], vs[0], row_bytes) if args.host_tier else None
@@ -494,6 +535,8 @@ def main():
         "append_gbps": append_bytes / (append_ms * 1e-3) / 1e9,
         "retain_gbps": retain_bytes / (retain_ms * 1e-3) / 1e9 if retain_ms > 0 else None,
     }
+    if alias:
+        rec["alias_v"] = alias
     if host:
         rec["host_tier"] = host
     rec["control_plane"] = control_plane_replay()

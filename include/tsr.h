@@ -190,6 +190,29 @@ tsr_status tsr_plan_create(const tsr_model* model, const tsr_request* reqs,
                            void* dev_workspace, size_t workspace_bytes,
                            void* stream, tsr_plan** out_plan);
 
+/* Plan options (tsr_plan_create_ex; NULL means all zero).
+ *   alias_v   1: V aliasing, a zero-copy form of composition.  A request
+ *             page that holds B gathered tokens of one HIT unit, slot for
+ *             slot (the unit starts on a page boundary), is not filled with
+ *             V by tsr_compose_kv (its K still is); attention reads that
+ *             page's V from the pool page instead (tsr_attn_aliased).  The
+ *             cached V is used as stored, so results equal the composed
+ *             path's bit for bit.  The pool pages must stay unchanged until
+ *             attention completes.  bf16 pools only (else UNSUPPORTED).
+ *   reserved  must be zero. */
+typedef struct {
+  int32_t alias_v;
+  int32_t reserved[7];
+} tsr_plan_options;
+
+/* tsr_plan_create with options; tsr_plan_create is this with NULL.  The
+ * workspace size does not depend on the options. */
+tsr_status tsr_plan_create_ex(const tsr_model* model, const tsr_request* reqs,
+                              int32_t n_req, int32_t n_pool_pages, int32_t n_req_pages,
+                              const tsr_plan_options* options, const void* dev_rope_table,
+                              void* dev_workspace, size_t workspace_bytes, void* stream,
+                              tsr_plan** out_plan);
+
 /* Number of computed rows T (inputs q/k/v and outputs have T rows). */
 int32_t tsr_plan_num_compute_tokens(const tsr_plan* plan);
 /* Number of cached tokens gathered by tsr_compose_kv. */
@@ -222,6 +245,10 @@ typedef enum {
 /* Items of one part (padding to whole XCD rounds included); -1 for a NULL
  * plan or an unknown part. */
 int32_t tsr_plan_num_attn_items_part(const tsr_plan* plan, int32_t part);
+
+/* Request pages whose V attention reads from the pool (alias_v plans; 0
+ * otherwise). */
+int32_t tsr_plan_num_aliased_pages(const tsr_plan* plan);
 
 /* Prompt position and request index of every computed row, in plan order.
  * host_positions: [T] (required); host_requests: [T] or NULL. */
@@ -303,6 +330,15 @@ tsr_status tsr_attn(const tsr_plan* plan, const void* q, const void* req_k,
 tsr_status tsr_attn_part(const tsr_plan* plan, int32_t part, const void* q,
                          const void* req_k, const void* req_v, const float* req_scale,
                          void* out, float* lse, void* stream);
+
+/* Attention of an alias_v plan (one part, or TSR_ATTN_ALL): as tsr_attn_part,
+ * with the V of aliased request pages read from pool_v (device, the pool
+ * arena tsr_compose_kv read, [n_pool_pages][H_kv][B][d] bf16).  The
+ * non-aliased entry points refuse alias_v plans, and this one refuses the
+ * others (INVALID_ARG). */
+tsr_status tsr_attn_aliased(const tsr_plan* plan, int32_t part, const void* q,
+                            const void* req_k, const void* req_v, const void* pool_v,
+                            void* out, float* lse, void* stream);
 
 /* Retain (Section 5.4): for every MISS unit with retain = 1 and token j:
  *   K_pool[block j/B][slot j%B] = k (before RoPE), V_pool[...] = v

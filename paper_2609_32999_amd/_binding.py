@@ -35,7 +35,8 @@ EXPORTS = (
     "tsr_rope_table_init", "tsr_plan_workspace_size", "tsr_plan_create",
     "tsr_plan_num_compute_tokens", "tsr_plan_num_gather_tokens",
     "tsr_plan_num_retain_tokens", "tsr_plan_num_attn_items",
-    "tsr_plan_num_attn_items_part", "tsr_attn_part",
+    "tsr_plan_num_attn_items_part", "tsr_attn_part", "tsr_plan_create_ex",
+    "tsr_plan_num_aliased_pages", "tsr_attn_aliased",
     "tsr_plan_compute_positions", "tsr_plan_row_kv_lo", "tsr_plan_destroy", "tsr_compose_kv",
     "tsr_prefill_attn", "tsr_append_kv", "tsr_attn", "tsr_retain_kv",
     "tsr_cache_create", "tsr_cache_destroy", "tsr_cache_reserve", "tsr_cache_publish",
@@ -76,6 +77,10 @@ class tsr_request(ctypes.Structure):
                 ("units", POINTER(tsr_unit)), ("n_text", c_int32),
                 ("miss_scope", c_int32), ("text_segs", POINTER(c_int32)),
                 ("block_table", POINTER(c_int32))]
+
+
+class tsr_plan_options(ctypes.Structure):
+    _fields_ = [("alias_v", c_int32), ("reserved", c_int32 * 7)]
 
 
 class tsr_replay_config(ctypes.Structure):
@@ -121,6 +126,11 @@ def lib():
             "tsr_plan_num_retain_tokens": (c_int32, [P]),
             "tsr_plan_num_attn_items": (c_int32, [P]),
             "tsr_plan_num_attn_items_part": (c_int32, [P, c_int32]),
+            "tsr_plan_num_aliased_pages": (c_int32, [P]),
+            "tsr_plan_create_ex": (c_int32, [POINTER(tsr_model), POINTER(tsr_request), c_int32,
+                                             c_int32, c_int32, POINTER(tsr_plan_options), P, P,
+                                             c_size_t, P, POINTER(c_void_p)]),
+            "tsr_attn_aliased": (c_int32, [P, c_int32, P, P, P, P, P, P, P]),
             "tsr_plan_compute_positions": (c_int32, [P, POINTER(c_int32), POINTER(c_int32)]),
             "tsr_plan_row_kv_lo": (c_int32, [P, POINTER(c_int32)]),
             "tsr_plan_destroy": (None, [P]),
@@ -292,6 +302,10 @@ class Plan:
     def num_attn_items_part(self, part: int) -> int:
         return lib().tsr_plan_num_attn_items_part(self.handle, part)
 
+    @property
+    def num_aliased_pages(self) -> int:
+        return lib().tsr_plan_num_aliased_pages(self.handle)
+
     def compute_positions(self):
         T = self.num_compute_tokens
         pos = np.empty(max(T, 1), dtype=np.int32)
@@ -322,12 +336,21 @@ class Plan:
 
 def tsr_plan_create(model: tsr_model, batch: RequestBatch, n_pool_pages: int,
                     n_req_pages: int, dev_rope_table=None, dev_workspace=None,
-                    workspace_bytes: int = 0, stream=None) -> Plan:
+                    workspace_bytes: int = 0, stream=None, alias_v: bool = False) -> Plan:
     out = c_void_p()
-    _check(lib().tsr_plan_create(ctypes.byref(model), batch.array, batch.n, n_pool_pages,
-                                 n_req_pages, _ptr(dev_rope_table), _ptr(dev_workspace),
-                                 workspace_bytes, _stream(stream), ctypes.byref(out)))
-    return Plan(out.value, model)
+    if alias_v:
+        opts = tsr_plan_options(alias_v=1)
+        _check(lib().tsr_plan_create_ex(ctypes.byref(model), batch.array, batch.n,
+                                        n_pool_pages, n_req_pages, ctypes.byref(opts),
+                                        _ptr(dev_rope_table), _ptr(dev_workspace),
+                                        workspace_bytes, _stream(stream), ctypes.byref(out)))
+    else:
+        _check(lib().tsr_plan_create(ctypes.byref(model), batch.array, batch.n, n_pool_pages,
+                                     n_req_pages, _ptr(dev_rope_table), _ptr(dev_workspace),
+                                     workspace_bytes, _stream(stream), ctypes.byref(out)))
+    plan = Plan(out.value, model)
+    plan.alias_v = bool(alias_v)
+    return plan
 
 
 def tsr_compose_kv(plan: Plan, pool_k, pool_v, pool_scale, req_k, req_v, req_scale,
@@ -554,3 +577,9 @@ def tsr_replay(cfg: tsr_replay_config, requests, return_routes: bool = False):
                             len(requests), ctypes.byref(st), _i32p(routes)))
     stats = {n: getattr(st, n) for n, _ in tsr_replay_stats._fields_}
     return (stats, routes[:len(requests)].copy()) if return_routes else stats
+
+
+def tsr_attn_aliased(plan: Plan, part: int, q, req_k, req_v, pool_v, out, lse=None,
+                     stream=None) -> None:
+    _check(lib().tsr_attn_aliased(plan.handle, part, _ptr(q), _ptr(req_k), _ptr(req_v),
+                                  _ptr(pool_v), _ptr(out), _ptr(lse), _stream(stream)))

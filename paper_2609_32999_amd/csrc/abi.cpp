@@ -46,6 +46,36 @@ tsr_status check_scales(const tsr_plan* p, const float* a, const float* b,
   return TSR_OK;
 }
 
+tsr_status attn_common(const tsr_plan* p, int32_t part, const void* q, const void* req_k,
+                       const void* req_v, const void* pool_v, const float* req_scale,
+                       void* out, float* lse, void* stream) {
+  tsr_status st = check_exec(p);
+  if (st != TSR_OK) return st;
+  if (part < TSR_ATTN_ALL || part > TSR_ATTN_AFTER_COMPOSE) {
+    set_error("attn: part must be TSR_ATTN_ALL, _BEFORE_COMPOSE or _AFTER_COMPOSE");
+    return TSR_ERR_INVALID_ARG;
+  }
+  if ((st = check_scales(p, nullptr, req_scale, false, true)) != TSR_OK) return st;
+  if (p->alias_v != (pool_v != nullptr)) {
+    set_error(p->alias_v ? "the plan reads V from the pool: use tsr_attn_aliased with pool_v"
+                         : "tsr_attn_aliased needs a plan created with alias_v");
+    return TSR_ERR_INVALID_ARG;
+  }
+  if (p->T == 0) return TSR_OK;
+  if (!q || !req_k || !req_v || !out) {
+    set_error("attn: a required pointer is NULL");
+    return TSR_ERR_INVALID_ARG;
+  }
+  const AttnItem* items = part == TSR_ATTN_ALL ? p->dev.items : p->dev.items_part[part - 1];
+  const int32_t n = part == TSR_ATTN_ALL ? p->n_items : p->n_items_part[part - 1];
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t e = is_e4m3(p)
+                     ? launch_attn_e4m3(p, items, n, q, req_k, req_v, req_scale, out, lse, s)
+                     : launch_attn(p, items, n, pool_v, q, req_k, req_v, out, lse, s);
+  if (e != hipSuccess) return device_fail("attention launch", e);
+  return TSR_OK;
+}
+
 }  // namespace
 
 void set_error(const std::string& msg) { g_error = msg; }
@@ -103,7 +133,7 @@ size_t tsr_plan_workspace_size(const tsr_model* model, const tsr_request* reqs,
   size_t bytes = 0;
   guarded([&]() -> tsr_status {
     tsr_plan tmp{};
-    tsr_status st = build_plan(model, reqs, n_req, n_pool_pages, n_req_pages, &tmp);
+    tsr_status st = build_plan(model, reqs, n_req, n_pool_pages, n_req_pages, false, &tmp);
     if (st == TSR_OK) bytes = tmp.ws_bytes;
     return st;
   });
@@ -115,14 +145,36 @@ tsr_status tsr_plan_create(const tsr_model* model, const tsr_request* reqs,
                            int32_t n_req_pages, const void* dev_rope_table,
                            void* dev_workspace, size_t workspace_bytes,
                            void* stream, tsr_plan** out_plan) {
+  return tsr_plan_create_ex(model, reqs, n_req, n_pool_pages, n_req_pages, nullptr,
+                            dev_rope_table, dev_workspace, workspace_bytes, stream, out_plan);
+}
+
+tsr_status tsr_plan_create_ex(const tsr_model* model, const tsr_request* reqs,
+                              int32_t n_req, int32_t n_pool_pages, int32_t n_req_pages,
+                              const tsr_plan_options* options, const void* dev_rope_table,
+                              void* dev_workspace, size_t workspace_bytes, void* stream,
+                              tsr_plan** out_plan) {
   return guarded([&]() -> tsr_status {
     if (!out_plan) {
       set_error("out_plan is NULL");
       return TSR_ERR_INVALID_ARG;
     }
     *out_plan = nullptr;
+    bool alias_v = false;
+    if (options) {
+      for (int32_t r : options->reserved)
+        if (r != 0) {
+          set_error("tsr_plan_options.reserved must be zero");
+          return TSR_ERR_INVALID_ARG;
+        }
+      if (options->alias_v != 0 && options->alias_v != 1) {
+        set_error("tsr_plan_options.alias_v must be 0 or 1");
+        return TSR_ERR_INVALID_ARG;
+      }
+      alias_v = options->alias_v == 1;
+    }
     tsr_plan* p = new tsr_plan();
-    tsr_status st = build_plan(model, reqs, n_req, n_pool_pages, n_req_pages, p);
+    tsr_status st = build_plan(model, reqs, n_req, n_pool_pages, n_req_pages, alias_v, p);
     if (st != TSR_OK) {
       delete p;
       return st;
@@ -156,6 +208,7 @@ tsr_status tsr_plan_create(const tsr_model* model, const tsr_request* reqs,
       for (int q = 0; q < 2; ++q)
         p->dev.items_part[q] = reinterpret_cast<const AttnItem*>(base + p->off_items_part[q]);
       p->dev.block_tables = reinterpret_cast<const int32_t*>(base + p->off_bt);
+      p->dev.v_block_tables = reinterpret_cast<const int32_t*>(base + p->off_vbt);
       p->dev.gpages = reinterpret_cast<const PageDesc*>(base + p->off_gpages);
       p->dev.apages = reinterpret_cast<const PageDesc*>(base + p->off_apages);
       p->dev.rpages = reinterpret_cast<const PageDesc*>(base + p->off_rpages);
@@ -173,6 +226,7 @@ int32_t tsr_plan_num_compute_tokens(const tsr_plan* p) { return p ? p->T : -1; }
 int32_t tsr_plan_num_gather_tokens(const tsr_plan* p) { return p ? p->n_gather : -1; }
 int32_t tsr_plan_num_retain_tokens(const tsr_plan* p) { return p ? p->n_retain : -1; }
 int32_t tsr_plan_num_attn_items(const tsr_plan* p) { return p ? p->n_items : -1; }
+int32_t tsr_plan_num_aliased_pages(const tsr_plan* p) { return p ? p->n_aliased : -1; }
 
 int32_t tsr_plan_num_attn_items_part(const tsr_plan* p, int32_t part) {
   if (!p || part < TSR_ATTN_ALL || part > TSR_ATTN_AFTER_COMPOSE) return -1;
@@ -255,13 +309,18 @@ tsr_status tsr_prefill_attn(const tsr_plan* p, const void* q, const void* k,
       set_error("prefill_attn: a required pointer is NULL");
       return TSR_ERR_INVALID_ARG;
     }
+    if (p->alias_v) {
+      set_error("the plan reads V from the pool: use tsr_append_kv and tsr_attn_aliased");
+      return TSR_ERR_INVALID_ARG;
+    }
     hipStream_t s = static_cast<hipStream_t>(stream);
     hipError_t e = is_e4m3(p) ? launch_append_e4m3(p, k, v, req_k, req_v, req_scale, s)
                               : launch_append(p, k, v, req_k, req_v, s);
     if (e != hipSuccess) return device_fail("append launch", e);
     e = is_e4m3(p) ? launch_attn_e4m3(p, p->dev.items, p->n_items, q, req_k, req_v,
                                       req_scale, out, lse, s)
-                   : launch_attn(p, p->dev.items, p->n_items, q, req_k, req_v, out, lse, s);
+                   : launch_attn(p, p->dev.items, p->n_items, nullptr, q, req_k, req_v, out,
+                                 lse, s);
     if (e != hipSuccess) return device_fail("attention launch", e);
     return TSR_OK;
   });
@@ -287,30 +346,24 @@ tsr_status tsr_append_kv(const tsr_plan* p, const void* k, const void* v,
   });
 }
 
+
 tsr_status tsr_attn_part(const tsr_plan* p, int32_t part, const void* q,
                          const void* req_k, const void* req_v, const float* req_scale,
                          void* out, float* lse, void* stream) {
   return guarded([&]() -> tsr_status {
-    tsr_status st = check_exec(p);
-    if (st != TSR_OK) return st;
-    if (part < TSR_ATTN_ALL || part > TSR_ATTN_AFTER_COMPOSE) {
-      set_error("attn: part must be TSR_ATTN_ALL, _BEFORE_COMPOSE or _AFTER_COMPOSE");
+    return attn_common(p, part, q, req_k, req_v, nullptr, req_scale, out, lse, stream);
+  });
+}
+
+tsr_status tsr_attn_aliased(const tsr_plan* p, int32_t part, const void* q,
+                            const void* req_k, const void* req_v, const void* pool_v,
+                            void* out, float* lse, void* stream) {
+  return guarded([&]() -> tsr_status {
+    if (!pool_v) {
+      set_error("tsr_attn_aliased: pool_v is NULL");
       return TSR_ERR_INVALID_ARG;
     }
-    if ((st = check_scales(p, nullptr, req_scale, false, true)) != TSR_OK) return st;
-    if (p->T == 0) return TSR_OK;
-    if (!q || !req_k || !req_v || !out) {
-      set_error("attn: a required pointer is NULL");
-      return TSR_ERR_INVALID_ARG;
-    }
-    const AttnItem* items = part == TSR_ATTN_ALL ? p->dev.items : p->dev.items_part[part - 1];
-    const int32_t n = part == TSR_ATTN_ALL ? p->n_items : p->n_items_part[part - 1];
-    hipStream_t s = static_cast<hipStream_t>(stream);
-    hipError_t e = is_e4m3(p)
-                       ? launch_attn_e4m3(p, items, n, q, req_k, req_v, req_scale, out, lse, s)
-                       : launch_attn(p, items, n, q, req_k, req_v, out, lse, s);
-    if (e != hipSuccess) return device_fail("attention launch", e);
-    return TSR_OK;
+    return attn_common(p, part, q, req_k, req_v, pool_v, nullptr, out, lse, stream);
   });
 }
 

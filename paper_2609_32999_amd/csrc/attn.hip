@@ -162,11 +162,15 @@ __device__ __forceinline__ uint32_t pack_f16x2(float a, float b) {
   return __builtin_bit_cast(uint32_t, h);
 }
 
-template <int G>
+// AV: V aliasing -- the V of a 16-key block comes from the page the V block
+// table names, a pool page when kPoolPageFlag is set (else the request page
+// the K block table names).
+template <int G, bool AV>
 __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc,
-    const uint16_t* __restrict__ vc, const AttnItem* __restrict__ items,
-    const int32_t* __restrict__ bts, const RowDesc* __restrict__ rows,
+    const uint16_t* __restrict__ vc, const uint16_t* __restrict__ pool_v,
+    const AttnItem* __restrict__ items, const int32_t* __restrict__ bts,
+    const int32_t* __restrict__ vbts, const RowDesc* __restrict__ rows,
     const float* __restrict__ rope_cos, const float* __restrict__ rope_sin,
     uint16_t* __restrict__ out, float* __restrict__ lse, int n_q_heads,
     int n_kv_heads, int log2_page, float scale, float scale_log2e) {
@@ -267,11 +271,21 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(
       const int kq = key0 + 16 * q;
       base[q] = ((((int64_t)page[q] * n_kv_heads + g) << log2_page) + (kq & page_mask)) * kD;
     }
-    const int64_t vbase = vq == 0 ? base[0] : vq == 1 ? base[1] : vq == 2 ? base[2] : base[3];
+    int64_t vbase = vq == 0 ? base[0] : vq == 1 ? base[1] : vq == 2 ? base[2] : base[3];
+    const uint16_t* vsrc = vc;
+    if constexpr (AV) {
+      // this thread's V keys lie in block vq of the tile
+      const int kv = key0 + 16 * vq;
+      const int32_t vp =
+          vbts[it.bt_off + min(kv >> log2_page, it.n_pages - 1)];
+      vsrc = (vp & kPoolPageFlag) ? pool_v : vc;
+      vbase = ((((int64_t)(vp & ~kPoolPageFlag) * n_kv_heads + g) << log2_page) +
+               (kv & page_mask)) * kD;
+    }
 #pragma unroll
     for (int pb = 0; pb < 4; ++pb) {
       kr[pb] = *reinterpret_cast<const uint4*>(kc + base[pb] + koff);
-      vr[pb] = *reinterpret_cast<const uint4*>(vc + vbase + voff + pb * kD);
+      vr[pb] = *reinterpret_cast<const uint4*>(vsrc + vbase + voff + pb * kD);
     }
     if (key0 + kKT > it.kv_len) {
       // last, partial tile: keys past kv_len may be unwritten slots
@@ -473,7 +487,7 @@ int ilog2(int x) {
 }  // namespace
 
 hipError_t launch_attn(const tsr_plan* p, const AttnItem* items, int32_t n_items,
-                       const void* q, const void* req_k,
+                       const void* pool_v, const void* q, const void* req_k,
                        const void* req_v, void* out, float* lse, hipStream_t s) {
   if (n_items == 0 || p->T == 0) return hipSuccess;
   const tsr_model& m = p->model;
@@ -498,18 +512,25 @@ hipError_t launch_attn(const tsr_plan* p, const AttnItem* items, int32_t n_items
     return hipGetLastError();
   }
   const float sl2e = (float)((double)p->scale * 1.4426950408889634);
-#define TSR_MFMA(GG)                                                               \
-  hipLaunchKernelGGL(attn_mfma_kernel<GG>, grid, block, 0, s,                      \
+#define TSR_MFMA(GG, AV)                                                           \
+  hipLaunchKernelGGL((attn_mfma_kernel<GG, AV>), grid, block, 0, s,                \
                      static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(req_k), \
-                     static_cast<const uint16_t*>(req_v), items,                     \
-                     p->dev.block_tables, p->dev.rows, p->dev.rope_cos,             \
+                     static_cast<const uint16_t*>(req_v),                          \
+                     static_cast<const uint16_t*>(pool_v), items,                  \
+                     p->dev.block_tables, p->dev.v_block_tables, p->dev.rows,       \
+                     p->dev.rope_cos,                                               \
                      p->dev.rope_sin, static_cast<uint16_t*>(out), lse,             \
                      m.n_q_heads, m.n_kv_heads, lp, p->scale, sl2e)
-  switch (G) {
-    case 1: TSR_MFMA(1); break;
-    case 2: TSR_MFMA(2); break;
-    case 4: TSR_MFMA(4); break;
-    case 8: TSR_MFMA(8); break;
+  const bool av = pool_v != nullptr;
+  switch (G * 2 + (av ? 1 : 0)) {
+    case 2: TSR_MFMA(1, false); break;
+    case 3: TSR_MFMA(1, true); break;
+    case 4: TSR_MFMA(2, false); break;
+    case 5: TSR_MFMA(2, true); break;
+    case 8: TSR_MFMA(4, false); break;
+    case 9: TSR_MFMA(4, true); break;
+    case 16: TSR_MFMA(8, false); break;
+    case 17: TSR_MFMA(8, true); break;
     default: return hipErrorInvalidValue;
   }
 #undef TSR_MFMA

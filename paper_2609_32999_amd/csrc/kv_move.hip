@@ -91,9 +91,11 @@ __global__ __launch_bounds__(kThreads) void kv_move_kernel(
   dst_v += layer * dst_layer_stride;
 
   int32_t src, dst, pos = 0;
+  bool move_v = true;         // false: attention reads this token's V from the pool
   if constexpr (MODE == kCompose) {
     const GatherDesc gd = static_cast<const GatherDesc*>(descs)[i];
     src = gd.src; dst = gd.dst; pos = gd.pos;
+    move_v = gd.k_only == 0;
   } else if constexpr (MODE == kAppend) {
     const RowDesc rd = static_cast<const RowDesc*>(descs)[i];
     src = i; dst = rd.dst; pos = rd.pos;
@@ -132,8 +134,10 @@ __global__ __launch_bounds__(kThreads) void kv_move_kernel(
         const int64_t sb = src_off(h);
         kl[b].load(src_k + sb + lo);
         kh[b].load(src_k + sb + hi);
-        vl[b].load(src_v + sb + lo);
-        vh[b].load(src_v + sb + hi);
+        if (move_v) {
+          vl[b].load(src_v + sb + lo);
+          vh[b].load(src_v + sb + hi);
+        }
       }
     }
 #pragma unroll
@@ -141,8 +145,10 @@ __global__ __launch_bounds__(kThreads) void kv_move_kernel(
       const int h = hb + b * kHeadStep;
       if (h < n_kv_heads) {
         const int64_t db = dst_off(h);
-        vl[b].store(dst_v + db + lo);
-        vh[b].store(dst_v + db + hi);
+        if (move_v) {
+          vl[b].store(dst_v + db + lo);
+          vh[b].store(dst_v + db + hi);
+        }
         if constexpr (MODE == kRetain) {
           kl[b].store(dst_k + db + lo);
           kh[b].store(dst_k + db + hi);

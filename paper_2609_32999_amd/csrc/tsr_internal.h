@@ -19,6 +19,8 @@ namespace tsr {
 constexpr int kTileRows = 32;
 // Keys per attention KV tile.
 constexpr int kKvTile = 64;
+// Set in a V block-table entry whose page is a pool page (V aliasing).
+constexpr int32_t kPoolPageFlag = 1 << 30;
 // Workgroups of the MFMA attention are dealt round-robin over this many XCDs.
 constexpr int kNumXcd = 8;
 
@@ -28,7 +30,7 @@ struct alignas(16) GatherDesc {
   int32_t src;
   int32_t dst;
   int32_t pos;
-  int32_t pad;
+  int32_t k_only;   // 1: V is read from the pool page by attention (aliased)
 };
 
 // A computed row: its request slot and prompt position.
@@ -81,6 +83,7 @@ struct PlanDev {
   const AttnItem* items;
   const AttnItem* items_part[2];
   const int32_t* block_tables;
+  const int32_t* v_block_tables;  // block_tables, with aliased pages flagged
   const PageDesc* gpages;  // e4m3 plans only
   const PageDesc* apages;
   const PageDesc* rpages;
@@ -109,6 +112,9 @@ struct tsr_plan {
   std::vector<char> image;  // host copy of the device image
   size_t off_gather, off_rows, off_retain, off_items, off_bt, ws_bytes;
   size_t off_items_part[2];
+  size_t off_vbt;
+  bool alias_v;               // V of whole gathered pages read from the pool
+  int32_t n_aliased;          // request pages whose V is read from the pool
   size_t off_gpages, off_apages, off_rpages;
   const void* rope_table;   // device
   void* ws;                 // device, NULL for host-only plans
@@ -150,7 +156,7 @@ tsr_status check_model(const tsr_model* m);
 // Build a plan's host part (validation + descriptors + image layout).
 tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
                       int32_t n_req, int32_t n_pool_pages, int32_t n_req_pages,
-                      tsr_plan* plan);
+                      bool alias_v, tsr_plan* plan);
 
 // Kernel launchers (return hipSuccess or the launch error).
 hipError_t launch_compose(const tsr_plan* p, const void* pool_k,
@@ -162,7 +168,7 @@ hipError_t launch_append(const tsr_plan* p, const void* k, const void* v,
 // Attention launchers run `n_items` items from `items` (a plan's full
 // schedule or one of its parts).
 hipError_t launch_attn(const tsr_plan* p, const AttnItem* items, int32_t n_items,
-                       const void* q, const void* req_k,
+                       const void* pool_v, const void* q, const void* req_k,
                        const void* req_v, void* out, float* lse, hipStream_t s);
 hipError_t launch_retain(const tsr_plan* p, const void* k, const void* v,
                          void* pool_k, void* pool_v, hipStream_t s);

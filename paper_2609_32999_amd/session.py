@@ -101,13 +101,16 @@ class Session:
         B.tsr_rope_table_init(self.model, self.rope, nbytes, self.stream)
 
     # ------------------------------------------------------------- plans
-    def plan(self, requests, stream=None):
+    def plan(self, requests, stream=None, alias_v: bool = False):
+        """Validate and upload a batch's plan; `alias_v` selects V aliasing
+        (attention reads V of whole gathered pages from the pool)."""
         batch = B.RequestBatch(requests)
         ws_bytes = B.tsr_plan_workspace_size(self.model, batch, self.n_pool_pages,
                                              self.n_req_pages)
         ws = torch.empty(ws_bytes, dtype=torch.uint8, device=self.device)
         plan = B.tsr_plan_create(self.model, batch, self.n_pool_pages, self.n_req_pages,
-                                 self.rope, ws, ws_bytes, stream or self.stream)
+                                 self.rope, ws, ws_bytes, stream or self.stream,
+                                 alias_v=alias_v)
         plan.workspace = ws     # keep the workspace alive with the plan
         plan.batch = batch
         return plan
@@ -152,6 +155,10 @@ class Session:
         return out, lse
 
     def prefill_attn(self, plan, q, k, v, out, lse=None, layer: int = 0, stream=None):
+        if getattr(plan, "alias_v", False):       # append, then attention with pool V
+            self.append(plan, k, v, layer=layer, stream=stream)
+            self.attn(plan, q, out, lse, layer=layer, stream=stream)
+            return
         B.tsr_prefill_attn(plan, q, k, v, self.req_k[layer], self.req_v[layer],
                            self._rs(layer), out, lse, stream or self.stream)
 
@@ -162,6 +169,10 @@ class Session:
     def attn(self, plan, q, out, lse=None, layer: int = 0, stream=None, part: int = 0):
         """Attention over the assembled pages; `part` selects all items
         (TSR_ATTN_ALL) or the items before / after compose."""
+        if getattr(plan, "alias_v", False):
+            B.tsr_attn_aliased(plan, part, q, self.req_k[layer], self.req_v[layer],
+                               self._pv(layer), out, lse, stream or self.stream)
+            return
         B.tsr_attn_part(plan, part, q, self.req_k[layer], self.req_v[layer], self._rs(layer),
                         out, lse, stream or self.stream)
 

@@ -208,3 +208,56 @@ def test_bad_miss_scope_and_negative_local_window_are_rejected():
     # under the global scope a MISS unit's n_recompute is not used
     glob = NS(**{**vars(req), "units": units, "miss_scope": 0})
     _plan(wl, [glob]).destroy()
+
+
+def _expected_aliased_pages(wl):
+    """Request pages whose B positions are all cached tokens of one HIT unit,
+    held in the same slots of one pool page (counted from the oracle's
+    gather set)."""
+    B = wl.model.page_size
+    n = 0
+    for req in wl.requests:
+        by_page = {}
+        for ui, j, p in L.gather_tokens(req):
+            u = req.units[ui]
+            src = (int(u.pool_pages[j // B]), j % B)
+            by_page.setdefault(p // B, []).append((ui, src, p % B))
+        for pg, toks in by_page.items():
+            units = {t[0] for t in toks}
+            if len(toks) == B and len(units) == 1 and len({t[1][0] for t in toks}) == 1 \
+                    and all(t[1][1] == t[2] for t in toks):
+                n += 1
+    return n
+
+
+@pytest.mark.parametrize("name", ["rag8b", "small_bf16", "small_bf16_g8", "agent8b"])
+def test_alias_v_pages_match_the_gather_set(name):
+    wl = workloads.generate(name)
+    plan = P.tsr_plan_create(_model(wl), P.RequestBatch(wl.requests), wl.n_pool_pages,
+                             wl.n_req_pages, alias_v=True)
+    assert plan.num_aliased_pages == _expected_aliased_pages(wl)
+    plain = _plan(wl)
+    assert plain.num_aliased_pages == 0
+    assert plan.num_gather_tokens == plain.num_gather_tokens
+    if name == "rag8b":
+        assert plan.num_aliased_pages > 0
+
+
+def test_alias_v_is_bf16_only_and_options_are_checked():
+    for name in ("small_f32", "small_fp8"):
+        wl = workloads.generate(name)
+        with pytest.raises(P.TsrError) as e:
+            P.tsr_plan_create(_model(wl), P.RequestBatch(wl.requests), wl.n_pool_pages,
+                              wl.n_req_pages, alias_v=True)
+        assert e.value.status == P.TSR_ERR_UNSUPPORTED
+    import ctypes
+    from paper_2609_32999_amd._binding import tsr_plan_options
+    wl = workloads.generate("small_bf16")
+    opts = tsr_plan_options(alias_v=0)
+    opts.reserved[3] = 1
+    out = ctypes.c_void_p()
+    batch = P.RequestBatch(wl.requests)
+    st = P.lib().tsr_plan_create_ex(ctypes.byref(_model(wl)), batch.array,
+                                    len(wl.requests), wl.n_pool_pages, wl.n_req_pages,
+                                    ctypes.byref(opts), None, None, 0, None, ctypes.byref(out))
+    assert st == P.TSR_ERR_INVALID_ARG

@@ -1,0 +1,85 @@
+"""GPU tests of V aliasing (a zero-copy form of composition): attention reads
+V of whole gathered pages from the pool, compose writes only their K.  The
+result equals the composed path bit for bit and matches the oracle."""
+import numpy as np
+import pytest
+import torch
+
+import workloads
+from gpu_harness import check_request, fill_sentinel, is_sentinel, say
+from oracle import layout as L
+from paper_2609_32999_amd import staging
+from paper_2609_32999_amd.session import Session
+
+pytestmark = pytest.mark.gpu
+
+ALIGNED = dict(instruction_tokens=64, extra={"unit_tokens_multiple": 64}, unit_tokens=(1, 3))
+CASES = [("small_bf16", ALIGNED), ("small_bf16", {**ALIGNED, "miss_scope": "local"}),
+         ("small_bf16_g8", ALIGNED), ("small_bf16", {**ALIGNED, "n_recompute": 0})]
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU visible")
+    import paper_2609_32999_amd as P
+    P.lib()
+
+
+def aliased_pages(wl):
+    """(request, prompt page) of every request page whose B positions are
+    cached tokens of one HIT unit in the same slots of one pool page."""
+    B = wl.model.page_size
+    out = []
+    for r, req in enumerate(wl.requests):
+        by_page = {}
+        for ui, j, p in L.gather_tokens(req):
+            u = req.units[ui]
+            by_page.setdefault(p // B, []).append((ui, int(u.pool_pages[j // B]), j % B == p % B))
+        for pg, toks in by_page.items():
+            if len(toks) == B and len({t[0] for t in toks}) == 1 and \
+                    len({t[1] for t in toks}) == 1 and all(t[2] for t in toks):
+                out.append((r, pg))
+    return out
+
+
+class Run:
+    def __init__(self, wl, alias):
+        m = wl.model
+        self.wl = wl
+        s = self.sess = Session(m, wl.n_pool_pages, wl.n_req_pages)
+        for t in (s.pool_k, s.pool_v, s.req_k, s.req_v):
+            fill_sentinel(t)
+        staging.upload_pool(s, wl)
+        self.plan = p = s.plan(wl.requests, alias_v=alias)
+        q, k, v = staging.fresh_inputs(s, wl, p)
+        self.pos, self.req = p.compute_positions()
+        s.compose(p)
+        self.out, self.lse = s.new_outputs(p, True)
+        s.prefill_attn(p, q, k, v, self.out, self.lse)
+        torch.cuda.synchronize()
+
+    def request_kv(self, r):
+        return staging.request_kv(self.sess, self.wl, r)
+
+    def rows_of(self, r):
+        return np.nonzero(self.req == r)[0]
+
+
+@pytest.mark.parametrize("name,over", CASES)
+def test_alias_v_equals_composed_path(name, over):
+    wl = workloads.make_workload(workloads.get_config(name).with_(**over))
+    pages = aliased_pages(wl)
+    say(f"[gpu] alias_v: workload={wl.name} seed={wl.seed} aliased pages={len(pages)}")
+    ref = Run(wl, False)
+    run = Run(wl, True)
+    assert run.plan.num_aliased_pages == len(pages) > 0
+    assert torch.equal(run.out.view(torch.int16), ref.out.view(torch.int16))
+    assert torch.equal(run.lse.view(torch.int32), ref.lse.view(torch.int32))
+    # K is composed everywhere; V of aliased pages is never written
+    assert torch.equal(run.sess.req_k.view(torch.int16), ref.sess.req_k.view(torch.int16))
+    for r, pg in pages:
+        rp = int(wl.requests[r].block_table[pg])
+        assert bool(is_sentinel(run.sess.req_v[0, rp]).all()), (r, pg)
+    for r in range(len(wl.requests)):
+        check_request(run, r, check_kv=False)
