@@ -359,6 +359,8 @@ def main():
     ap.add_argument("--no-peaks", dest="peaks", action="store_false",
                     help="skip measuring the achievable copy and bf16 GEMM rates")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-alias-v", dest="alias_v", action="store_false",
+                    help="skip timing the step with V aliasing")
     ap.add_argument("--no-host-tier", dest="host_tier", action="store_false",
                     help="skip timing compose and retain against a pool in pinned host memory")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
@@ -476,7 +478,7 @@ def main():
     compose_all_ms = ev_a.elapsed_time(ev_b) / reps
 
     alias = alias_v_leg(torch, sess, wl, qs, ks, vs, out, lse, L, args.steps, args.warmup) \
-        if m.kv_dtype == "bf16" else None
+        if m.kv_dtype == "bf16" and args.alias_v else None
 
     w = kv_elem_bytes(m.kv_dtype)
     row_bytes = 2 * m.n_kv_heads * m.head_dim * w           # K + V of one token
@@ -493,7 +495,8 @@ def main():
     compose_gbs = gather_bytes / (compose_ms * 1e-3) / 1e9
     peak = PEAK_E4M3_BLEND if m.kv_dtype == "e4m3" else PEAK_MFMA_TFLOPS[m.act_dtype]
     G = m.n_q_heads // m.n_kv_heads
-    attn_kernel = f"attn_fp8_kernel<{G}>" if m.kv_dtype == "e4m3" else f"attn_mfma_kernel<{G}>"
+    attn_kernel = (f"attn_fp8_kernel<{G}>" if m.kv_dtype == "e4m3"
+                   else f"attn_mfma_kernel<{G}, false>")
     compose_kernel = ("page_fp8_kernel<0>" if m.kv_dtype == "e4m3" else
                       f"kv_move_kernel<{m.head_dim}, unsigned short, 0>")
     value = wl.prompt_tokens / (ms * 1e-3)
