@@ -125,8 +125,6 @@ typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 
-typedef int i32x4 __attribute__((ext_vector_type(4)));
-typedef i32x4 __attribute__((aligned(4))) i32x4u;
 
 union Frag {
   uint4 u;
@@ -143,18 +141,44 @@ union Frag {
 
 constexpr int kD = 128;
 constexpr int kKT = kKvTile;           // keys per tile
-constexpr int kKStr = kD + 8;          // bf16 elements per K row in LDS
 // V^T rows (fp16) are 16-byte aligned and hold each 16-key step permuted as
 // keys [0..3, 8..11, 4..7, 12..15], so that the eight keys a lane feeds to
 // the PV MFMA (4h .. 4h+3 and 8+4h .. 8+4h+3 for half-wave h, the order in
 // which the S^T accumulators hand out P^T) are one 16-byte LDS read.
 constexpr int kVStr = kKT + 8;         // fp16 elements per V^T row in LDS
-constexpr int kKElems = kKT * kKStr;
-constexpr int kVElems = kD * kVStr;
-constexpr int kStage = kKElems + kVElems;
+// A K tile sits in LDS in the order the QK^T MFMAs consume it: one 1 KB
+// block per (32-key half kb, 16-dim step kst), in which lane l's 16 bytes
+// (at l * 16) are K[32 kb + l % 32][16 kst + 8 (l / 32) .. + 8].  Fragment
+// reads are then lane-contiguous (no bank conflicts, immediate offsets), and
+// one direct global->LDS load of 16 bytes per lane fills one block.
+constexpr int kKBlk = 1024;
+constexpr int kKBytes = 16 * kKBlk;
+constexpr int kVBytes = kD * kVStr * 2;
+// s_waitcnt immediate that waits for every outstanding vector memory
+// access (direct global->LDS loads included) and leaves the other counters.
+constexpr int kWaitVm0 = 0x0F70;
 // Lazy rescale threshold (log2 units): P may grow to 2^kLazy before the
 // running max is moved.
 constexpr float kLazy = 8.0f;
+
+// Direct global->LDS load of 16 bytes per lane: lane l's bytes land at LDS
+// address lds + 16 l (lds wave-uniform).  Written as assembly so that the
+// compiler does not take the LDS write for a possible alias of the LDS reads
+// that follow it (it would wait for the load before each of them); callers
+// wait for these loads themselves (s_waitcnt vmcnt) before the barrier that
+// hands the buffer to the workgroup.  M0 holds no other value in the
+// kernels that use this.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void lds_dma16(const void* src, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
+               :: "v"(src), "s"(lds) : "m0");
+}
+#pragma clang diagnostic pop
+
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const void*)p;
+}
 
 __device__ __forceinline__ uint32_t pack_f16x2(float a, float b) {
   // bf16 values convert to fp16 exactly inside fp16's normal range
@@ -175,7 +199,9 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(
     uint16_t* __restrict__ out, float* __restrict__ lse, int n_q_heads,
     int n_kv_heads, int log2_page, float scale, float scale_log2e) {
   constexpr int HPW = 1;  // query heads per wave
-  __shared__ __attribute__((aligned(16))) uint16_t smem[2 * kStage];
+  // double-buffered K and V^T tiles
+  __shared__ __attribute__((aligned(16))) uint8_t kl[2][kKBytes];
+  __shared__ __attribute__((aligned(16))) uint16_t vl[2][kVBytes / 2];
 
   const AttnItem it = items[blockIdx.x];
   if (it.n_rows == 0) return;
@@ -246,26 +272,35 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(
   //    it writes four consecutive keys (at their permuted place) of each of
   //    its 8 dims to the transposed V tile, and the 16 lanes of a group fill
   //    one 128-byte row segment (no LDS bank conflicts).
-  uint4 kr[4], vr[4];
-  const int kc8 = (tid & 15) * 8;
+  uint4 vr[4];
   const int vkg = tid & 15;
   const int vc8 = (tid >> 4) * 8;
-  const int koff = (tid >> 4) * kD + kc8;
+  // K: wave w loads blocks 4w .. 4w+3 of the tile, i.e. half kw = w / 2 and
+  // steps kst0 .. kst0+3; lane l fetches key 32 kw + l % 32, which lies in
+  // 16-key block 2 kw + (l / 16) % 2 of the tile.
+  const int wu = __builtin_amdgcn_readfirstlane(w);
+  const int kw = wu >> 1, kst0 = 4 * (wu & 1);
+  const int klane = (lane & 15) * kD + 8 * (lane >> 5) + 16 * kst0;
+  const bool khi = (lane >> 4) & 1;
   const int voff = 4 * (vkg & 3) * kD + vc8;
   const int vq = vkg >> 2;
   const int vcol = 16 * vq + ((vkg & 1) << 3) + ((vkg & 2) << 1);
-  auto load_tile = [&](int j) {
+  // Page ids of a tile's four 16-key blocks: lane q (mod 4) loads block q's
+  // id with a vector load one tile before the tile's K/V loads need it, and
+  // readlane moves the four ids to scalar registers.  (A scalar load there
+  // would stall the wave at the top of every tile: scalar loads share their
+  // wait counter with LDS reads.)
+  auto fetch_pages = [&](int j) -> int {
+    return bt[min((j * kKT + 16 * (lane & 3)) >> log2_page, it.n_pages - 1)];
+  };
+  // Issues tile j's loads: K directly into the LDS buffer kt, V into
+  // registers (written to LDS as V^T by store_tile).
+  auto load_tile = [&](int j, int pid, uint8_t* kt) __attribute__((always_inline)) {
     const int key0 = j * kKT;
     int64_t base[4];
     int page[4];
-    const int idx0 = key0 >> log2_page;
-    if (log2_page == 4 && idx0 + 3 < it.n_pages) {   // one 16-byte scalar load
-      const i32x4u p4 = *reinterpret_cast<const i32x4u*>(bt + idx0);
-      page[0] = p4[0]; page[1] = p4[1]; page[2] = p4[2]; page[3] = p4[3];
-    } else {
 #pragma unroll
-      for (int q = 0; q < 4; ++q) page[q] = bt[min((key0 + 16 * q) >> log2_page, it.n_pages - 1)];
-    }
+    for (int q = 0; q < 4; ++q) page[q] = __builtin_amdgcn_readlane(pid, q);
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const int kq = key0 + 16 * q;
@@ -282,27 +317,26 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(
       vbase = ((((int64_t)(vp & ~kPoolPageFlag) * n_kv_heads + g) << log2_page) +
                (kv & page_mask)) * kD;
     }
-#pragma unroll
-    for (int pb = 0; pb < 4; ++pb) {
-      kr[pb] = *reinterpret_cast<const uint4*>(kc + base[pb] + koff);
-      vr[pb] = *reinterpret_cast<const uint4*>(vsrc + vbase + voff + pb * kD);
-    }
-    if (key0 + kKT > it.kv_len) {
-      // last, partial tile: keys past kv_len may be unwritten slots
-#pragma unroll
-      for (int pb = 0; pb < 4; ++pb) {
-        if (key0 + 16 * pb + (tid >> 4) >= it.kv_len) kr[pb] = make_uint4(0, 0, 0, 0);
-        if (key0 + 4 * vkg + pb >= it.kv_len) vr[pb] = make_uint4(0, 0, 0, 0);
-      }
-    }
-  };
-
-  auto store_tile = [&](int buf) {
-    uint16_t* ks = smem + buf * kStage;
-    uint16_t* vs = ks + kKElems;
+    const int64_t klo = kw ? base[2] : base[0], kup = kw ? base[3] : base[1];
 #pragma unroll
     for (int pb = 0; pb < 4; ++pb)
-      *reinterpret_cast<uint4*>(ks + (16 * pb + (tid >> 4)) * kKStr + kc8) = kr[pb];
+      vr[pb] = *reinterpret_cast<const uint4*>(vsrc + vbase + voff + pb * kD);
+    if (key0 + kKT > it.kv_len) {
+      // last, partial tile: keys past kv_len may be unwritten slots.  Their
+      // scores are masked (a select), but 0 * NaN in P V would not be, so
+      // V is zeroed.
+#pragma unroll
+      for (int pb = 0; pb < 4; ++pb)
+        if (key0 + 4 * vkg + pb >= it.kv_len) vr[pb] = make_uint4(0, 0, 0, 0);
+    }
+    // this wave's four blocks 4w .. 4w+3 of the K tile
+    const uint16_t* ksrc = kc + (khi ? kup : klo) + klane;
+    const uint32_t kdst = lds_addr(kt) + (8 * kw + kst0) * kKBlk;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) lds_dma16(ksrc + 16 * i, kdst + i * kKBlk);
+  };
+
+  auto store_tile = [&](uint16_t* vs) __attribute__((always_inline)) {
     const uint32_t* v0 = reinterpret_cast<const uint32_t*>(&vr[0]);
     const uint32_t* v1 = reinterpret_cast<const uint32_t*>(&vr[1]);
     const uint32_t* v2 = reinterpret_cast<const uint32_t*>(&vr[2]);
@@ -322,10 +356,9 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(
   // One 64-key tile: S^T = K Q^T, online softmax, O^T += V^T P^T.
   // MASK: apply the causal mask (only tiles reaching past the smallest row
   // position of the item need it).
-  auto tile = [&](int j, auto mask_tag) {
+  auto tile = [&](int j, auto mask_tag, const uint8_t* ks, const uint16_t* vs)
+      __attribute__((always_inline)) {
     constexpr bool MASK = decltype(mask_tag)::value;
-    const uint16_t* ks = smem + (j & 1) * kStage;
-    const uint16_t* vs = ks + kKElems;
 
     // S^T[key][row] for two 32-key blocks
     TSR_PRIO_MFMA();
@@ -341,7 +374,7 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
         Frag a;
-        a.u = *reinterpret_cast<const uint4*>(ks + (32 * kb + lrow) * kKStr + 16 * kst + 8 * lh);
+        a.u = *reinterpret_cast<const uint4*>(ks + (8 * kb + kst) * kKBlk + lane * 16);
 #pragma unroll
         for (int i = 0; i < HPW; ++i)
           s[i][kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a.b, qf[i][kst], s[i][kb], 0, 0, 0);
@@ -439,17 +472,27 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(
   const int j0 = it.kv_lo / kKT;
   const int jlo = min(ntiles, (it.kv_lo + kKT - 1) / kKT);   // first tile without keys < kv_lo
   const int nfull = min(ntiles, (it.min_pos + 1) / kKT);      // tiles ending at or before min_pos
-  auto run_tiles = [&](int ja, int jb, auto mask_tag) {
+  int pid = fetch_pages(j0);   // ids of the next tile to load
+  // One tile j: issue the next tile's loads into the other buffers, compute
+  // this one, stage the next V^T, wait for this wave's direct K loads, then
+  // the workgroup barrier.
+  auto run_tiles = [&](int ja, int jb, auto mask_tag) __attribute__((always_inline)) {
     for (int j = ja; j < jb; ++j) {
       const bool more = j + 1 < ntiles;
-      if (more) load_tile(j + 1);
-      tile(j, mask_tag);
-      if (more) store_tile((j + 1) & 1);
+      if (more) {
+        load_tile(j + 1, pid, kl[(j + 1) & 1]);
+        pid = fetch_pages(j + 2);
+      }
+      tile(j, mask_tag, kl[j & 1], vl[j & 1]);
+      if (more) store_tile(vl[(j + 1) & 1]);
+      __builtin_amdgcn_s_waitcnt(kWaitVm0);
       __syncthreads();
     }
   };
-  load_tile(j0);
-  store_tile(j0 & 1);
+  load_tile(j0, pid, kl[j0 & 1]);
+  pid = fetch_pages(j0 + 1);
+  store_tile(vl[j0 & 1]);
+  __builtin_amdgcn_s_waitcnt(kWaitVm0);
   __syncthreads();
   run_tiles(j0, jlo, std::true_type{});
   run_tiles(jlo, max(jlo, nfull), std::false_type{});
