@@ -443,6 +443,28 @@ tsr_status tsr_copy_blocks(void* dst, int32_t n_dst_blocks, const int32_t* dst_b
                            int32_t n_layers, int64_t dst_layer_stride,
                            int64_t src_layer_stride, void* stream);
 
+/* ------------------------------------------------- measurement aids */
+/* Not part of the composed-prefill path and not taken from the paper: two
+ * kernels that show the rates the running GPU sustains, which the benchmark
+ * reports next to the published peaks (the matrix cores hold a lower clock
+ * under load than the one the published figures assume).
+ *
+ * tsr_peak_mfma: n_workgroups workgroups of 256 threads each issue
+ *   iters x 8 back-to-back v_mfma_f32_32x32x16_bf16 per wave on register
+ *   operands (eight independent accumulators, no memory traffic in the
+ *   loop); tsr_peak_mfma_flops gives the launch's FLOP count (0 for
+ *   non-positive arguments).  dev_out: device buffer of n_workgroups * 256
+ *   floats (owned by the caller) that receives per-thread sums, so that the
+ *   products are not optimised away.  INVALID_ARG for non-positive sizes or
+ *   a NULL buffer; DEVICE if the launch fails.
+ * tsr_peak_copy: dst[0, bytes) <- src[0, bytes) with 16-byte loads and
+ *   stores by a grid-stride kernel.  Both pointers device memory, 16-byte
+ *   aligned, not overlapping; bytes a positive multiple of 16, else
+ *   INVALID_ARG. */
+int64_t tsr_peak_mfma_flops(int32_t n_workgroups, int32_t iters);
+tsr_status tsr_peak_mfma(int32_t n_workgroups, int32_t iters, float* dev_out, void* stream);
+tsr_status tsr_peak_copy(void* dst, const void* src, size_t bytes, void* stream);
+
 /* Thread-local message of the last failure on this thread ("" if none). */
 const char* tsr_last_error(void);
 

@@ -42,6 +42,7 @@ EXPORTS = (
     "tsr_cache_create", "tsr_cache_destroy", "tsr_cache_reserve", "tsr_cache_publish",
     "tsr_cache_cancel", "tsr_cache_reclaim", "tsr_cache_acquire", "tsr_cache_release",
     "tsr_cache_evict", "tsr_cache_query", "tsr_cache_free_blocks", "tsr_copy_blocks",
+    "tsr_peak_mfma_flops", "tsr_peak_mfma", "tsr_peak_copy",
     # include/tsr_control.h
     "tsr_scorer_create", "tsr_scorer_destroy", "tsr_scorer_observe", "tsr_scorer_score",
     "tsr_scorer_counts", "tsr_window_for_capacity", "tsr_admitter_create",
@@ -157,6 +158,9 @@ def lib():
             "tsr_copy_blocks": (c_int32, [P, c_int32, POINTER(c_int32), P, c_int32,
                                           POINTER(c_int32), c_int32, c_int64, c_int32,
                                           c_int64, c_int64, P]),
+            "tsr_peak_mfma_flops": (c_int64, [c_int32, c_int32]),
+            "tsr_peak_mfma": (c_int32, [c_int32, c_int32, P, P]),
+            "tsr_peak_copy": (c_int32, [P, P, c_size_t, P]),
             "tsr_scorer_create": (c_int32, [c_int32, c_double, c_double, POINTER(c_void_p)]),
             "tsr_scorer_destroy": (None, [P]),
             "tsr_scorer_observe": (c_int32, [P, POINTER(c_uint64), c_int32]),
@@ -463,6 +467,18 @@ def tsr_copy_blocks(dst, n_dst_blocks: int, dst_blocks, src, n_src_blocks: int, 
     _check(lib().tsr_copy_blocks(_ptr(dst), n_dst_blocks, _i32p(d), _ptr(src), n_src_blocks,
                                  _i32p(sb), len(d), block_bytes, n_layers, dst_layer_stride,
                                  src_layer_stride, _stream(stream)))
+
+
+def tsr_peak_mfma_flops(n_workgroups: int, iters: int) -> int:
+    return int(lib().tsr_peak_mfma_flops(n_workgroups, iters))
+
+
+def tsr_peak_mfma(n_workgroups: int, iters: int, dev_out, stream=None) -> None:
+    _check(lib().tsr_peak_mfma(n_workgroups, iters, _ptr(dev_out), _stream(stream)))
+
+
+def tsr_peak_copy(dst, src, nbytes: int, stream=None) -> None:
+    _check(lib().tsr_peak_copy(_ptr(dst), _ptr(src), nbytes, _stream(stream)))
 
 
 def tsr_attn_part(plan: Plan, part: int, q, req_k, req_v, req_scale, out, lse=None,

@@ -261,3 +261,19 @@ def test_alias_v_is_bf16_only_and_options_are_checked():
                                     len(wl.requests), wl.n_pool_pages, wl.n_req_pages,
                                     ctypes.byref(opts), None, None, 0, None, ctypes.byref(out))
     assert st == P.TSR_ERR_INVALID_ARG
+
+
+def test_peak_kernels_validate_before_launch():
+    # measurement aids: sizes and alignment are checked on the host, nothing
+    # is launched for a rejected call
+    assert P.tsr_peak_mfma_flops(2, 3) == 2 * 4 * 3 * 8 * 2 * 32 * 32 * 16
+    assert P.tsr_peak_mfma_flops(0, 3) == 0 and P.tsr_peak_mfma_flops(2, -1) == 0
+    for args in [(0, 10, 1 << 12), (4, 0, 1 << 12), (4, 10, 0)]:
+        with pytest.raises(P.TsrError) as e:
+            P.tsr_peak_mfma(*args)
+        assert e.value.status == P.TSR_ERR_INVALID_ARG
+    for dst, src, n in [(0, 1 << 12, 64), (1 << 12, 0, 64), (1 << 12, 1 << 13, 0),
+                        (1 << 12, 1 << 13, 24), (1 << 12 | 8, 1 << 13, 64)]:
+        with pytest.raises(P.TsrError) as e:
+            P.tsr_peak_copy(dst, src, n)
+        assert e.value.status == P.TSR_ERR_INVALID_ARG
