@@ -13,7 +13,8 @@
 //                     rows of one request x one KV head; the G query heads of
 //                     that KV head are packed into the workgroup (wave w owns
 //                     heads w, w+4, ...), so every K/V tile staged in LDS feeds
-//                     all of them.  Per 64-key tile:
+//                     all of them.  Per 32-key tile (K loaded straight into
+//                     LDS, V staged through registers as V^T in fp16):
 //                       S^T = K Q^T        v_mfma_f32_32x32x16_bf16
 //                       online softmax     fp32, exp2 with folded scale
 //                       O^T += V^T P^T     v_mfma_f32_32x32x16_f16
@@ -21,7 +22,9 @@
 //                     row, so row statistics are lane-local except for one
 //                     exchange between the two half-waves.  P and V enter the
 //                     second product as fp16 (bf16 P would cost ~2e-3
-//                     relative error; fp16 keeps it near 2e-4).
+//                     relative error; fp16 keeps it near 2e-4).  A wave
+//                     holds under 168 registers and a workgroup 36 KB of
+//                     LDS, so three waves share each SIMD.
 #include <cmath>
 #include <type_traits>
 
@@ -133,26 +136,25 @@ union Frag {
   f16x8 h;
 };
 
-// Wave-priority hooks around MFMA blocks (see s_setprio); empty by default.
-#ifndef TSR_PRIO_MFMA
-#define TSR_PRIO_MFMA() ((void)0)
-#define TSR_PRIO_VALU() ((void)0)
-#endif
 
 constexpr int kD = 128;
-constexpr int kKT = kKvTile;           // keys per tile
+// Keys per tile.  32-key tiles keep a wave's registers under 168 (three
+// waves per SIMD) and a workgroup's LDS under 53 KB (three workgroups per
+// CU): the kernel is bound by latency, and the third wave per SIMD hides
+// more of it than the per-tile overhead costs.
+constexpr int kKT = 32;
 // V^T rows (fp16) are 16-byte aligned and hold each 16-key step permuted as
 // keys [0..3, 8..11, 4..7, 12..15], so that the eight keys a lane feeds to
 // the PV MFMA (4h .. 4h+3 and 8+4h .. 8+4h+3 for half-wave h, the order in
 // which the S^T accumulators hand out P^T) are one 16-byte LDS read.
 constexpr int kVStr = kKT + 8;         // fp16 elements per V^T row in LDS
 // A K tile sits in LDS in the order the QK^T MFMAs consume it: one 1 KB
-// block per (32-key half kb, 16-dim step kst), in which lane l's 16 bytes
-// (at l * 16) are K[32 kb + l % 32][16 kst + 8 (l / 32) .. + 8].  Fragment
-// reads are then lane-contiguous (no bank conflicts, immediate offsets), and
-// one direct global->LDS load of 16 bytes per lane fills one block.
+// block per 16-dim step kst, in which lane l's 16 bytes (at l * 16) are
+// K[l % 32][16 kst + 8 (l / 32) .. + 8].  Fragment reads are then
+// lane-contiguous (no bank conflicts, immediate offsets), and one direct
+// global->LDS load of 16 bytes per lane fills one block.
 constexpr int kKBlk = 1024;
-constexpr int kKBytes = 16 * kKBlk;
+constexpr int kKBytes = 8 * kKBlk;
 constexpr int kVBytes = kD * kVStr * 2;
 // s_waitcnt immediate that waits for every outstanding vector memory
 // access (direct global->LDS loads included) and leaves the other counters.
@@ -190,7 +192,7 @@ __device__ __forceinline__ uint32_t pack_f16x2(float a, float b) {
 // table names, a pool page when kPoolPageFlag is set (else the request page
 // the K block table names).
 template <int G, bool AV>
-__global__ __launch_bounds__(256, 2) void attn_mfma_kernel(
+__global__ __launch_bounds__(256, 3) void attn_mfma_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc,
     const uint16_t* __restrict__ vc, const uint16_t* __restrict__ pool_v,
     const AttnItem* __restrict__ items, const int32_t* __restrict__ bts,
@@ -198,7 +200,6 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(
     const float* __restrict__ rope_cos, const float* __restrict__ rope_sin,
     uint16_t* __restrict__ out, float* __restrict__ lse, int n_q_heads,
     int n_kv_heads, int log2_page, float scale, float scale_log2e) {
-  constexpr int HPW = 1;  // query heads per wave
   // double-buffered K and V^T tiles
   __shared__ __attribute__((aligned(16))) uint8_t kl[2][kKBytes];
   __shared__ __attribute__((aligned(16))) uint16_t vl[2][kVBytes / 2];
@@ -206,7 +207,7 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(
   const AttnItem it = items[blockIdx.x];
   if (it.n_rows == 0) return;
   const int tid = threadIdx.x;
-  const int w = tid >> 6;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lane = tid & 63;
   const int lrow = lane & 31;
   const int lh = lane >> 5;
@@ -216,14 +217,14 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(
 
   const int row = it.row0 + min(lrow, it.n_rows - 1);
   const int pos = rows[row].pos;
+  // wave w owns query head head0 + w of the group; with G < 4 the spare
+  // waves recompute head G-1 and store nothing
+  const int hl = G >= 4 ? it.head0 + w : min(w, G - 1);
+  const bool wave_active = G >= 4 || w < G;
 
   // ---- rotated queries as bf16 B operands: lane = query row, k = head dim
-  bf16x8 qf[HPW][8];
-#pragma unroll
-  for (int i = 0; i < HPW; ++i) {
-    // wave w owns query head head0 + w of the group; with G < 4 the spare
-    // waves recompute head G-1 and store nothing
-    const int hl = G >= 4 ? it.head0 + w + 4 * i : min(w + 4 * i, G - 1);
+  bf16x8 qf[8];
+  {
     const uint16_t* qp = q + ((int64_t)row * n_q_heads + g * G + hl) * kD;
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
@@ -240,230 +241,162 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(
         a.w[e] = f32_to_bf16(lo[2 * e]) | (f32_to_bf16(lo[2 * e + 1]) << 16);
         b.w[e] = f32_to_bf16(hi[2 * e]) | (f32_to_bf16(hi[2 * e + 1]) << 16);
       }
-      qf[i][ks] = a.b;
-      qf[i][ks + 4] = b.b;
+      qf[ks] = a.b;
+      qf[ks + 4] = b.b;
     }
   }
 
-  f32x16 o[HPW][4];
-  float m[HPW], l[HPW];
+  f32x16 o[4];
 #pragma unroll
-  for (int i = 0; i < HPW; ++i) {
-    m[i] = -INFINITY;
-    l[i] = 0.0f;
+  for (int db = 0; db < 4; ++db)
 #pragma unroll
-    for (int db = 0; db < 4; ++db)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) o[i][db][r] = 0.0f;
-  }
-  // With G < 4 some waves own no head: they compute a duplicate of head
-  // G-1 (branch-free MFMA code) and store nothing.
-  bool wave_active[HPW];
-#pragma unroll
-  for (int i = 0; i < HPW; ++i) wave_active[i] = G >= 4 || (w + 4 * i) < G;
+    for (int r = 0; r < 16; ++r) o[db][r] = 0.0f;
+  float m = -INFINITY, l = 0.0f;
 
-  // ---- global -> register staging of one K/V tile
-  // The tile's 64 keys form four 16-key blocks; with B >= 16 each block lies
-  // in one page, so its base address is uniform (scalar block-table loads)
-  // and every lane adds a fixed offset.
-  // K: thread owns 16 bytes (dims 8*(tid%16) ..) of key 16*pb + tid/16 of
-  //    block pb; the K tile is stored row-major.
-  // V: thread owns 16 bytes (dims 8*(tid/16) ..) of keys 4*(tid%16) + pb, so
-  //    it writes four consecutive keys (at their permuted place) of each of
-  //    its 8 dims to the transposed V tile, and the 16 lanes of a group fill
-  //    one 128-byte row segment (no LDS bank conflicts).
-  uint4 vr[4];
-  const int vkg = tid & 15;
-  const int vc8 = (tid >> 4) * 8;
-  // K: wave w loads blocks 4w .. 4w+3 of the tile, i.e. half kw = w / 2 and
-  // steps kst0 .. kst0+3; lane l fetches key 32 kw + l % 32, which lies in
-  // 16-key block 2 kw + (l / 16) % 2 of the tile.
-  const int wu = __builtin_amdgcn_readfirstlane(w);
-  const int kw = wu >> 1, kst0 = 4 * (wu & 1);
-  const int klane = (lane & 15) * kD + 8 * (lane >> 5) + 16 * kst0;
+  // ---- staging.  A tile's 32 keys form two 16-key blocks; with B >= 16
+  // each block lies in one page.
+  // K: wave w loads fragment blocks kst = 2w, 2w + 1 with direct loads; lane
+  //    l fetches key l % 32, in 16-key block (l / 16) % 2.
+  // V: thread t owns 16 bytes (dims 8 (t / 16) ..) of keys 2 (t % 16) and
+  //    2 (t % 16) + 1, which sit next to each other in the permuted V^T row;
+  //    each of its 8 dims takes one 4-byte write.
+  const int klane = (lane & 15) * kD + 8 * lh + 32 * w;
   const bool khi = (lane >> 4) & 1;
-  const int voff = 4 * (vkg & 3) * kD + vc8;
-  const int vq = vkg >> 2;
-  const int vcol = 16 * vq + ((vkg & 1) << 3) + ((vkg & 2) << 1);
-  // Page ids of a tile's four 16-key blocks: lane q (mod 4) loads block q's
-  // id with a vector load one tile before the tile's K/V loads need it, and
-  // readlane moves the four ids to scalar registers.  (A scalar load there
-  // would stall the wave at the top of every tile: scalar loads share their
-  // wait counter with LDS reads.)
+  uint4 vr[2];
+  const int kp = tid & 15;                 // key pair
+  const int vb = kp >> 3;                  // 16-key block of the pair
+  const int vc8 = (tid >> 4) * 8;          // first dim
+  const int voff = (2 * kp - 16 * vb) * kD + vc8;
+  const int vk = 2 * kp - 16 * vb;         // key within its block
+  const int vcol = 16 * vb + ((vk >> 2) & 1) * 8 + ((vk >> 3) & 1) * 4 + (vk & 3);
+  // Page ids of a tile's two 16-key blocks: lane q (mod 2) loads block q's
+  // id with a vector load one tile before the tile's loads need it, and
+  // readlane moves the ids to scalar registers.
   auto fetch_pages = [&](int j) -> int {
-    return bt[min((j * kKT + 16 * (lane & 3)) >> log2_page, it.n_pages - 1)];
+    return bt[min((j * kKT + 16 * (lane & 1)) >> log2_page, it.n_pages - 1)];
+  };
+  auto block_base = [&](int page, int kq) -> int64_t {
+    return ((((int64_t)page * n_kv_heads + g) << log2_page) + (kq & page_mask)) * kD;
   };
   // Issues tile j's loads: K directly into the LDS buffer kt, V into
   // registers (written to LDS as V^T by store_tile).
   auto load_tile = [&](int j, int pid, uint8_t* kt) __attribute__((always_inline)) {
     const int key0 = j * kKT;
-    int64_t base[4];
-    int page[4];
-#pragma unroll
-    for (int q = 0; q < 4; ++q) page[q] = __builtin_amdgcn_readlane(pid, q);
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int kq = key0 + 16 * q;
-      base[q] = ((((int64_t)page[q] * n_kv_heads + g) << log2_page) + (kq & page_mask)) * kD;
-    }
-    int64_t vbase = vq == 0 ? base[0] : vq == 1 ? base[1] : vq == 2 ? base[2] : base[3];
+    const int p0 = __builtin_amdgcn_readlane(pid, 0), p1 = __builtin_amdgcn_readlane(pid, 1);
+    const int64_t b0 = block_base(p0, key0), b1 = block_base(p1, key0 + 16);
+    int64_t vbase = vb ? b1 : b0;
     const uint16_t* vsrc = vc;
     if constexpr (AV) {
-      // this thread's V keys lie in block vq of the tile
-      const int kv = key0 + 16 * vq;
-      const int32_t vp =
-          vbts[it.bt_off + min(kv >> log2_page, it.n_pages - 1)];
+      const int kv = key0 + 16 * vb;
+      const int32_t vp = vbts[it.bt_off + min(kv >> log2_page, it.n_pages - 1)];
       vsrc = (vp & kPoolPageFlag) ? pool_v : vc;
-      vbase = ((((int64_t)(vp & ~kPoolPageFlag) * n_kv_heads + g) << log2_page) +
-               (kv & page_mask)) * kD;
+      vbase = block_base(vp & ~kPoolPageFlag, kv);
     }
-    const int64_t klo = kw ? base[2] : base[0], kup = kw ? base[3] : base[1];
 #pragma unroll
-    for (int pb = 0; pb < 4; ++pb)
-      vr[pb] = *reinterpret_cast<const uint4*>(vsrc + vbase + voff + pb * kD);
+    for (int i = 0; i < 2; ++i)
+      vr[i] = *reinterpret_cast<const uint4*>(vsrc + vbase + voff + i * kD);
     if (key0 + kKT > it.kv_len) {
       // last, partial tile: keys past kv_len may be unwritten slots.  Their
       // scores are masked (a select), but 0 * NaN in P V would not be, so
       // V is zeroed.
 #pragma unroll
-      for (int pb = 0; pb < 4; ++pb)
-        if (key0 + 4 * vkg + pb >= it.kv_len) vr[pb] = make_uint4(0, 0, 0, 0);
+      for (int i = 0; i < 2; ++i)
+        if (key0 + 2 * kp + i >= it.kv_len) vr[i] = make_uint4(0, 0, 0, 0);
     }
-    // this wave's four blocks 4w .. 4w+3 of the K tile
-    const uint16_t* ksrc = kc + (khi ? kup : klo) + klane;
-    const uint32_t kdst = lds_addr(kt) + (8 * kw + kst0) * kKBlk;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) lds_dma16(ksrc + 16 * i, kdst + i * kKBlk);
+    const uint16_t* ksrc = kc + (khi ? b1 : b0) + klane;
+    const uint32_t kdst = lds_addr(kt) + 2 * w * kKBlk;
+    lds_dma16(ksrc, kdst);
+    lds_dma16(ksrc + 16, kdst + kKBlk);
   };
-
   auto store_tile = [&](uint16_t* vs) __attribute__((always_inline)) {
     const uint32_t* v0 = reinterpret_cast<const uint32_t*>(&vr[0]);
     const uint32_t* v1 = reinterpret_cast<const uint32_t*>(&vr[1]);
-    const uint32_t* v2 = reinterpret_cast<const uint32_t*>(&vr[2]);
-    const uint32_t* v3 = reinterpret_cast<const uint32_t*>(&vr[3]);
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       const int sh = (e & 1) ? 16 : 0;
       const float f0 = bf16_to_f32((v0[e >> 1] >> sh) & 0xffffu);
       const float f1 = bf16_to_f32((v1[e >> 1] >> sh) & 0xffffu);
-      const float f2 = bf16_to_f32((v2[e >> 1] >> sh) & 0xffffu);
-      const float f3 = bf16_to_f32((v3[e >> 1] >> sh) & 0xffffu);
-      *reinterpret_cast<uint2*>(vs + (vc8 + e) * kVStr + vcol) =
-          make_uint2(pack_f16x2(f0, f1), pack_f16x2(f2, f3));
+      *reinterpret_cast<uint32_t*>(vs + (vc8 + e) * kVStr + vcol) = pack_f16x2(f0, f1);
     }
   };
 
-  // One 64-key tile: S^T = K Q^T, online softmax, O^T += V^T P^T.
+  // One 32-key tile: S^T = K Q^T, online softmax, O^T += V^T P^T.
   // MASK: apply the causal mask (only tiles reaching past the smallest row
-  // position of the item need it).
+  // position of the item, or starting below kv_lo, need it).
   auto tile = [&](int j, auto mask_tag, const uint8_t* ks, const uint16_t* vs)
       __attribute__((always_inline)) {
     constexpr bool MASK = decltype(mask_tag)::value;
-
-    // S^T[key][row] for two 32-key blocks
-    TSR_PRIO_MFMA();
-    f32x16 s[HPW][2];
+    f32x16 s;
 #pragma unroll
-    for (int i = 0; i < HPW; ++i)
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) s[i][kb][r] = 0.0f;
+    for (int r = 0; r < 16; ++r) s[r] = 0.0f;
 #pragma unroll
     for (int kst = 0; kst < 8; ++kst) {
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-        Frag a;
-        a.u = *reinterpret_cast<const uint4*>(ks + (8 * kb + kst) * kKBlk + lane * 16);
-#pragma unroll
-        for (int i = 0; i < HPW; ++i)
-          s[i][kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a.b, qf[i][kst], s[i][kb], 0, 0, 0);
-      }
+      Frag a;
+      a.u = *reinterpret_cast<const uint4*>(ks + kst * kKBlk + lane * 16);
+      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a.b, qf[kst], s, 0, 0, 0);
     }
     // keep four LDS fragment reads in flight ahead of the MFMAs
     // (scheduling groups: 0x100 = LDS read, 0x008 = MFMA)
     __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
 #pragma unroll
-    for (int t = 0; t < 12; ++t) {
+    for (int t = 0; t < 4; ++t) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
       __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
     }
     __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
 
-    TSR_PRIO_VALU();
     if constexpr (MASK) {
       const int kbase = j * kKT;
 #pragma unroll
-      for (int i = 0; i < HPW; ++i)
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int key = kbase + 32 * kb + 8 * (r >> 2) + 4 * lh + (r & 3);
-            s[i][kb][r] = (key > pos || key < it.kv_lo) ? -INFINITY : s[i][kb][r];
-          }
+      for (int r = 0; r < 16; ++r) {
+        const int key = kbase + 8 * (r >> 2) + 4 * lh + (r & 3);
+        s[r] = (key > pos || key < it.kv_lo) ? -INFINITY : s[r];
+      }
     }
-
     // Online softmax with a lazily updated running max: the max (and with
-    // it O and l) is only rescaled when a row's block max exceeds it by more
+    // it O and l) is only rescaled when a row's tile max exceeds it by more
     // than 2^kLazy in probability units, so P stays <= 2^kLazy (exact range
-    // for fp16) and the rescale is skipped almost always.  The tile is
-    // processed as two 32-key halves (softmax, then its PV MFMAs) so that the
-    // second half's VALU work can issue while the first half's MFMAs run.
+    // for fp16) and the rescale is skipped almost always.  Each half-wave
+    // holds half of every row's keys: the halves exchange their maxima only
+    // on the rescale path.
+    float mt = -INFINITY;
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      f16x8 pf[HPW][2];
+    for (int r = 0; r < 16; ++r) mt = fmaxf(mt, s[r]);
+    const bool grow = mt * scale_log2e > m * scale_log2e + kLazy;
+    if (__builtin_amdgcn_ballot_w64(grow)) {
+      const float mn = fmaxf(m, fmaxf(mt, __shfl_xor(mt, 32)));
+      const float alpha = __builtin_amdgcn_exp2f((m - mn) * scale_log2e);
+      m = mn;
+      l *= alpha;
 #pragma unroll
-      for (int i = 0; i < HPW; ++i) {
-        // each half-wave holds half of every row's keys: the halves
-        // exchange their maxima only on the rare rescale path
-        float mt = -INFINITY;
+      for (int db = 0; db < 4; ++db)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) mt = fmaxf(mt, s[i][kb][r]);
-        const bool grow = mt * scale_log2e > m[i] * scale_log2e + kLazy;
-        if (__builtin_amdgcn_ballot_w64(grow)) {
-          const float mn = fmaxf(m[i], fmaxf(mt, __shfl_xor(mt, 32)));
-          const float alpha = __builtin_amdgcn_exp2f((m[i] - mn) * scale_log2e);
-          m[i] = mn;
-          l[i] *= alpha;
-#pragma unroll
-          for (int db = 0; db < 4; ++db)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) o[i][db][r] *= alpha;
-        }
-        // a half with no visible key yet leaves m at -inf (all its scores
-        // are -inf too): exponentiate against 0 so that P = 0, not NaN
-        const float mc = m[i] == -INFINITY ? 0.0f : m[i] * scale_log2e;
-#pragma unroll
-        for (int r = 0; r < 16; ++r)
-          s[i][kb][r] = __builtin_amdgcn_exp2f(fmaf(s[i][kb][r], scale_log2e, -mc));
-        // row sum in fp32 from the unrounded P, as four independent chains
-        // of plain adds (v_dot2_f32_f16 stalls behind the matrix core)
-        float ls[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-        for (int r = 0; r < 16; ++r) ls[r & 3] += s[i][kb][r];
-#pragma unroll
-        for (int h = 0; h < 2; ++h)
-#pragma unroll
-          for (int e = 0; e < 8; ++e) pf[i][h][e] = (_Float16)s[i][kb][8 * h + e];
-        l[i] += (ls[0] + ls[1]) + (ls[2] + ls[3]);
-      }
-      // O^T[d][row] += V^T[d][keys] P^T[keys][row] for this half's 32 keys
-      TSR_PRIO_MFMA();
-#pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const int k2 = 2 * kb + h;
-#pragma unroll
-        for (int db = 0; db < 4; ++db) {
-          Frag a;
-          a.u = *reinterpret_cast<const uint4*>(vs + (32 * db + lrow) * kVStr + 16 * k2 + 8 * lh);
-#pragma unroll
-          for (int i = 0; i < HPW; ++i)
-            o[i][db] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a.h, pf[i][h], o[i][db], 0, 0, 0);
-        }
-      }
-      TSR_PRIO_VALU();
+        for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
     }
+    // a half with no visible key yet leaves m at -inf (all its scores are
+    // -inf too): exponentiate against 0 so that P = 0, not NaN
+    const float mc = m == -INFINITY ? 0.0f : m * scale_log2e;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) s[r] = __builtin_amdgcn_exp2f(fmaf(s[r], scale_log2e, -mc));
+    // row sum in fp32 from the unrounded P, as four independent chains
+    float ls[4] = {s[0], s[1], s[2], s[3]};
+#pragma unroll
+    for (int r = 4; r < 16; ++r) ls[r & 3] += s[r];
+    l += (ls[0] + ls[1]) + (ls[2] + ls[3]);
+    f16x8 pf[2];
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) pf[h][e] = (_Float16)s[8 * h + e];
+    // O^T[d][row] += V^T[d][keys] P^T[keys][row]
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int db = 0; db < 4; ++db) {
+        Frag a;
+        a.u = *reinterpret_cast<const uint4*>(vs + (32 * db + lrow) * kVStr + 16 * h + 8 * lh);
+        o[db] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a.h, pf[h], o[db], 0, 0, 0);
+      }
   };
 
   // keys kv_lo .. kv_len-1: tiles j0 .. ntiles-1.  A tile needs the mask
@@ -499,26 +432,22 @@ __global__ __launch_bounds__(256, 2) void attn_mfma_kernel(
   run_tiles(max(jlo, nfull), ntiles, std::true_type{});
 
   // ---- epilogue: normalise, round to bf16, store rows of this tile
+  const float lt = l + __shfl_xor(l, 32);
+  if (!wave_active || lrow >= it.n_rows) return;
+  const float inv = 1.0f / lt;
+  const int hq = g * G + (G >= 4 ? it.head0 : 0) + w;
+  uint16_t* op = out + ((int64_t)row * n_q_heads + hq) * kD;
 #pragma unroll
-  for (int i = 0; i < HPW; ++i) {
-    if (!wave_active[i]) continue;
-    const float lt = l[i] + __shfl_xor(l[i], 32);
-    if (lrow >= it.n_rows) continue;
-    const float inv = 1.0f / lt;
-    const int hq = g * G + (G >= 4 ? it.head0 : 0) + w + 4 * i;
-    uint16_t* op = out + ((int64_t)row * n_q_heads + hq) * kD;
+  for (int db = 0; db < 4; ++db)
 #pragma unroll
-    for (int db = 0; db < 4; ++db)
-#pragma unroll
-      for (int rg = 0; rg < 4; ++rg) {
-        const int d0 = 32 * db + 8 * rg + 4 * lh;
-        uint2 v;
-        v.x = f32_to_bf16(o[i][db][4 * rg] * inv) | (f32_to_bf16(o[i][db][4 * rg + 1] * inv) << 16);
-        v.y = f32_to_bf16(o[i][db][4 * rg + 2] * inv) | (f32_to_bf16(o[i][db][4 * rg + 3] * inv) << 16);
-        *reinterpret_cast<uint2*>(op + d0) = v;
-      }
-    if (lse && lh == 0) lse[(int64_t)row * n_q_heads + hq] = m[i] * scale + logf(lt);
-  }
+    for (int rg = 0; rg < 4; ++rg) {
+      const int d0 = 32 * db + 8 * rg + 4 * lh;
+      uint2 v;
+      v.x = f32_to_bf16(o[db][4 * rg] * inv) | (f32_to_bf16(o[db][4 * rg + 1] * inv) << 16);
+      v.y = f32_to_bf16(o[db][4 * rg + 2] * inv) | (f32_to_bf16(o[db][4 * rg + 3] * inv) << 16);
+      *reinterpret_cast<uint2*>(op + d0) = v;
+    }
+  if (lse && lh == 0) lse[(int64_t)row * n_q_heads + hq] = m * scale + logf(lt);
 }
 
 int ilog2(int x) {
