@@ -376,8 +376,9 @@ def main():
     ap.add_argument("--no-host-tier", dest="host_tier", action="store_false",
                     help="skip timing compose and retain against a pool in pinned host memory")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
-                    help="run one plain device copy of this size first (to scale "
-                         "HBM byte counters against a kernel of known traffic)")
+                    help="run one launch of libtsr's plain copy kernel of this size "
+                         "first (to scale HBM byte counters against a kernel of known "
+                         "traffic)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the path "
@@ -392,11 +393,14 @@ def main():
     measured = measured_peaks(torch) if args.peaks else None
 
     if args.calib_copy_mib:
+        # one launch of libtsr's plain 16-byte copy kernel of known size, for
+        # scaling HBM byte counters (FETCH_SIZE, WRITE_SIZE) per byte moved
+        from paper_2609_32999_amd import tsr_peak_copy
         n = args.calib_copy_mib << 20
         a = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)
         b = torch.empty_like(a)
         torch.cuda.synchronize()
-        b.copy_(a)
+        tsr_peak_copy(b, a, n)
         torch.cuda.synchronize()
         log(f"[bench] calibration copy of {args.calib_copy_mib} MiB done")
         del a, b
