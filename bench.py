@@ -541,7 +541,9 @@ def main():
                       "attention": attn_ms * 1e3, "retain_side_stream": retain_ms * 1e3},
         "roofline": {"bound": "mfma", "achieved": attn_tflops, "peak": peak,
                      "unit": "TFLOP/s", "frac": attn_tflops / peak,
-                     "traffic": profiled_traffic(args.workload, attn_kernel),
+                     # the committed profiles are of the GLOBAL scope
+                     "traffic": (profiled_traffic(args.workload, attn_kernel)
+                                 if args.scope == "global" else None),
                      "kernel": attn_kernel, "flops_per_launch": attn_flops},
         "roofline_compose": {"bound": "hbm", "achieved": compose_gbs, "peak": PEAK_HBM_GBS,
                              "unit": "GB/s", "frac": compose_gbs / PEAK_HBM_GBS,
