@@ -222,30 +222,7 @@ __global__ __launch_bounds__(256, 3) void attn_mfma_kernel(
   const int hl = G >= 4 ? it.head0 + w : min(w, G - 1);
   const bool wave_active = G >= 4 || w < G;
 
-  // ---- rotated queries as bf16 B operands: lane = query row, k = head dim
   bf16x8 qf[8];
-  {
-    const uint16_t* qp = q + ((int64_t)row * n_q_heads + g * G + hl) * kD;
-#pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
-      const int d0 = 16 * ks + 8 * lh;
-      float lo[8], hi[8], c[8], s[8];
-      load8(qp + d0, lo);
-      load8(qp + d0 + kD / 2, hi);
-      load8(rope_cos + (int64_t)pos * (kD / 2) + d0, c);
-      load8(rope_sin + (int64_t)pos * (kD / 2) + d0, s);
-      rope_rotate<8>(lo, hi, c, s);
-      Frag a, b;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        a.w[e] = f32_to_bf16(lo[2 * e]) | (f32_to_bf16(lo[2 * e + 1]) << 16);
-        b.w[e] = f32_to_bf16(hi[2 * e]) | (f32_to_bf16(hi[2 * e + 1]) << 16);
-      }
-      qf[ks] = a.b;
-      qf[ks + 4] = b.b;
-    }
-  }
-
   f32x16 o[4];
 #pragma unroll
   for (int db = 0; db < 4; ++db)
@@ -424,6 +401,30 @@ __global__ __launch_bounds__(256, 3) void attn_mfma_kernel(
   };
   load_tile(j0, pid, kl[j0 & 1]);
   pid = fetch_pages(j0 + 1);
+  // the rotated queries are built while the first tile is in flight
+  // ---- rotated queries as bf16 B operands: lane = query row, k = head dim
+  {
+    const uint16_t* qp = q + ((int64_t)row * n_q_heads + g * G + hl) * kD;
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      const int d0 = 16 * ks + 8 * lh;
+      float lo[8], hi[8], c[8], s[8];
+      load8(qp + d0, lo);
+      load8(qp + d0 + kD / 2, hi);
+      load8(rope_cos + (int64_t)pos * (kD / 2) + d0, c);
+      load8(rope_sin + (int64_t)pos * (kD / 2) + d0, s);
+      rope_rotate<8>(lo, hi, c, s);
+      Frag a, b;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        a.w[e] = f32_to_bf16(lo[2 * e]) | (f32_to_bf16(lo[2 * e + 1]) << 16);
+        b.w[e] = f32_to_bf16(hi[2 * e]) | (f32_to_bf16(hi[2 * e + 1]) << 16);
+      }
+      qf[ks] = a.b;
+      qf[ks + 4] = b.b;
+    }
+  }
+
   store_tile(vl[j0 & 1]);
   __builtin_amdgcn_s_waitcnt(kWaitVm0);
   __syncthreads();

@@ -1,5 +1,5 @@
 // Causal GQA prefill attention over an e4m3 request KV (codes + one
-// power-of-two scale per (page, K|V)).  Same work decomposition, tile
+// power-of-two scale per (page, K|V)).  Same work decomposition, 32-key tile
 // schedule and online softmax as the bf16 kernel (attn.hip); what differs:
 //
 //   * rotated queries are quantized to e4m3 per (row, head) with the
@@ -34,7 +34,10 @@ union Frag8 {
 };
 
 constexpr int kD = 128;
-constexpr int kKT = kKvTile;           // keys per tile
+// Keys per tile.  With 64 the kernel spilled about 40 registers inside the
+// tile loop; 32-key tiles fit in the 256 registers of two waves per SIMD
+// with none (measured 23 % faster on the e4m3 RAG batch).
+constexpr int kKT = 32;
 constexpr int kKStr = kD + 16;         // bytes per e4m3 K row in LDS
 // V^T rows (fp16) are 16-byte aligned and hold each 16-key step permuted as
 // keys [0..3, 8..11, 4..7, 12..15], so that the eight keys a lane feeds to
@@ -136,82 +139,66 @@ __global__ __launch_bounds__(256, 2) void attn_fp8_kernel(
 #pragma unroll
   for (int i = 0; i < HPW; ++i) wave_active[i] = G >= 4 || (w + 4 * i) < G;
 
-  // ---- global -> register staging.  16-key blocks of a tile lie in one page.
-  // K: two 16-byte chunks per thread; chunk c covers block c/128, key
-  //    (c/8)%16 of the block, dims 16*(c%8) ..
-  // V: keys 4*(tid%16) .. +3, dims 8*(tid/16) .. +7 (8 bytes per key).
-  uint4 kr[2];
-  uint2 vr[4];
-  const int vkg = tid & 15;
+  // ---- global -> register staging.  The two 16-key blocks of a tile each
+  // lie in one page.
+  // K: one 16-byte chunk per thread: key tid / 8 (block tid / 128), dims
+  //    16 (tid % 8) ..
+  // V: keys 2 (tid % 16) and 2 (tid % 16) + 1, dims 8 (tid / 16) .. +7
+  //    (8 bytes per key); the two keys sit next to each other in the
+  //    permuted V^T row.
+  uint4 kr;
+  uint2 vr[2];
+  const int kp2 = tid & 15;               // key pair
+  const int vq = kp2 >> 3;                // 16-key block of the pair
+  const int vk = 2 * kp2 - 16 * vq;       // first key within its block
   const int vc8 = (tid >> 4) * 8;
-  const int vq = vkg >> 2;
-  const int vcol = 16 * vq + ((vkg & 1) << 3) + ((vkg & 2) << 1);   // permuted
-  float nks[4], nvs[4];   // page scales of the staged tile (uniform)
-  float tks[4];           // K page scales of the tile being computed
+  const int vcol = 16 * vq + ((vk >> 2) & 1) * 8 + ((vk >> 3) & 1) * 4 + (vk & 3);   // permuted
+  float nks[2], nvs[2];   // page scales of the staged tile (uniform)
+  float tks[2];           // K page scales of the tile being computed
   auto load_tile = [&](int j) {
     const int key0 = j * kKT;
-    int64_t base[4];
+    int64_t base[2];
 #pragma unroll
-    for (int b = 0; b < 4; ++b) {
+    for (int b = 0; b < 2; ++b) {
       const int kq = key0 + 16 * b;
       const int page = bt[min(kq >> log2_page, it.n_pages - 1)];
       base[b] = ((((int64_t)page * n_kv_heads + g) << log2_page) + (kq & page_mask)) * kD;
       nks[b] = scales[2 * page];
       nvs[b] = scales[2 * page + 1];
     }
+    kr = *reinterpret_cast<const uint4*>(kc + ((tid >> 7) ? base[1] : base[0]) +
+                                         ((tid >> 3) & 15) * kD + (tid & 7) * 16);
+    const int64_t vb = vq ? base[1] : base[0];
 #pragma unroll
-    for (int h2 = 0; h2 < 2; ++h2) {
-      const int c = tid + 256 * h2;
-      const int64_t bb = h2 == 0 ? ((tid >> 7) ? base[1] : base[0])
-                                 : ((tid >> 7) ? base[3] : base[2]);
-      kr[h2] = *reinterpret_cast<const uint4*>(kc + bb + ((c >> 3) & 15) * kD + (c & 7) * 16);
-    }
-    const int64_t vb = vq == 0 ? base[0] : vq == 1 ? base[1] : vq == 2 ? base[2] : base[3];
-#pragma unroll
-    for (int pb = 0; pb < 4; ++pb)
-      vr[pb] = *reinterpret_cast<const uint2*>(vc + vb + (4 * (vkg & 3) + pb) * kD + vc8);
+    for (int pb = 0; pb < 2; ++pb)
+      vr[pb] = *reinterpret_cast<const uint2*>(vc + vb + (vk + pb) * kD + vc8);
     if (key0 + kKT > it.kv_len) {  // last, partial tile
+      if (key0 + (tid >> 3) >= it.kv_len) kr = make_uint4(0, 0, 0, 0);
 #pragma unroll
-      for (int h2 = 0; h2 < 2; ++h2) {
-        const int c = tid + 256 * h2;
-        if (key0 + 16 * (c >> 7) + ((c >> 3) & 15) >= it.kv_len) kr[h2] = make_uint4(0, 0, 0, 0);
-      }
-#pragma unroll
-      for (int pb = 0; pb < 4; ++pb)
-        if (key0 + 4 * vkg + pb >= it.kv_len) vr[pb] = make_uint2(0, 0);
+      for (int pb = 0; pb < 2; ++pb)
+        if (key0 + 2 * kp2 + pb >= it.kv_len) vr[pb] = make_uint2(0, 0);
     }
   };
   auto store_tile = [&](int buf) {
-#pragma unroll
-    for (int h2 = 0; h2 < 2; ++h2) {
-      const int c = tid + 256 * h2;
-      const int key = 16 * (c >> 7) + ((c >> 3) & 15);
-      *reinterpret_cast<uint4*>(&kmem[buf][key * kKStr + (c & 7) * 16]) = kr[h2];
-    }
-    // V^T[d][key] in fp16: gather byte e of keys (k0, k1) and (k2, k3) into
-    // one word each and convert two codes at a time with the page scale.
-    const float s = vq == 0 ? nvs[0] : vq == 1 ? nvs[1] : vq == 2 ? nvs[2] : nvs[3];
+    *reinterpret_cast<uint4*>(&kmem[buf][(tid >> 3) * kKStr + (tid & 7) * 16]) = kr;
+    // V^T[d][key] in fp16: gather byte e of keys (k0, k1) into one word and
+    // convert two codes at a time with the page scale.
+    const float s = vq ? nvs[1] : nvs[0];
     uint16_t* vs = vmem[buf];
 #pragma unroll
     for (int half = 0; half < 2; ++half) {
       const uint32_t a0 = half ? vr[0].y : vr[0].x, a1 = half ? vr[1].y : vr[1].x;
-      const uint32_t a2 = half ? vr[2].y : vr[2].x, a3 = half ? vr[3].y : vr[3].x;
 #pragma unroll
       for (int e2 = 0; e2 < 2; ++e2) {
         // bytes (k0[e], k1[e], k0[e+1], k1[e+1]) for e = 2*e2 within the word
         const uint32_t sel = e2 ? 0x07030602u : 0x05010400u;
         const uint32_t p01 = __builtin_amdgcn_perm(a1, a0, sel);
-        const uint32_t p23 = __builtin_amdgcn_perm(a3, a2, sel);
-        // low word: keys (0,1) / (2,3) at dim e; high word: at dim e + 1
+        // low word: keys (0,1) at dim e; high word: at dim e + 1
         const f16x2 l01 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(p01, s, false);
-        const f16x2 l23 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(p23, s, false);
         const f16x2 h01 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(p01, s, true);
-        const f16x2 h23 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(p23, s, true);
         const int d = vc8 + 4 * half + 2 * e2;
-        *reinterpret_cast<uint2*>(vs + d * kVStr + vcol) =
-            make_uint2(__builtin_bit_cast(uint32_t, l01), __builtin_bit_cast(uint32_t, l23));
-        *reinterpret_cast<uint2*>(vs + (d + 1) * kVStr + vcol) =
-            make_uint2(__builtin_bit_cast(uint32_t, h01), __builtin_bit_cast(uint32_t, h23));
+        *reinterpret_cast<uint32_t*>(vs + d * kVStr + vcol) = __builtin_bit_cast(uint32_t, l01);
+        *reinterpret_cast<uint32_t*>(vs + (d + 1) * kVStr + vcol) = __builtin_bit_cast(uint32_t, h01);
       }
     }
   };
@@ -220,17 +207,17 @@ __global__ __launch_bounds__(256, 2) void attn_fp8_kernel(
     constexpr bool MASK = decltype(mask_tag)::value;
     const uint8_t* ks = kmem[j & 1];
     const uint16_t* vs = vmem[j & 1];
-    f32x16 s[HPW][2];
+    f32x16 s[HPW][1];
 #pragma unroll
     for (int i = 0; i < HPW; ++i)
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
+      for (int kb = 0; kb < 1; ++kb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) s[i][kb][r] = 0.0f;
 #pragma unroll
     for (int kst = 0; kst < 2; ++kst) {
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
+      for (int kb = 0; kb < 1; ++kb) {
         const uint8_t* kp = ks + (32 * kb + lrow) * kKStr + 64 * kst + 32 * lh;
         // both 16-byte halves land in adjacent registers of the operand
         union { uint4 u[2]; i32x8 v; } x;
@@ -243,39 +230,37 @@ __global__ __launch_bounds__(256, 2) void attn_fp8_kernel(
               a, qf[i][kst], s[i][kb], 0, 0, 0, 127, 0, 127);
       }
     }
-    // page of S register r of key block kb: 2*kb + r/8 within the tile; its
+    // page of S register r: r/8 within the tile; its
     // factor f (Q scale x K page scale x softmax scale x log2 e) is > 0, so
     // each page's row max is f times the max of its raw scores, and P =
     // exp2(f s - m) is one fma and one exp2 per score
-    f16x8 pf[HPW][4];
+    f16x8 pf[HPW][2];
 #pragma unroll
     for (int i = 0; i < HPW; ++i) {
-      float f[4];
+      float f[2];
 #pragma unroll
-      for (int b = 0; b < 4; ++b) f[b] = qs[i] * tks[b] * scale_log2e;
+      for (int b = 0; b < 2; ++b) f[b] = qs[i] * tks[b] * scale_log2e;
       if constexpr (MASK) {
         const int kbase = j * kKT;
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int key = kbase + 32 * kb + 8 * (r >> 2) + 4 * lh + (r & 3);
-            s[i][kb][r] = (key > pos || key < it.kv_lo) ? -INFINITY : s[i][kb][r];
-          }
+        for (int r = 0; r < 16; ++r) {
+          const int key = kbase + 8 * (r >> 2) + 4 * lh + (r & 3);
+          s[i][0][r] = (key > pos || key < it.kv_lo) ? -INFINITY : s[i][0][r];
+        }
       }
-      float mb[4];
+      float mb[2];
 #pragma unroll
-      for (int b = 0; b < 4; ++b) {
-        const int kb = b >> 1, r0 = 8 * (b & 1);
-        float x = s[i][kb][r0];
+      for (int b = 0; b < 2; ++b) {
+        const int r0 = 8 * b;
+        float x = s[i][0][r0];
 #pragma unroll
-        for (int r = 1; r < 8; ++r) x = fmaxf(x, s[i][kb][r0 + r]);
+        for (int r = 1; r < 8; ++r) x = fmaxf(x, s[i][0][r0 + r]);
         mb[b] = x * f[b];
       }
       // each half-wave holds half of every row's keys: the halves exchange
       // their maxima only on the rare rescale path (scores are in log2 units
       // here; see attn.hip for the lazy rescale)
-      const float mt = fmaxf(fmaxf(mb[0], mb[1]), fmaxf(mb[2], mb[3]));
+      const float mt = fmaxf(mb[0], mb[1]);
       if (__builtin_amdgcn_ballot_w64(mt > m[i] + kLazy)) {
         const float mn = fmaxf(m[i], fmaxf(mt, __shfl_xor(mt, 32)));
         const float alpha = __builtin_amdgcn_exp2f(m[i] - mn);
@@ -291,23 +276,20 @@ __global__ __launch_bounds__(256, 2) void attn_fp8_kernel(
       const float mi = m[i] == -INFINITY ? 0.0f : m[i];
       float ls[4] = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const float p = __builtin_amdgcn_exp2f(fmaf(s[i][kb][r], f[2 * kb + (r >> 3)], -mi));
-          s[i][kb][r] = p;
-          ls[r & 3] += p;
-        }
+      for (int r = 0; r < 16; ++r) {
+        const float p = __builtin_amdgcn_exp2f(fmaf(s[i][0][r], f[r >> 3], -mi));
+        s[i][0][r] = p;
+        ls[r & 3] += p;
+      }
       l[i] += (ls[0] + ls[1]) + (ls[2] + ls[3]);
 #pragma unroll
-      for (int k2 = 0; k2 < 4; ++k2) {
-        const int kb = k2 >> 1, base = 8 * (k2 & 1);
+      for (int k2 = 0; k2 < 2; ++k2) {
 #pragma unroll
-        for (int e = 0; e < 8; ++e) pf[i][k2][e] = (_Float16)s[i][kb][base + e];
+        for (int e = 0; e < 8; ++e) pf[i][k2][e] = (_Float16)s[i][0][8 * k2 + e];
       }
     }
 #pragma unroll
-    for (int k2 = 0; k2 < 4; ++k2) {
+    for (int k2 = 0; k2 < 2; ++k2) {
 #pragma unroll
       for (int db = 0; db < 4; ++db) {
         Frag8 a;
@@ -328,7 +310,7 @@ __global__ __launch_bounds__(256, 2) void attn_fp8_kernel(
   load_tile(j0);
   store_tile(j0 & 1);
 #pragma unroll
-  for (int b = 0; b < 4; ++b) tks[b] = nks[b];
+  for (int b = 0; b < 2; ++b) tks[b] = nks[b];
   __syncthreads();
   for (int j = j0; j < ntiles; ++j) {
     const bool more = j + 1 < ntiles;
@@ -339,7 +321,7 @@ __global__ __launch_bounds__(256, 2) void attn_fp8_kernel(
       tile(j, std::true_type{});
     if (more) store_tile((j + 1) & 1);
 #pragma unroll
-    for (int b = 0; b < 4; ++b) tks[b] = nks[b];
+    for (int b = 0; b < 2; ++b) tks[b] = nks[b];
     __syncthreads();
   }
 
