@@ -21,7 +21,7 @@ namespace {
 enum Fp8Mode { kFpCompose = 0, kFpAppend = 1, kFpRetain = 2 };
 
 constexpr int kD8 = 128;           // head dim of the e4m3 path
-constexpr int kMaxU = 8;           // (slot, head, pair-chunk) units per thread
+constexpr int kMaxU = 8;           // most (slot, head, pair-chunk) units per thread
 
 // k such that 2^k is the page scale for this amax.
 __device__ __forceinline__ int page_scale_exp(float amax) {
@@ -69,7 +69,10 @@ __device__ __forceinline__ uint2 encode8(const float* y) {
   return make_uint2(w[0], w[1]);
 }
 
-template <int MODE>
+// U: (slot, head, pair-chunk) units per thread, at least B * H_kv * 8 / 256
+// (instantiated for 2, 4 and 8; each unit holds 16 fp32 values and its raw
+// V, so U sets the kernel's registers and with them its occupancy).
+template <int MODE, int U>
 __global__ __launch_bounds__(256) void page_fp8_kernel(
     const PageDesc* __restrict__ pages, const float* __restrict__ rope_cos,
     const float* __restrict__ rope_sin, const void* __restrict__ src_k,
@@ -86,11 +89,11 @@ __global__ __launch_bounds__(256) void page_fp8_kernel(
   const int units = B * n_kv_heads * 8;          // (slot, head, pair-chunk)
 
   // unit u: pair-chunk c (dims 8c.. and 64+8c..), slot s, head h
-  float kv[kMaxU][16];
+  float kv[U][16];
   float amax_k = 0.0f, amax_v = 0.0f;
-  uint4 vraw[kMaxU][2];     // V source: e4m3 codes (compose, low 8 bytes) or bf16
+  uint4 vraw[U][2];         // V source: e4m3 codes (compose, low 8 bytes) or bf16
 #pragma unroll
-  for (int k = 0; k < kMaxU; ++k) {
+  for (int k = 0; k < U; ++k) {
     const int u = tid + 256 * k;
     if (u >= units) break;
     const int c = u & 7, s = (u >> 3) & (B - 1), h = u >> (3 + log2_page);
@@ -158,7 +161,7 @@ __global__ __launch_bounds__(256) void page_fp8_kernel(
                               : ldexpf(1.0f, ev);
   }
 #pragma unroll
-  for (int k = 0; k < kMaxU; ++k) {
+  for (int k = 0; k < U; ++k) {
     const int u = tid + 256 * k;
     if (u >= units) break;
     const int c = u & 7, s = (u >> 3) & (B - 1), h = u >> (3 + log2_page);
@@ -198,10 +201,17 @@ hipError_t launch_pages(const tsr_plan* p, const PageDesc* pages, int n,
                         hipStream_t s) {
   if (n <= 0) return hipSuccess;
   const tsr_model& m = p->model;
-  hipLaunchKernelGGL(page_fp8_kernel<MODE>, dim3(n, n_layers), dim3(256), 0, s, pages,
-                     p->dev.rope_cos, p->dev.rope_sin, sk, sv, ssc,
-                     static_cast<uint8_t*>(dk), static_cast<uint8_t*>(dv), dsc,
-                     m.n_kv_heads, ilog2(m.page_size), ss, ds, sss, dss);
+  const int units = m.page_size * m.n_kv_heads * 8;
+  if (units > 256 * kMaxU) return hipErrorInvalidValue;   // the planner rejects these
+#define TSR_PAGES(UU)                                                                    \
+  hipLaunchKernelGGL((page_fp8_kernel<MODE, UU>), dim3(n, n_layers), dim3(256), 0, s, pages, \
+                     p->dev.rope_cos, p->dev.rope_sin, sk, sv, ssc,                        \
+                     static_cast<uint8_t*>(dk), static_cast<uint8_t*>(dv), dsc,           \
+                     m.n_kv_heads, ilog2(m.page_size), ss, ds, sss, dss)
+  if (units <= 512) TSR_PAGES(2);
+  else if (units <= 1024) TSR_PAGES(4);
+  else TSR_PAGES(8);
+#undef TSR_PAGES
   return hipGetLastError();
 }
 
