@@ -513,7 +513,10 @@ def main():
     G = m.n_q_heads // m.n_kv_heads
     attn_kernel = (f"attn_fp8_kernel<{G}>" if m.kv_dtype == "e4m3"
                    else f"attn_mfma_kernel<{G}, false>")
-    compose_kernel = ("page_fp8_kernel<0>" if m.kv_dtype == "e4m3" else
+    # the e4m3 page kernel is instantiated for 2, 4 or 8 units per thread
+    units = m.page_size * m.n_kv_heads * 8
+    u = 2 if units <= 512 else 4 if units <= 1024 else 8
+    compose_kernel = (f"page_fp8_kernel<0, {u}>" if m.kv_dtype == "e4m3" else
                       f"kv_move_kernel<{m.head_dim}, unsigned short, 0>")
     value = wl.prompt_tokens / (ms * 1e-3)
 
