@@ -322,6 +322,11 @@ __global__ __launch_bounds__(256, 3) void attn_mfma_kernel(
     }
     __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
 
+    // the V^T fragments of the first 16 keys are read while the softmax runs
+    Frag va[4];
+#pragma unroll
+    for (int db = 0; db < 4; ++db)
+      va[db].u = *reinterpret_cast<const uint4*>(vs + (32 * db + lrow) * kVStr + 8 * lh);
     if constexpr (MASK) {
       const int kbase = j * kKT;
 #pragma unroll
@@ -355,25 +360,33 @@ __global__ __launch_bounds__(256, 3) void attn_mfma_kernel(
     const float mc = m == -INFINITY ? 0.0f : m * scale_log2e;
 #pragma unroll
     for (int r = 0; r < 16; ++r) s[r] = __builtin_amdgcn_exp2f(fmaf(s[r], scale_log2e, -mc));
-    // row sum in fp32 from the unrounded P, as four independent chains
-    float ls[4] = {s[0], s[1], s[2], s[3]};
-#pragma unroll
-    for (int r = 4; r < 16; ++r) ls[r & 3] += s[r];
-    l += (ls[0] + ls[1]) + (ls[2] + ls[3]);
     f16x8 pf[2];
 #pragma unroll
     for (int h = 0; h < 2; ++h)
 #pragma unroll
       for (int e = 0; e < 8; ++e) pf[h][e] = (_Float16)s[8 * h + e];
-    // O^T[d][row] += V^T[d][keys] P^T[keys][row]
+    // O^T[d][row] += V^T[d][keys] P^T[keys][row], in program order (the
+    // scheduling barriers keep the compiler from serialising the fragment
+    // reads behind one register set): each MFMA of the first 16 keys frees
+    // its fragment registers for the matching fragment of the last 16, and
+    // the row sum (fp32, from the unrounded P, four independent chains) sits
+    // between the MFMAs of the second half.
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int h = 0; h < 2; ++h)
+    for (int db = 0; db < 4; ++db) {
+      o[db] = __builtin_amdgcn_mfma_f32_32x32x16_f16(va[db].h, pf[0], o[db], 0, 0, 0);
+      va[db].u = *reinterpret_cast<const uint4*>(vs + (32 * db + lrow) * kVStr + 16 + 8 * lh);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    float ls[4] = {s[0], s[1], s[2], s[3]};
 #pragma unroll
-      for (int db = 0; db < 4; ++db) {
-        Frag a;
-        a.u = *reinterpret_cast<const uint4*>(vs + (32 * db + lrow) * kVStr + 16 * h + 8 * lh);
-        o[db] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a.h, pf[h], o[db], 0, 0, 0);
-      }
+    for (int db = 0; db < 4; ++db) {
+      o[db] = __builtin_amdgcn_mfma_f32_32x32x16_f16(va[db].h, pf[1], o[db], 0, 0, 0);
+#pragma unroll
+      for (int r = 4 + 3 * db; r < 7 + 3 * db; ++r) ls[r & 3] += s[r];
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    l += (ls[0] + ls[1]) + (ls[2] + ls[3]);
   };
 
   // keys kv_lo .. kv_len-1: tiles j0 .. ntiles-1.  A tile needs the mask
