@@ -512,7 +512,7 @@ def main():
     peak = PEAK_E4M3_BLEND if m.kv_dtype == "e4m3" else PEAK_MFMA_TFLOPS[m.act_dtype]
     G = m.n_q_heads // m.n_kv_heads
     attn_kernel = (f"attn_fp8_kernel<{G}>" if m.kv_dtype == "e4m3"
-                   else f"attn_mfma_kernel<{G}, false>")
+                   else f"attn_mfma_kernel<{G}, false, {plan.attn_rows_per_item // 32}>")
     # the e4m3 page kernel is instantiated for 2, 4 or 8 units per thread
     units = m.page_size * m.n_kv_heads * 8
     u = 2 if units <= 512 else 4 if units <= 1024 else 8

@@ -219,8 +219,14 @@ int32_t tsr_plan_num_compute_tokens(const tsr_plan* plan);
 int32_t tsr_plan_num_gather_tokens(const tsr_plan* plan);
 /* Number of tokens written by tsr_retain_kv. */
 int32_t tsr_plan_num_retain_tokens(const tsr_plan* plan);
-/* Number of attention work items (row tile x KV head). */
+/* Number of attention work items (row tile x KV head, plus launch padding).
+ * A row tile holds up to 32 consecutive computed rows, or up to 96 in bf16
+ * plans whose runs of rows with a common first visible key are long enough
+ * (the bf16 kernel then runs three 32-row blocks per workgroup). */
 int32_t tsr_plan_num_attn_items(const tsr_plan* plan);
+/* Most computed rows an attention item of this plan holds: 32, or 96 when
+ * the bf16 kernel runs three row blocks per workgroup; -1 for a null plan. */
+int32_t tsr_plan_attn_rows_per_item(const tsr_plan* plan);
 
 /* The attention items in two parts, so that attention can start while the
  * cached states are still on their way (Section 5.3: cache hits transfer

@@ -34,7 +34,7 @@ EXPORTS = (
     "tsr_abi_version", "tsr_last_error", "tsr_rope_table_bytes",
     "tsr_rope_table_init", "tsr_plan_workspace_size", "tsr_plan_create",
     "tsr_plan_num_compute_tokens", "tsr_plan_num_gather_tokens",
-    "tsr_plan_num_retain_tokens", "tsr_plan_num_attn_items",
+    "tsr_plan_num_retain_tokens", "tsr_plan_num_attn_items", "tsr_plan_attn_rows_per_item",
     "tsr_plan_num_attn_items_part", "tsr_attn_part", "tsr_plan_create_ex",
     "tsr_plan_num_aliased_pages", "tsr_attn_aliased",
     "tsr_plan_compute_positions", "tsr_plan_row_kv_lo", "tsr_plan_destroy", "tsr_compose_kv",
@@ -126,6 +126,7 @@ def lib():
             "tsr_plan_num_gather_tokens": (c_int32, [P]),
             "tsr_plan_num_retain_tokens": (c_int32, [P]),
             "tsr_plan_num_attn_items": (c_int32, [P]),
+            "tsr_plan_attn_rows_per_item": (c_int32, [P]),
             "tsr_plan_num_attn_items_part": (c_int32, [P, c_int32]),
             "tsr_plan_num_aliased_pages": (c_int32, [P]),
             "tsr_plan_create_ex": (c_int32, [POINTER(tsr_model), POINTER(tsr_request), c_int32,
@@ -302,6 +303,10 @@ class Plan:
     @property
     def num_attn_items(self) -> int:
         return lib().tsr_plan_num_attn_items(self.handle)
+
+    @property
+    def attn_rows_per_item(self) -> int:
+        return lib().tsr_plan_attn_rows_per_item(self.handle)
 
     def num_attn_items_part(self, part: int) -> int:
         return lib().tsr_plan_num_attn_items_part(self.handle, part)

@@ -226,6 +226,9 @@ int32_t tsr_plan_num_compute_tokens(const tsr_plan* p) { return p ? p->T : -1; }
 int32_t tsr_plan_num_gather_tokens(const tsr_plan* p) { return p ? p->n_gather : -1; }
 int32_t tsr_plan_num_retain_tokens(const tsr_plan* p) { return p ? p->n_retain : -1; }
 int32_t tsr_plan_num_attn_items(const tsr_plan* p) { return p ? p->n_items : -1; }
+int32_t tsr_plan_attn_rows_per_item(const tsr_plan* p) {
+  return p ? kTileRows * p->row_blocks : -1;
+}
 int32_t tsr_plan_num_aliased_pages(const tsr_plan* p) { return p ? p->n_aliased : -1; }
 
 int32_t tsr_plan_num_attn_items_part(const tsr_plan* p, int32_t part) {

@@ -191,8 +191,10 @@ __device__ __forceinline__ uint32_t pack_f16x2(float a, float b) {
 // AV: V aliasing -- the V of a 16-key block comes from the page the V block
 // table names, a pool page when kPoolPageFlag is set (else the request page
 // the K block table names).
-template <int G, bool AV>
-__global__ __launch_bounds__(256, 3) void attn_mfma_kernel(
+// R: row blocks per workgroup.  Waves 4 b .. 4 b + 3 own the 32 rows of row
+// block b; the first four waves stage every K/V tile for all of them.
+template <int G, bool AV, int R>
+__global__ __launch_bounds__(256 * R, 3) void attn_mfma_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc,
     const uint16_t* __restrict__ vc, const uint16_t* __restrict__ pool_v,
     const AttnItem* __restrict__ items, const int32_t* __restrict__ bts,
@@ -207,7 +209,10 @@ __global__ __launch_bounds__(256, 3) void attn_mfma_kernel(
   const AttnItem it = items[blockIdx.x];
   if (it.n_rows == 0) return;
   const int tid = threadIdx.x;
-  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wg = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int w = R == 1 ? wg : wg & 3;    // query head slot
+  const int rb = R == 1 ? 0 : wg >> 2;   // row block
+  const bool stager = R == 1 || wg < 4;  // waves that stage K and V
   const int lane = tid & 63;
   const int lrow = lane & 31;
   const int lh = lane >> 5;
@@ -215,8 +220,17 @@ __global__ __launch_bounds__(256, 3) void attn_mfma_kernel(
   const int page_mask = (1 << log2_page) - 1;
   const int32_t* bt = bts + it.bt_off;
 
-  const int row = it.row0 + min(lrow, it.n_rows - 1);
+  const int rbase = 32 * rb;
+  const int row = it.row0 + min(rbase + lrow, it.n_rows - 1);
   const int pos = rows[row].pos;
+  // key tiles this wave's rows need: up to their largest position
+  int my_ntiles = 0;
+  if constexpr (R > 1) {
+    int wmax = rbase + lrow < it.n_rows ? pos : -1;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) wmax = max(wmax, __shfl_xor(wmax, o));
+    my_ntiles = __builtin_amdgcn_readfirstlane(wmax + kKT) / kKT;
+  }
   // wave w owns query head head0 + w of the group; with G < 4 the spare
   // waves recompute head G-1 and store nothing
   const int hl = G >= 4 ? it.head0 + w : min(w, G - 1);
@@ -395,25 +409,42 @@ __global__ __launch_bounds__(256, 3) void attn_mfma_kernel(
   const int j0 = it.kv_lo / kKT;
   const int jlo = min(ntiles, (it.kv_lo + kKT - 1) / kKT);   // first tile without keys < kv_lo
   const int nfull = min(ntiles, (it.min_pos + 1) / kKT);      // tiles ending at or before min_pos
-  int pid = fetch_pages(j0);   // ids of the next tile to load
+  int pid = fetch_pages(j0);   // ids of the next tile to load (staging waves)
   // One tile j: issue the next tile's loads into the other buffers, compute
   // this one, stage the next V^T, wait for this wave's direct K loads, then
   // the workgroup barrier.
-  auto run_tiles = [&](int ja, int jb, auto mask_tag) __attribute__((always_inline)) {
+  // SKIP: tiles past a row block's last row occur only in the masked tail.
+  auto run_tiles = [&](int ja, int jb, auto mask_tag, auto skip_tag)
+      __attribute__((always_inline)) {
+    constexpr bool SKIP = R > 1 && decltype(skip_tag)::value;
     for (int j = ja; j < jb; ++j) {
       const bool more = j + 1 < ntiles;
       if (more) {
         load_tile(j + 1, pid, kl[(j + 1) & 1]);
         pid = fetch_pages(j + 2);
       }
-      tile(j, mask_tag, kl[j & 1], vl[j & 1]);
+      if (!SKIP || j < my_ntiles) tile(j, mask_tag, kl[j & 1], vl[j & 1]);
       if (more) store_tile(vl[(j + 1) & 1]);
       __builtin_amdgcn_s_waitcnt(kWaitVm0);
       __syncthreads();
     }
   };
-  load_tile(j0, pid, kl[j0 & 1]);
-  pid = fetch_pages(j0 + 1);
+  // The waves of the other row blocks stage nothing and skip the tiles past
+  // their own rows (fully masked for them).  Kept as a separate loop: with
+  // the staging under a wave-dependent condition in one loop the compiler
+  // kept the staging registers live in every wave and spilled.
+  auto run_tiles_ns = [&](int ja, int jb, auto mask_tag, auto skip_tag)
+      __attribute__((always_inline)) {
+    constexpr bool SKIP = decltype(skip_tag)::value;
+    for (int j = ja; j < jb; ++j) {
+      if (!SKIP || j < my_ntiles) tile(j, mask_tag, kl[j & 1], vl[j & 1]);
+      __syncthreads();
+    }
+  };
+  if (stager) {
+    load_tile(j0, pid, kl[j0 & 1]);
+    pid = fetch_pages(j0 + 1);
+  }
   // the rotated queries are built while the first tile is in flight
   // ---- rotated queries as bf16 B operands: lane = query row, k = head dim
   {
@@ -438,16 +469,22 @@ __global__ __launch_bounds__(256, 3) void attn_mfma_kernel(
     }
   }
 
-  store_tile(vl[j0 & 1]);
+  if (stager) store_tile(vl[j0 & 1]);
   __builtin_amdgcn_s_waitcnt(kWaitVm0);
   __syncthreads();
-  run_tiles(j0, jlo, std::true_type{});
-  run_tiles(jlo, max(jlo, nfull), std::false_type{});
-  run_tiles(max(jlo, nfull), ntiles, std::true_type{});
+  if (stager) {
+    run_tiles(j0, jlo, std::true_type{}, std::false_type{});
+    run_tiles(jlo, max(jlo, nfull), std::false_type{}, std::false_type{});
+    run_tiles(max(jlo, nfull), ntiles, std::true_type{}, std::true_type{});
+  } else {
+    run_tiles_ns(j0, jlo, std::true_type{}, std::false_type{});
+    run_tiles_ns(jlo, max(jlo, nfull), std::false_type{}, std::false_type{});
+    run_tiles_ns(max(jlo, nfull), ntiles, std::true_type{}, std::true_type{});
+  }
 
   // ---- epilogue: normalise, round to bf16, store rows of this tile
   const float lt = l + __shfl_xor(l, 32);
-  if (!wave_active || lrow >= it.n_rows) return;
+  if (!wave_active || rbase + lrow >= it.n_rows) return;
   const float inv = 1.0f / lt;
   const int hq = g * G + (G >= 4 ? it.head0 : 0) + w;
   uint16_t* op = out + ((int64_t)row * n_q_heads + hq) * kD;
@@ -479,8 +516,9 @@ hipError_t launch_attn(const tsr_plan* p, const AttnItem* items, int32_t n_items
   const tsr_model& m = p->model;
   const int lp = ilog2(m.page_size);
   const int G = m.n_q_heads / m.n_kv_heads;
-  const dim3 grid(n_items), block(256);
+  const dim3 grid(n_items);
   if (m.act_dtype == TSR_F32) {
+    const dim3 block(256);
 #define TSR_F32K(DIM)                                                             \
   hipLaunchKernelGGL(attn_f32_kernel<DIM>, grid, block, 0, s,                     \
                      static_cast<const float*>(q), static_cast<const float*>(req_k), \
@@ -499,7 +537,12 @@ hipError_t launch_attn(const tsr_plan* p, const AttnItem* items, int32_t n_items
   }
   const float sl2e = (float)((double)p->scale * 1.4426950408889634);
 #define TSR_MFMA(GG, AV)                                                           \
-  hipLaunchKernelGGL((attn_mfma_kernel<GG, AV>), grid, block, 0, s,                \
+  if (p->row_blocks == kMaxRowBlocks)                                              \
+    TSR_MFMA_R(GG, AV, kMaxRowBlocks);                                             \
+  else                                                                             \
+    TSR_MFMA_R(GG, AV, 1)
+#define TSR_MFMA_R(GG, AV, RB)                                                     \
+  hipLaunchKernelGGL((attn_mfma_kernel<GG, AV, RB>), grid, dim3(256 * (RB)), 0, s, \
                      static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(req_k), \
                      static_cast<const uint16_t*>(req_v),                          \
                      static_cast<const uint16_t*>(pool_v), items,                  \
@@ -520,6 +563,7 @@ hipError_t launch_attn(const tsr_plan* p, const AttnItem* items, int32_t n_items
     default: return hipErrorInvalidValue;
   }
 #undef TSR_MFMA
+#undef TSR_MFMA_R
   return hipGetLastError();
 }
 

@@ -338,41 +338,66 @@ tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
     return fail(TSR_ERR_OUT_OF_RANGE, "batch too large");
   }
 
-  // attention items: tiles of kTileRows consecutive rows x KV heads
-  // The MFMA kernels give each of their 4 waves one query head; a larger
-  // GQA group is split over several items that read the same K/V tiles
-  // (adjacent in the launch order, so the repeat reads hit L2).
+  // attention items: up to rb * kTileRows consecutive rows x KV heads
+  // The MFMA kernels give each of their 4 waves per row block one query
+  // head; a larger GQA group is split over several items that read the same
+  // K/V tiles (adjacent in the launch order, so the repeat reads hit L2).
   const int G = m.n_q_heads / Hkv;
   const int hsplit = (m.act_dtype == TSR_BF16 && G > 4) ? G / 4 : 1;
   struct Item { AttnItem it; int64_t cost; int group; int part; };
   std::vector<Item> items;
   int32_t max_kv = 0;
-  for (int r = 0; r < n_req; ++r) {
-    // runs of consecutive rows with the same first visible key
-    for (int32_t a0 = req_row0[r]; a0 < req_row0[r + 1];) {
-      int32_t a1 = a0 + 1;
-      while (a1 < req_row0[r + 1] && p->row_lo[a1] == p->row_lo[a0]) ++a1;
-      const int32_t kv_lo = p->row_lo[a0];
-      for (int32_t t0 = a0; t0 < a1; t0 += kTileRows) {
-        const int32_t n = std::min(kTileRows, a1 - t0);
-        const int32_t lo = p->row_pos[t0], hi = p->row_pos[t0 + n - 1];
-        max_kv = std::max(max_kv, hi + 1);
-        // part 1 if a gathered position lies in the key tiles the kernels
-        // load for this item (masked keys included): [tile of kv_lo, end of
-        // the tile of hi]
-        const int32_t klo = kv_lo / kKvTile * kKvTile;
-        const int32_t khi = (hi / kKvTile + 1) * kKvTile;
-        int part = 0;
-        for (const auto& iv : gathered[r])
-          if (iv.first < khi && iv.second > klo) part = 1;
-        for (int g = 0; g < Hkv; ++g)
-          for (int hs = 0; hs < hsplit; ++hs) {
-            AttnItem a{t0, n, hi + 1, lo, g, bt_off[r], bt_len[r], 4 * hs, kv_lo, {0, 0, 0}};
-            items.push_back({a, (int64_t)(hi + 1 - kv_lo), r * Hkv + g, part});
-          }
+  // Builds the items for row blocks of kTileRows rows, rb per item; returns
+  // the share of the items' (row block x key tile) slots that hold keys a
+  // row block needs (a row block skips the tiles past its last row).
+  auto build_items = [&](int rb) -> double {
+    items.clear();
+    max_kv = 0;
+    const int32_t tile_rows = kTileRows * rb;
+    int64_t need = 0, slots = 0;
+    for (int r = 0; r < n_req; ++r) {
+      // runs of consecutive rows with the same first visible key
+      for (int32_t a0 = req_row0[r]; a0 < req_row0[r + 1];) {
+        int32_t a1 = a0 + 1;
+        while (a1 < req_row0[r + 1] && p->row_lo[a1] == p->row_lo[a0]) ++a1;
+        const int32_t kv_lo = p->row_lo[a0];
+        for (int32_t t0 = a0; t0 < a1; t0 += tile_rows) {
+          const int32_t n = std::min(tile_rows, a1 - t0);
+          const int32_t lo = p->row_pos[t0], hi = p->row_pos[t0 + n - 1];
+          max_kv = std::max(max_kv, hi + 1);
+          const int32_t t_lo = kv_lo / kMfmaKeys;
+          slots += (int64_t)rb * (hi / kMfmaKeys + 1 - t_lo);
+          for (int32_t b0 = 0; b0 < n; b0 += kTileRows)
+            need += p->row_pos[t0 + std::min(n, b0 + kTileRows) - 1] / kMfmaKeys + 1 - t_lo;
+          // part 1 if a gathered position lies in the key tiles the kernels
+          // load for this item (masked keys included): [tile of kv_lo, end
+          // of the tile of hi]
+          const int32_t klo = kv_lo / kKvTile * kKvTile;
+          const int32_t khi = (hi / kKvTile + 1) * kKvTile;
+          int part = 0;
+          for (const auto& iv : gathered[r])
+            if (iv.first < khi && iv.second > klo) part = 1;
+          for (int g = 0; g < Hkv; ++g)
+            for (int hs = 0; hs < hsplit; ++hs) {
+              AttnItem a{t0, n, hi + 1, lo, g, bt_off[r], bt_len[r], 4 * hs, kv_lo, {0, 0, 0}};
+              items.push_back({a, (int64_t)(hi + 1 - kv_lo), r * Hkv + g, part});
+            }
+        }
+        a0 = a1;
       }
-      a0 = a1;
     }
+    return slots ? (double)need / (double)slots : 1.0;
+  };
+  // The bf16 MFMA kernel runs kMaxRowBlocks row blocks per workgroup (its
+  // K/V staging then serves three times the rows) unless short runs of rows
+  // (unit-local attention) would leave too many row blocks idle; the other
+  // kernels take one row block.
+  p->row_blocks = 1;
+  if (m.act_dtype == TSR_BF16 && m.kv_dtype == TSR_BF16 &&
+      build_items(kMaxRowBlocks) >= kMinRowBlockUse) {
+    p->row_blocks = kMaxRowBlocks;
+  } else {
+    build_items(1);
   }
   // XCD-aware order: (request, KV head) groups share K/V, so each group is
   // bound to one XCD bin (workgroup w runs on XCD w % kNumXcd); bins are

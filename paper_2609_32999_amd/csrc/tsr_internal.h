@@ -15,10 +15,17 @@
 
 namespace tsr {
 
-// Rows of one attention tile: consecutive computed rows of one request.
+// Rows of one attention row block: consecutive computed rows of one request.
 constexpr int kTileRows = 32;
-// Keys per attention KV tile.
+// Row blocks per bf16 attention item (one workgroup of 4 waves per row
+// block), used when at least kMinRowBlockUse of the item's row-block x key
+// tile slots hold work.
+constexpr int kMaxRowBlocks = 3;
+constexpr double kMinRowBlockUse = 0.8;
+// Keys per attention KV tile (granularity of the host-tier split of items).
 constexpr int kKvTile = 64;
+// Keys per tile of the bf16 MFMA attention kernel.
+constexpr int kMfmaKeys = 32;
 // Set in a V block-table entry whose page is a pool page (V aliasing).
 constexpr int32_t kPoolPageFlag = 1 << 30;
 // Workgroups of the MFMA attention are dealt round-robin over this many XCDs.
@@ -58,13 +65,13 @@ struct alignas(16) PageDesc {
   int32_t n;
 };
 
-// One attention work item: up to kTileRows consecutive computed rows of one
-// request, all with the same first visible key, against one KV head, for
+// One attention work item: up to row_blocks x kTileRows consecutive computed
+// rows of one request, all with the same first visible key, against one KV head, for
 // query heads head0 .. head0+3 of that KV head's group (MFMA kernels; a
 // group of G > 4 heads is split over G/4 items).  n_rows == 0 marks padding.
 struct alignas(16) AttnItem {
   int32_t row0;      // first computed row (plan order)
-  int32_t n_rows;    // rows in the tile (<= kTileRows)
+  int32_t n_rows;    // rows in the item (<= row_blocks * kTileRows)
   int32_t kv_len;    // keys kv_lo .. kv_len-1 are visible to some row (max pos + 1)
   int32_t min_pos;   // smallest position among the rows
   int32_t kv_head;
@@ -107,6 +114,7 @@ struct tsr_plan {
   // [0] none (runnable before compose), [1] some; each scheduled on its own
   int32_t n_items_part[2];
   int32_t max_kv_len;
+  int32_t row_blocks;       // row blocks per attention item (1 or kMaxRowBlocks)
   int32_t n_gpages, n_apages, n_rpages;   // e4m3 plans only
   std::vector<int32_t> row_pos, row_req, row_lo;
   std::vector<char> image;  // host copy of the device image

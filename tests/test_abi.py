@@ -61,6 +61,57 @@ def test_host_plan_matches_oracle_sets(name):
     assert plan.num_attn_items % 8 == 0
 
 
+def _items_per_kv_head(wl, rows_per_item):
+    """Attention items of each KV head (before launch padding) when runs of
+    rows with the same first visible key are cut into items of
+    rows_per_item rows, and the share of (32-row block x 32-key tile) slots
+    of those items that hold keys the block's rows need."""
+    n = need = slots = 0
+    for req in wl.requests:
+        pos, lo = L.compute_positions(req), L.row_kv_lo(req)
+        a0 = 0
+        while a0 < len(pos):
+            a1 = a0 + 1
+            while a1 < len(pos) and lo[a1] == lo[a0]:
+                a1 += 1
+            for t0 in range(a0, a1, rows_per_item):
+                p = pos[t0:min(a1, t0 + rows_per_item)]
+                n += 1
+                slots += (rows_per_item // 32) * (p[-1] // 32 + 1 - lo[t0] // 32)
+                need += sum(p[b:b + 32].max() // 32 + 1 - lo[t0] // 32
+                            for b in range(0, len(p), 32))
+            a0 = a1
+    return n, need / slots
+
+
+@pytest.mark.parametrize("name,scope", [("rag8b", "global"), ("rag8b", "local"),
+                                        ("agent8b", "local"), ("long70b", "global"),
+                                        ("fp8rag", "global"), ("small_f32", "global")])
+def test_attention_row_blocks(name, scope):
+    """bf16 plans put three 32-row blocks in an item unless fewer than 80 % of
+    the items' block x tile slots would hold work; other dtypes use one."""
+    cfg = workloads.get_config(name)
+    if scope != "global":
+        cfg = cfg.with_(miss_scope=scope)
+    wl = workloads.make_workload(cfg)
+    m = wl.model
+    n1, _ = _items_per_kv_head(wl, 32)
+    n3, use3 = _items_per_kv_head(wl, 96)
+    three = m.kv_dtype == "bf16" and m.act_dtype == "bf16" and use3 >= 0.8
+    groups = (m.n_q_heads // m.n_kv_heads) // 4 if m.act_dtype == "bf16" and \
+        m.n_q_heads // m.n_kv_heads > 4 else 1
+    per = m.n_kv_heads * groups
+    plan = _plan(wl)
+    # launch padding only adds items: three row blocks give fewer items than
+    # one-block items would need, one row block at least that many
+    if three:
+        assert n3 * per <= plan.num_attn_items < n1 * per, (plan.num_attn_items, n1, n3, use3)
+    else:
+        assert plan.num_attn_items >= n1 * per, (plan.num_attn_items, n1, n3, use3)
+    assert bool(three) == ((name, scope) in {("rag8b", "global"), ("long70b", "global")})
+    assert plan.attn_rows_per_item == (96 if three else 32)
+
+
 def _tiny_req(**over):
     wl = workloads.generate("tiny")
     req = wl.requests[0]
