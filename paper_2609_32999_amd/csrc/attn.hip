@@ -430,14 +430,13 @@ __global__ __launch_bounds__(256 * R, 3) void attn_mfma_kernel(
     }
   };
   // The waves of the other row blocks stage nothing and skip the tiles past
-  // their own rows (fully masked for them).  Kept as a separate loop: with
-  // the staging under a wave-dependent condition in one loop the compiler
-  // kept the staging registers live in every wave and spilled.
-  auto run_tiles_ns = [&](int ja, int jb, auto mask_tag, auto skip_tag)
-      __attribute__((always_inline)) {
-    constexpr bool SKIP = decltype(skip_tag)::value;
+  // their own rows (fully masked for them; all tiles for a row block past
+  // the item's last row).  Kept as a separate loop: with the staging under
+  // a wave-dependent condition in one loop the compiler kept the staging
+  // registers live in every wave and spilled.
+  auto run_tiles_ns = [&](int ja, int jb, auto mask_tag) __attribute__((always_inline)) {
     for (int j = ja; j < jb; ++j) {
-      if (!SKIP || j < my_ntiles) tile(j, mask_tag, kl[j & 1], vl[j & 1]);
+      if (j < my_ntiles) tile(j, mask_tag, kl[j & 1], vl[j & 1]);
       __syncthreads();
     }
   };
@@ -477,9 +476,9 @@ __global__ __launch_bounds__(256 * R, 3) void attn_mfma_kernel(
     run_tiles(jlo, max(jlo, nfull), std::false_type{}, std::false_type{});
     run_tiles(max(jlo, nfull), ntiles, std::true_type{}, std::true_type{});
   } else {
-    run_tiles_ns(j0, jlo, std::true_type{}, std::false_type{});
-    run_tiles_ns(jlo, max(jlo, nfull), std::false_type{}, std::false_type{});
-    run_tiles_ns(max(jlo, nfull), ntiles, std::true_type{}, std::true_type{});
+    run_tiles_ns(j0, jlo, std::true_type{});
+    run_tiles_ns(jlo, max(jlo, nfull), std::false_type{});
+    run_tiles_ns(max(jlo, nfull), ntiles, std::true_type{});
   }
 
   // ---- epilogue: normalise, round to bf16, store rows of this tile
