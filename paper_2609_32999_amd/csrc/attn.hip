@@ -188,6 +188,12 @@ __device__ __forceinline__ uint32_t pack_f16x2(float a, float b) {
   return __builtin_bit_cast(uint32_t, h);
 }
 
+// Masking of a tile's scores (tile loops are instantiated per kind).
+constexpr int kNoMask = 0, kMaskCausal = 1, kMaskBoth = 2;
+using NoMask = std::integral_constant<int, kNoMask>;
+using MaskCausal = std::integral_constant<int, kMaskCausal>;
+using MaskBoth = std::integral_constant<int, kMaskBoth>;
+
 // AV: V aliasing -- the V of a 16-key block comes from the page the V block
 // table names, a pool page when kPoolPageFlag is set (else the request page
 // the K block table names).
@@ -223,6 +229,7 @@ __global__ __launch_bounds__(256 * R, 3) void attn_mfma_kernel(
   const int rbase = 32 * rb;
   const int row = it.row0 + min(rbase + lrow, it.n_rows - 1);
   const int pos = rows[row].pos;
+  const int pos_l = pos - 4 * lh;   // position less the lane's key offset in a tile
   // key tiles this wave's rows need: up to their largest position
   int my_ntiles = 0;
   if constexpr (R > 1) {
@@ -312,11 +319,12 @@ __global__ __launch_bounds__(256 * R, 3) void attn_mfma_kernel(
   };
 
   // One 32-key tile: S^T = K Q^T, online softmax, O^T += V^T P^T.
-  // MASK: apply the causal mask (only tiles reaching past the smallest row
-  // position of the item, or starting below kv_lo, need it).
+  // MASK: kNoMask, kMaskCausal (keys past the row's position: tiles reaching
+  // past the smallest row position of the item) or kMaskBoth (also keys
+  // below kv_lo: the tile holding kv_lo).
   auto tile = [&](int j, auto mask_tag, const uint8_t* ks, const uint16_t* vs)
       __attribute__((always_inline)) {
-    constexpr bool MASK = decltype(mask_tag)::value;
+    constexpr int MASK = decltype(mask_tag)::value;
     f32x16 s;
 #pragma unroll
     for (int r = 0; r < 16; ++r) s[r] = 0.0f;
@@ -341,12 +349,16 @@ __global__ __launch_bounds__(256 * R, 3) void attn_mfma_kernel(
 #pragma unroll
     for (int db = 0; db < 4; ++db)
       va[db].u = *reinterpret_cast<const uint4*>(vs + (32 * db + lrow) * kVStr + 8 * lh);
-    if constexpr (MASK) {
-      const int kbase = j * kKT;
+    if constexpr (MASK != kNoMask) {
+      // score r holds key j kKT + 8 (r / 4) + 4 lh + r % 4: compare its
+      // offset in the tile with the row's bounds moved to the same origin
+      const int dhi = pos_l - j * kKT;
+      const int dlo = it.kv_lo - 4 * lh - j * kKT;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int key = kbase + 8 * (r >> 2) + 4 * lh + (r & 3);
-        s[r] = (key > pos || key < it.kv_lo) ? -INFINITY : s[r];
+        const int off = 8 * (r >> 2) + (r & 3);
+        const bool out = MASK == kMaskBoth ? (off > dhi || off < dlo) : off > dhi;
+        s[r] = out ? -INFINITY : s[r];
       }
     }
     // Online softmax with a lazily updated running max: the max (and with
@@ -472,13 +484,13 @@ __global__ __launch_bounds__(256 * R, 3) void attn_mfma_kernel(
   __builtin_amdgcn_s_waitcnt(kWaitVm0);
   __syncthreads();
   if (stager) {
-    run_tiles(j0, jlo, std::true_type{}, std::false_type{});
-    run_tiles(jlo, max(jlo, nfull), std::false_type{}, std::false_type{});
-    run_tiles(max(jlo, nfull), ntiles, std::true_type{}, std::true_type{});
+    run_tiles(j0, jlo, MaskBoth{}, std::false_type{});
+    run_tiles(jlo, max(jlo, nfull), NoMask{}, std::false_type{});
+    run_tiles(max(jlo, nfull), ntiles, MaskCausal{}, std::true_type{});
   } else {
-    run_tiles_ns(j0, jlo, std::true_type{});
-    run_tiles_ns(jlo, max(jlo, nfull), std::false_type{});
-    run_tiles_ns(max(jlo, nfull), ntiles, std::true_type{});
+    run_tiles_ns(j0, jlo, MaskBoth{});
+    run_tiles_ns(jlo, max(jlo, nfull), NoMask{});
+    run_tiles_ns(max(jlo, nfull), ntiles, MaskCausal{});
   }
 
   // ---- epilogue: normalise, round to bf16, store rows of this tile
