@@ -202,8 +202,10 @@ __global__ __launch_bounds__(256, 3) void attn_fp8_kernel(
     }
   };
 
+  // MASK: 0 none, 1 keys past the row's position (tiles reaching past the
+  // item's smallest position), 2 also keys below kv_lo (the tile holding it)
   auto tile = [&](int j, auto mask_tag) {
-    constexpr bool MASK = decltype(mask_tag)::value;
+    constexpr int MASK = decltype(mask_tag)::value;
     const uint8_t* ks = kmem[j & 1];
     const uint16_t* vs = vmem[j & 1];
     f32x16 s[HPW][1];
@@ -239,12 +241,16 @@ __global__ __launch_bounds__(256, 3) void attn_fp8_kernel(
       float f[2];
 #pragma unroll
       for (int b = 0; b < 2; ++b) f[b] = qs[i] * tks[b] * scale_log2e;
-      if constexpr (MASK) {
-        const int kbase = j * kKT;
+      if constexpr (MASK != 0) {
+        // score r holds key j kKT + 8 (r / 4) + 4 lh + r % 4: compare its
+        // in-tile offset with the row's bounds moved to the same origin
+        const int dhi = pos - 4 * lh - j * kKT;
+        const int dlo = it.kv_lo - 4 * lh - j * kKT;
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const int key = kbase + 8 * (r >> 2) + 4 * lh + (r & 3);
-          s[i][0][r] = (key > pos || key < it.kv_lo) ? -INFINITY : s[i][0][r];
+          const int off = 8 * (r >> 2) + (r & 3);
+          const bool out = MASK == 2 ? (off > dhi || off < dlo) : off > dhi;
+          s[i][0][r] = out ? -INFINITY : s[i][0][r];
         }
       }
       float mb[2];
@@ -327,9 +333,9 @@ __global__ __launch_bounds__(256, 3) void attn_fp8_kernel(
     }
   };
   const int jl = min(ntiles, max(j0, jlo));
-  run_tiles(j0, jl, std::true_type{});
-  run_tiles(jl, max(jl, nfull), std::false_type{});
-  run_tiles(max(jl, nfull), ntiles, std::true_type{});
+  run_tiles(j0, jl, std::integral_constant<int, 2>{});
+  run_tiles(jl, max(jl, nfull), std::integral_constant<int, 0>{});
+  run_tiles(max(jl, nfull), ntiles, std::integral_constant<int, 1>{});
 
   // ---- epilogue
 #pragma unroll
