@@ -221,6 +221,22 @@ def test_local_miss_scope_large(name):
     assert run.pool_after_attn_ok
 
 
+@pytest.mark.slow
+@pytest.mark.parametrize("G", [1, 2])
+def test_row_blocks_small_groups(G):
+    """Three row blocks per workgroup with fewer than four query heads per KV
+    head (spare waves compute a duplicate head and store nothing): a
+    two-request RAG-shaped batch, every row of sampled KV heads checked."""
+    cfg = workloads.get_config("rag8b")
+    shape = cfg.model.__class__(**{**vars(cfg.model), "n_q_heads": cfg.model.n_kv_heads * G})
+    wl = workloads.make_workload(cfg.with_(model=shape, n_requests=2))
+    run = GpuRun(wl)
+    assert run.plan.attn_rows_per_item == 96
+    rng = np.random.default_rng(41 + G)
+    for r in range(len(wl.requests)):
+        check_request(run, r, kv_heads=sorted(rng.choice(shape.n_kv_heads, 2, replace=False).tolist()))
+
+
 @pytest.mark.parametrize("name", ["small_bf16", "small_fp8", "small_f32"])
 def test_host_tier_pool(name):
     """The pool in pinned host memory (the host tier): compose gathers cached
