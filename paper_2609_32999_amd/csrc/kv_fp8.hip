@@ -91,6 +91,10 @@ __global__ __launch_bounds__(256) void page_fp8_kernel(
   // unit u: pair-chunk c (dims 8c.. and 64+8c..), slot s, head h
   float kv[U][16];
   float amax_k = 0.0f, amax_v = 0.0f;
+  // a thread's units share their chunk and, for pages of at most 32 slots,
+  // their slot: the cos/sin row is then loaded once
+  float cs[8], sn[8];
+  const bool one_slot = log2_page <= 5;
   uint4 vraw[U][2];         // V source: e4m3 codes (compose, low 8 bytes) or bf16
 #pragma unroll
   for (int k = 0; k < U; ++k) {
@@ -127,9 +131,10 @@ __global__ __launch_bounds__(256) void page_fp8_kernel(
       for (int i = 0; i < 16; ++i) amax_v = fmaxf(amax_v, fabsf(v[i]));
     }
     if constexpr (MODE != kFpRetain) {
-      float cs[8], sn[8];
-      load8(rope_cos + (int64_t)(pd.pos + s) * (kD8 / 2) + 8 * c, cs);
-      load8(rope_sin + (int64_t)(pd.pos + s) * (kD8 / 2) + 8 * c, sn);
+      if (k == 0 || !one_slot) {
+        load8(rope_cos + (int64_t)(pd.pos + s) * (kD8 / 2) + 8 * c, cs);
+        load8(rope_sin + (int64_t)(pd.pos + s) * (kD8 / 2) + 8 * c, sn);
+      }
       rope_rotate<8>(x, x + 8, cs, sn);
     }
 #pragma unroll
