@@ -83,3 +83,22 @@ def test_alias_v_equals_composed_path(name, over):
         assert bool(is_sentinel(run.sess.req_v[0, rp]).all()), (r, pg)
     for r in range(len(wl.requests)):
         check_request(run, r, check_kv=False)
+
+
+@pytest.mark.slow
+def test_alias_v_three_row_blocks():
+    """V aliasing under the twelve-wave attention (96-row items): a
+    two-request RAG-shaped batch, bit-equal to the composed path, one sampled
+    KV head of each request against the oracle."""
+    wl = workloads.make_workload(workloads.get_config("rag8b").with_(n_requests=2))
+    pages = aliased_pages(wl)
+    say(f"[gpu] alias_v: workload={wl.name} seed={wl.seed} aliased pages={len(pages)}")
+    ref = Run(wl, False)
+    run = Run(wl, True)
+    assert run.plan.attn_rows_per_item == 96
+    assert run.plan.num_aliased_pages == len(pages) > 0
+    assert torch.equal(run.out.view(torch.int16), ref.out.view(torch.int16))
+    assert torch.equal(run.lse.view(torch.int32), ref.lse.view(torch.int32))
+    rng = np.random.default_rng(43)
+    for r in range(len(wl.requests)):
+        check_request(run, r, kv_heads=[int(rng.integers(wl.model.n_kv_heads))], check_kv=False)
