@@ -9,11 +9,13 @@
 //
 // Two kernels:
 //   attn_f32_kernel   fp32 reference mode, scalar, one workgroup per item.
-//   attn_mfma_kernel  bf16 mode.  Work item = up to 32 consecutive computed
-//                     rows of one request x one KV head; the G query heads of
-//                     that KV head are packed into the workgroup (wave w owns
-//                     heads w, w+4, ...), so every K/V tile staged in LDS feeds
-//                     all of them.  Per 32-key tile (K loaded straight into
+//   attn_mfma_kernel  bf16 mode.  Work item = R row blocks of up to 32
+//                     consecutive computed rows of one request x one KV head
+//                     (R = 1 or 3, chosen per plan); the query heads of that
+//                     KV head are packed into the workgroup (four waves per
+//                     row block, one head each; G = 8 takes two items), so
+//                     every K/V tile staged in LDS feeds all of them.  Per
+//                     32-key tile (K loaded straight into
 //                     LDS, V staged through registers as V^T in fp16):
 //                       S^T = K Q^T        v_mfma_f32_32x32x16_bf16
 //                       online softmax     fp32, exp2 with folded scale
@@ -23,8 +25,9 @@
 //                     exchange between the two half-waves.  P and V enter the
 //                     second product as fp16 (bf16 P would cost ~2e-3
 //                     relative error; fp16 keeps it near 2e-4).  A wave
-//                     holds under 168 registers and a workgroup 36 KB of
-//                     LDS, so three waves share each SIMD.
+//                     holds 168 registers and a workgroup 36 KB of LDS, so
+//                     three waves share each SIMD: three 4-wave workgroups or
+//                     one 12-wave workgroup per CU.
 #include <cmath>
 #include <type_traits>
 
