@@ -214,6 +214,9 @@ __global__ __launch_bounds__(256 * R, 3) void attn_mfma_kernel(
   // double-buffered K and V^T tiles
   __shared__ __attribute__((aligned(16))) uint8_t kl[2][kKBytes];
   __shared__ __attribute__((aligned(16))) uint16_t vl[2][kVBytes / 2];
+  // cos (dims 0 .. d/2-1) and sin (d/2 ..) at each row's position, per row
+  // block: loaded once and shared by the block's four head waves
+  __shared__ __attribute__((aligned(16))) float rl[R][kTileRows][kD];
 
   const AttnItem it = items[blockIdx.x];
   if (it.n_rows == 0) return;
@@ -459,33 +462,57 @@ __global__ __launch_bounds__(256 * R, 3) void attn_mfma_kernel(
     load_tile(j0, pid, kl[j0 & 1]);
     pid = fetch_pages(j0 + 1);
   }
-  // the rotated queries are built while the first tile is in flight
-  // ---- rotated queries as bf16 B operands: lane = query row, k = head dim
+  // While the first tile is in flight: each row block's cos/sin rows go to
+  // LDS (thread t of the block loads 8 dims of cos and sin of row t / 8)
+  // and every wave loads its raw queries; the rotation follows the barrier.
+  {
+    const int t = tid & 255, lr = t >> 3, c8 = 8 * (t & 7);
+    const int ppos = rows[it.row0 + min(rbase + lr, it.n_rows - 1)].pos;
+    float c[8], sn[8];
+    load8(rope_cos + (int64_t)ppos * (kD / 2) + c8, c);
+    load8(rope_sin + (int64_t)ppos * (kD / 2) + c8, sn);
+    store8(&rl[rb][lr][c8], c);
+    store8(&rl[rb][lr][kD / 2 + c8], sn);
+  }
+  uint4 qraw[8];
   {
     const uint16_t* qp = q + ((int64_t)row * n_q_heads + g * G + hl) * kD;
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
       const int d0 = 16 * ks + 8 * lh;
-      float lo[8], hi[8], c[8], s[8];
-      load8(qp + d0, lo);
-      load8(qp + d0 + kD / 2, hi);
-      load8(rope_cos + (int64_t)pos * (kD / 2) + d0, c);
-      load8(rope_sin + (int64_t)pos * (kD / 2) + d0, s);
-      rope_rotate<8>(lo, hi, c, s);
-      Frag a, b;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        a.w[e] = f32_to_bf16(lo[2 * e]) | (f32_to_bf16(lo[2 * e + 1]) << 16);
-        b.w[e] = f32_to_bf16(hi[2 * e]) | (f32_to_bf16(hi[2 * e + 1]) << 16);
-      }
-      qf[ks] = a.b;
-      qf[ks + 4] = b.b;
+      qraw[ks] = *reinterpret_cast<const uint4*>(qp + d0);
+      qraw[ks + 4] = *reinterpret_cast<const uint4*>(qp + d0 + kD / 2);
     }
   }
-
   if (stager) store_tile(vl[j0 & 1]);
   __builtin_amdgcn_s_waitcnt(kWaitVm0);
   __syncthreads();
+  // ---- rotated queries as bf16 B operands: lane = query row, k = head dim
+#pragma unroll
+  for (int ks = 0; ks < 4; ++ks) {
+    const int d0 = 16 * ks + 8 * lh;
+    float lo[8], hi[8], c[8], sn[8];
+    const uint32_t wl[4] = {qraw[ks].x, qraw[ks].y, qraw[ks].z, qraw[ks].w};
+    const uint32_t wh[4] = {qraw[ks + 4].x, qraw[ks + 4].y, qraw[ks + 4].z, qraw[ks + 4].w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      lo[2 * e] = bf16_to_f32(wl[e] & 0xffffu);
+      lo[2 * e + 1] = bf16_to_f32(wl[e] >> 16);
+      hi[2 * e] = bf16_to_f32(wh[e] & 0xffffu);
+      hi[2 * e + 1] = bf16_to_f32(wh[e] >> 16);
+    }
+    load8(&rl[rb][lrow][d0], c);
+    load8(&rl[rb][lrow][kD / 2 + d0], sn);
+    rope_rotate<8>(lo, hi, c, sn);
+    Frag a, b;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      a.w[e] = f32_to_bf16(lo[2 * e]) | (f32_to_bf16(lo[2 * e + 1]) << 16);
+      b.w[e] = f32_to_bf16(hi[2 * e]) | (f32_to_bf16(hi[2 * e + 1]) << 16);
+    }
+    qf[ks] = a.b;
+    qf[ks + 4] = b.b;
+  }
   if (stager) {
     run_tiles(j0, jlo, MaskBoth{}, std::false_type{});
     run_tiles(jlo, max(jlo, nfull), NoMask{}, std::false_type{});
