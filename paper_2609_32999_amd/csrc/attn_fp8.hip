@@ -65,6 +65,9 @@ __global__ __launch_bounds__(256, 3) void attn_fp8_kernel(
   constexpr int HPW = 1;  // query heads per wave
   __shared__ __attribute__((aligned(16))) uint8_t kmem[2][kKBytes];
   __shared__ __attribute__((aligned(16))) uint16_t vmem[2][kVElems];
+  // cos (dims 0 .. d/2-1) and sin (d/2 ..) at each row's position, loaded
+  // once and shared by the four head waves
+  __shared__ __attribute__((aligned(16))) float rl[32][kD];
 
   const AttnItem it = items[blockIdx.x];
   if (it.n_rows == 0) return;
@@ -78,6 +81,16 @@ __global__ __launch_bounds__(256, 3) void attn_fp8_kernel(
   const int32_t* bt = bts + it.bt_off;
   const int row = it.row0 + min(lrow, it.n_rows - 1);
   const int pos = rows[row].pos;
+  {
+    const int lr = tid >> 3, c8 = 8 * (tid & 7);
+    const int ppos = rows[it.row0 + min(lr, it.n_rows - 1)].pos;
+    float c[8], sn[8];
+    load8(rope_cos + (int64_t)ppos * (kD / 2) + c8, c);
+    load8(rope_sin + (int64_t)ppos * (kD / 2) + c8, sn);
+    store8(&rl[lr][c8], c);
+    store8(&rl[lr][kD / 2 + c8], sn);
+  }
+  __syncthreads();
 
   // ---- queries: rotate in fp32, quantize per (row, head) to e4m3.  Lane
   // half lh holds dims [32 lh, 32 lh + 32) of both RoPE halves, i.e. the
@@ -97,8 +110,8 @@ __global__ __launch_bounds__(256, 3) void attn_fp8_kernel(
       float cs[8], sn[8];
       load8(qp + d0, lo + 8 * c);
       load8(qp + d0 + kD / 2, hi + 8 * c);
-      load8(rope_cos + (int64_t)pos * (kD / 2) + d0, cs);
-      load8(rope_sin + (int64_t)pos * (kD / 2) + d0, sn);
+      load8(&rl[lrow][d0], cs);
+      load8(&rl[lrow][kD / 2 + d0], sn);
       rope_rotate<8>(lo + 8 * c, hi + 8 * c, cs, sn);
     }
     float amax = 0.0f;
