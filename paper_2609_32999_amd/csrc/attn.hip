@@ -215,8 +215,10 @@ __global__ __launch_bounds__(256 * R, 3) void attn_mfma_kernel(
   __shared__ __attribute__((aligned(16))) uint8_t kl[2][kKBytes];
   __shared__ __attribute__((aligned(16))) uint16_t vl[2][kVBytes / 2];
   // cos (dims 0 .. d/2-1) and sin (d/2 ..) at each row's position, per row
-  // block: loaded once and shared by the block's four head waves
-  __shared__ __attribute__((aligned(16))) float rl[R][kTileRows][kD];
+  // block: loaded once and shared by the block's four head waves (rows
+  // padded by 4 floats so that the 32 rows of a fragment read fall in
+  // different banks)
+  __shared__ __attribute__((aligned(16))) float rl[R][kTileRows][kD + 4];
 
   const AttnItem it = items[blockIdx.x];
   if (it.n_rows == 0) return;

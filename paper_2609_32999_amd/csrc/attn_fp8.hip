@@ -66,8 +66,9 @@ __global__ __launch_bounds__(256, 3) void attn_fp8_kernel(
   __shared__ __attribute__((aligned(16))) uint8_t kmem[2][kKBytes];
   __shared__ __attribute__((aligned(16))) uint16_t vmem[2][kVElems];
   // cos (dims 0 .. d/2-1) and sin (d/2 ..) at each row's position, loaded
-  // once and shared by the four head waves
-  __shared__ __attribute__((aligned(16))) float rl[32][kD];
+  // once and shared by the four head waves (rows padded by 4 floats so
+  // that the 32 rows of a fragment read fall in different banks)
+  __shared__ __attribute__((aligned(16))) float rl[32][kD + 4];
 
   const AttnItem it = items[blockIdx.x];
   if (it.n_rows == 0) return;
