@@ -116,8 +116,9 @@ class Workload:
         Codes are torch's e4m3fn encoding of N(0,1)/scale draws clamped to the
         finite range, so code * scale is distributed like N(0,1).  As in any
         pool written by the retention quantizer, each page's scale is the
-        smallest power of two that covers the page: the first element of
-        every page holds the largest finite code (+448).
+        smallest power of two that covers the page: one element of every
+        page, at a seeded random (slot, head, dim) among its valid slots and
+        with a random sign, holds the largest finite magnitude (448).
         """
         m = self.model
         n = int(self.unit_len[unit_id])
@@ -132,7 +133,13 @@ class Workload:
             tok_scale = np.repeat(scale, m.page_size)[:n]
             x = np.clip(x / tok_scale[:, None, None], -448.0, 448.0)
             codes = torch.from_numpy(x).to(torch.float8_e4m3fn).view(torch.uint8).numpy()
-            codes[::m.page_size, 0, 0] = 0x7E
+            B = m.page_size
+            for pg in range(pages):
+                nv = min(B, n - pg * B)
+                j = pg * B + int(srng.integers(nv))
+                h = int(srng.integers(m.n_kv_heads))
+                d = int(srng.integers(m.head_dim))
+                codes[j, h, d] = 0xFE if srng.integers(2) else 0x7E   # -448 / +448
             out.append((codes, scale))
         (kc, ks), (vc, vs) = out
         return kc, vc, ks, vs
