@@ -48,7 +48,7 @@
 extern "C" {
 #endif
 
-#define TSR_ABI_VERSION 3
+#define TSR_ABI_VERSION 4
 
 typedef enum {
   TSR_OK = 0,
@@ -89,8 +89,17 @@ typedef enum { TSR_SCOPE_GLOBAL = 0, TSR_SCOPE_LOCAL = 1 } tsr_miss_scope;
  *   (every request page has one writer: segments start on page boundaries
  *   and end on one or at the prompt's end; recompute windows are whole
  *   pages or the whole unit), else tsr_plan_create returns UNSUPPORTED.
- *   RoPE pairs dimension i with i + head_dim/2 at frequency
- *   rope_theta^(-2i/head_dim) (Section 2.2; the variant is a reading).
+ *   RoPE (Section 2.2 names rotary encoding but not its dimension pairing,
+ *   so the pairing is a field):
+ *     rope_interleaved = 0  dimension i is paired with i + head_dim/2
+ *                           (the half-split pairing of Llama-family
+ *                           weights) at frequency rope_theta^(-2i/head_dim);
+ *     rope_interleaved = 1  dimensions 2i and 2i+1 are paired (GPT-J
+ *                           style).  Not implemented: tsr_plan_create and
+ *                           tsr_rope_table_bytes refuse it (UNSUPPORTED /
+ *                           0), so such a model is rejected, not run with
+ *                           the wrong pairing.
+ *     any other value       INVALID_ARG.
  *   Positions must be < max_position (the RoPE table's length).
  *   softmax_scale == 0 selects 1/sqrt(head_dim). */
 typedef struct {
@@ -101,6 +110,7 @@ typedef struct {
   int32_t kv_dtype;
   int32_t act_dtype;
   double rope_theta;
+  int32_t rope_interleaved;
   int32_t max_position;
   float softmax_scale;
 } tsr_model;
@@ -310,7 +320,13 @@ tsr_status tsr_compose_kv(const tsr_plan* plan, const void* pool_k,
  * enter the PV product as fp16 (|v| must stay below 65504).
  * e4m3: computed pages are quantized like composed ones (k after rotation);
  * q_rot is quantized per (row, head) to e4m3 with the smallest power-of-two
- * scale covering the row, QK^T runs in fp8 MFMA, PV in fp16 MFMA. */
+ * scale covering the row, QK^T runs in fp8 MFMA, PV in fp16 MFMA.
+ * Errors: every argument check runs before the first launch, so a status
+ * other than TSR_ERR_DEVICE means nothing was enqueued.  The call enqueues
+ * two kernels, append then attention; if the HIP runtime reports a failure
+ * of the second launch, the append stays enqueued (the request pages
+ * receive the computed rows' K/V, out and lse are not written) and
+ * TSR_ERR_DEVICE is returned. */
 tsr_status tsr_prefill_attn(const tsr_plan* plan, const void* q,
                             const void* k, const void* v, void* req_k,
                             void* req_v, float* req_scale, void* out,
@@ -448,28 +464,6 @@ tsr_status tsr_copy_blocks(void* dst, int32_t n_dst_blocks, const int32_t* dst_b
                            const int32_t* src_blocks, int32_t n, int64_t block_bytes,
                            int32_t n_layers, int64_t dst_layer_stride,
                            int64_t src_layer_stride, void* stream);
-
-/* ------------------------------------------------- measurement aids */
-/* Not part of the composed-prefill path and not taken from the paper: two
- * kernels that show the rates the running GPU sustains, which the benchmark
- * reports next to the published peaks (the matrix cores hold a lower clock
- * under load than the one the published figures assume).
- *
- * tsr_peak_mfma: n_workgroups workgroups of 256 threads each issue
- *   iters x 8 back-to-back v_mfma_f32_32x32x16_bf16 per wave on register
- *   operands (eight independent accumulators, no memory traffic in the
- *   loop); tsr_peak_mfma_flops gives the launch's FLOP count (0 for
- *   non-positive arguments).  dev_out: device buffer of n_workgroups * 256
- *   floats (owned by the caller) that receives per-thread sums, so that the
- *   products are not optimised away.  INVALID_ARG for non-positive sizes or
- *   a NULL buffer; DEVICE if the launch fails.
- * tsr_peak_copy: dst[0, bytes) <- src[0, bytes) with 16-byte loads and
- *   stores by a grid-stride kernel.  Both pointers device memory, 16-byte
- *   aligned, not overlapping; bytes a positive multiple of 16, else
- *   INVALID_ARG. */
-int64_t tsr_peak_mfma_flops(int32_t n_workgroups, int32_t iters);
-tsr_status tsr_peak_mfma(int32_t n_workgroups, int32_t iters, float* dev_out, void* stream);
-tsr_status tsr_peak_copy(void* dst, const void* src, size_t bytes, void* stream);
 
 /* Thread-local message of the last failure on this thread ("" if none). */
 const char* tsr_last_error(void);

@@ -62,8 +62,8 @@ class tsr_model(ctypes.Structure):
     _fields_ = [("n_q_heads", c_int32), ("n_kv_heads", c_int32),
                 ("head_dim", c_int32), ("page_size", c_int32),
                 ("kv_dtype", c_int32), ("act_dtype", c_int32),
-                ("rope_theta", c_double), ("max_position", c_int32),
-                ("softmax_scale", c_float)]
+                ("rope_theta", c_double), ("rope_interleaved", c_int32),
+                ("max_position", c_int32), ("softmax_scale", c_float)]
 
 
 class tsr_unit(ctypes.Structure):
@@ -222,10 +222,11 @@ def tsr_last_error() -> str:
 
 def make_model(n_q_heads, n_kv_heads, head_dim, page_size=16, kv_dtype="bf16",
                act_dtype="bf16", rope_theta=500000.0, max_position=65536,
-               softmax_scale=0.0) -> tsr_model:
+               softmax_scale=0.0, rope_interleaved=0) -> tsr_model:
     return tsr_model(n_q_heads, n_kv_heads, head_dim, page_size,
                      DTYPE_CODES[kv_dtype], DTYPE_CODES[act_dtype],
-                     float(rope_theta), max_position, float(softmax_scale))
+                     float(rope_theta), int(rope_interleaved), max_position,
+                     float(softmax_scale))
 
 
 class RequestBatch:

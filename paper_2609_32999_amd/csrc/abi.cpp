@@ -316,6 +316,9 @@ tsr_status tsr_prefill_attn(const tsr_plan* p, const void* q, const void* k,
       set_error("the plan reads V from the pool: use tsr_append_kv and tsr_attn_aliased");
       return TSR_ERR_INVALID_ARG;
     }
+    // Every check is above: from here on only a launch failure reported by
+    // the runtime can fail the call (append then stays enqueued if the
+    // attention launch is the one that fails).
     hipStream_t s = static_cast<hipStream_t>(stream);
     hipError_t e = is_e4m3(p) ? launch_append_e4m3(p, k, v, req_k, req_v, req_scale, s)
                               : launch_append(p, k, v, req_k, req_v, s);

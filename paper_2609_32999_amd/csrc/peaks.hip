@@ -7,6 +7,7 @@
 
 #include "kernels_common.h"
 #include "tsr_internal.h"
+#include "../../include/tsr_measure.h"
 
 namespace tsr {
 

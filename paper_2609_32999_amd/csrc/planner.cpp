@@ -51,6 +51,12 @@ tsr_status check_model(const tsr_model* m) {
     return fail(TSR_ERR_UNSUPPORTED, "page_size must be a power of two in [8, 64]");
   if (!(m->rope_theta > 0.0) || !std::isfinite(m->rope_theta))
     return fail(TSR_ERR_INVALID_ARG, "rope_theta must be positive and finite");
+  if (m->rope_interleaved != 0 && m->rope_interleaved != 1)
+    return fail(TSR_ERR_INVALID_ARG, "rope_interleaved must be 0 or 1");
+  if (m->rope_interleaved == 1)
+    return fail(TSR_ERR_UNSUPPORTED,
+                "interleaved RoPE pairing (2i, 2i+1) is not implemented; only the "
+                "half-split pairing (i, i + head_dim/2) is");
   if (m->max_position <= 0 || m->max_position > (1 << 20))
     return fail(TSR_ERR_INVALID_ARG, "max_position must be in [1, 2^20]");
   if (!(m->softmax_scale >= 0.0f) || !std::isfinite(m->softmax_scale))

@@ -42,7 +42,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_abi_version():
-    assert P.tsr_abi_version() == 3
+    assert P.tsr_abi_version() == 4
 
 
 @pytest.mark.parametrize("name", ["tiny", "small_bf16", "small_f32", "small_bf16_g8",
@@ -181,6 +181,21 @@ def test_rejects_unsupported_shapes():
             act_dtype="bf16")           # tiny has head_dim 64
     _expect(P._binding.TSR_ERR_OUT_OF_RANGE, wl, [r], "max_position", max_position=100)
     _expect(P._binding.TSR_ERR_INVALID_ARG, wl, [r], "multiple", n_q_heads=6)
+
+
+def test_rope_pairing_field():
+    """The model names its RoPE pairing (Section 2.2 leaves it open): the
+    half-split pairing runs, the interleaved one is refused rather than run
+    with the wrong pairing, and any other value is malformed."""
+    wl, r = _tiny_req()
+    _plan(wl, [r], rope_interleaved=0)
+    _expect(P._binding.TSR_ERR_UNSUPPORTED, wl, [r], "interleaved", rope_interleaved=1)
+    _expect(P._binding.TSR_ERR_INVALID_ARG, wl, [r], "rope_interleaved", rope_interleaved=2)
+    _expect(P._binding.TSR_ERR_INVALID_ARG, wl, [r], "rope_interleaved", rope_interleaved=-1)
+    assert P.tsr_rope_table_bytes(_model(wl, rope_interleaved=1)) == 0
+    with pytest.raises(P.TsrError, match="interleaved"):     # size 0: refused
+        P.tsr_plan_workspace_size(_model(wl, rope_interleaved=1), P.RequestBatch([r]),
+                                  wl.n_pool_pages, wl.n_req_pages)
 
 
 def test_rejects_bad_unit_fields():
