@@ -18,16 +18,20 @@
 //                     32-key tile (K loaded straight into
 //                     LDS, V staged through registers as V^T in fp16):
 //                       S^T = K Q^T        v_mfma_f32_32x32x16_bf16
-//                       online softmax     fp32, exp2 with folded scale
+//                       online softmax     fp32, exp2 with folded scale;
+//                                          the running max moves only when
+//                                          a tile's probability sum says so
 //                       O^T += V^T P^T     v_mfma_f32_32x32x16_f16
 //                     Keeping S and O transposed gives every lane one query
 //                     row, so row statistics are lane-local except for one
 //                     exchange between the two half-waves.  P and V enter the
 //                     second product as fp16 (bf16 P would cost ~2e-3
 //                     relative error; fp16 keeps it near 2e-4).  A wave
-//                     holds 168 registers and a workgroup 36 KB of LDS, so
-//                     three waves share each SIMD: three 4-wave workgroups or
-//                     one 12-wave workgroup per CU.
+//                     holds at most 168 registers, so three waves share each
+//                     SIMD.  LDS per workgroup: 36 KB of K/V tiles plus
+//                     16.5 KB of cos/sin rows per row block, 52.5 KB with
+//                     one row block (three 4-wave workgroups per CU) and
+//                     85.5 KB with three (one 12-wave workgroup per CU).
 #include <cmath>
 #include <type_traits>
 
@@ -165,6 +169,7 @@ constexpr int kWaitVm0 = 0x0F70;
 // Lazy rescale threshold (log2 units): P may grow to 2^kLazy before the
 // running max is moved.
 constexpr float kLazy = 8.0f;
+constexpr float kLazySum = 256.0f;   // 2^kLazy
 
 // Direct global->LDS load of 16 bytes per lane: lane l's bytes land at LDS
 // address lds + 16 l (lds wave-uniform).  Written as assembly so that the
@@ -369,42 +374,61 @@ __global__ __launch_bounds__(256 * R, 3) void attn_mfma_kernel(
         s[r] = out ? -INFINITY : s[r];
       }
     }
-    // Online softmax with a lazily updated running max: the max (and with
-    // it O and l) is only rescaled when a row's tile max exceeds it by more
-    // than 2^kLazy in probability units, so P stays <= 2^kLazy (exact range
-    // for fp16) and the rescale is skipped almost always.  Each half-wave
-    // holds half of every row's keys: the halves exchange their maxima only
-    // on the rescale path.
-    float mt = -INFINITY;
+    // Online softmax with a lazily updated running max m, common to the
+    // row's two half-waves.  P = exp2(s c - m c) is computed against the
+    // current m and its per-lane sum checked: while the sum stays <= 2^kLazy
+    // (so every P <= 2^kLazy, an exact range for fp16) no maximum is taken
+    // and nothing is rescaled.  Otherwise (or while m is still -inf) the
+    // tile's scores are computed again from the K tile in LDS, the maximum
+    // moves m, O and l are rescaled, and P is recomputed.
+    const float mc = m == -INFINITY ? 0.0f : m * scale_log2e;
+    float ls[4];
 #pragma unroll
-    for (int r = 0; r < 16; ++r) mt = fmaxf(mt, s[r]);
-    const bool grow = mt * scale_log2e > m * scale_log2e + kLazy;
-    if (__builtin_amdgcn_ballot_w64(grow)) {
+    for (int r = 0; r < 16; ++r) s[r] = __builtin_amdgcn_exp2f(fmaf(s[r], scale_log2e, -mc));
+#pragma unroll
+    for (int r = 0; r < 4; ++r) ls[r] = (s[r] + s[r + 4]) + (s[r + 8] + s[r + 12]);
+    float lt = (ls[0] + ls[1]) + (ls[2] + ls[3]);
+    if (__builtin_amdgcn_ballot_w64(!(lt <= kLazySum) || m == -INFINITY)) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) s[r] = 0.0f;
+#pragma unroll
+      for (int kst = 0; kst < 8; ++kst) {
+        Frag a;
+        a.u = *reinterpret_cast<const uint4*>(ks + kst * kKBlk + lane * 16);
+        s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a.b, qf[kst], s, 0, 0, 0);
+      }
+      if constexpr (MASK != kNoMask) {
+        const int dhi = pos_l - j * kKT;
+        const int dlo = it.kv_lo - 4 * lh - j * kKT;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int off = 8 * (r >> 2) + (r & 3);
+          const bool out = MASK == kMaskBoth ? (off > dhi || off < dlo) : off > dhi;
+          s[r] = out ? -INFINITY : s[r];
+        }
+      }
+      float mt = -INFINITY;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) mt = fmaxf(mt, s[r]);
       const float mn = fmaxf(m, fmaxf(mt, __shfl_xor(mt, 32)));
-      const float alpha = __builtin_amdgcn_exp2f((m - mn) * scale_log2e);
+      const float alpha = mn == -INFINITY ? 1.0f : __builtin_amdgcn_exp2f((m - mn) * scale_log2e);
       m = mn;
       l *= alpha;
 #pragma unroll
       for (int db = 0; db < 4; ++db)
 #pragma unroll
         for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
-    }
-    // a half with no visible key yet leaves m at -inf (all its scores are
-    // -inf too): exponentiate against 0 so that P = 0, not NaN
-    const float mc = m == -INFINITY ? 0.0f : m * scale_log2e;
+      const float mc2 = m == -INFINITY ? 0.0f : m * scale_log2e;
 #pragma unroll
-    for (int r = 0; r < 16; ++r) s[r] = __builtin_amdgcn_exp2f(fmaf(s[r], scale_log2e, -mc));
+      for (int r = 0; r < 16; ++r) s[r] = __builtin_amdgcn_exp2f(fmaf(s[r], scale_log2e, -mc2));
+#pragma unroll
+      for (int r = 0; r < 4; ++r) ls[r] = (s[r] + s[r + 4]) + (s[r + 8] + s[r + 12]);
+    }
     f16x8 pf[2];
 #pragma unroll
     for (int h = 0; h < 2; ++h)
 #pragma unroll
       for (int e = 0; e < 8; ++e) pf[h][e] = (_Float16)s[8 * h + e];
-    // O^T[d][row] += V^T[d][keys] P^T[keys][row], in program order (the
-    // scheduling barriers keep the compiler from serialising the fragment
-    // reads behind one register set): each MFMA of the first 16 keys frees
-    // its fragment registers for the matching fragment of the last 16, and
-    // the row sum (fp32, from the unrounded P, four independent chains) sits
-    // between the MFMAs of the second half.
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int db = 0; db < 4; ++db) {
@@ -412,12 +436,9 @@ __global__ __launch_bounds__(256 * R, 3) void attn_mfma_kernel(
       va[db].u = *reinterpret_cast<const uint4*>(vs + (32 * db + lrow) * kVStr + 16 + 8 * lh);
       __builtin_amdgcn_sched_barrier(0);
     }
-    float ls[4] = {s[0], s[1], s[2], s[3]};
 #pragma unroll
     for (int db = 0; db < 4; ++db) {
       o[db] = __builtin_amdgcn_mfma_f32_32x32x16_f16(va[db].h, pf[1], o[db], 0, 0, 0);
-#pragma unroll
-      for (int r = 4 + 3 * db; r < 7 + 3 * db; ++r) ls[r & 3] += s[r];
       __builtin_amdgcn_sched_barrier(0);
     }
     l += (ls[0] + ls[1]) + (ls[2] + ls[3]);

@@ -173,6 +173,13 @@ hipError_t launch_compose(const tsr_plan* p, const void* pool_k,
                           int64_t req_stride, hipStream_t s);
 hipError_t launch_append(const tsr_plan* p, const void* k, const void* v,
                          void* req_k, void* req_v, hipStream_t s);
+// compose + append of one layer in one launch
+hipError_t launch_assemble(const tsr_plan* p, const void* pool_k, const void* pool_v,
+                           const void* k, const void* v, void* req_k, void* req_v,
+                           hipStream_t s);
+hipError_t launch_assemble_e4m3(const tsr_plan* p, const void* pool_k, const void* pool_v,
+                                const float* pool_scale, const void* k, const void* v,
+                                void* req_k, void* req_v, float* req_scale, hipStream_t s);
 // Attention launchers run `n_items` items from `items` (a plan's full
 // schedule or one of its parts).
 hipError_t launch_attn(const tsr_plan* p, const AttnItem* items, int32_t n_items,
