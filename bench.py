@@ -24,9 +24,11 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBS = 8000.0
-PEAK_MFMA_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
+PEAK_MFMA_TFLOPS = {"bf16": 2500.0, "f32": 157.3, "fp8": 5000.0}
 # e4m3 KV: QK^T runs in fp8 MFMA (5.0 PFLOP/s dense) and PV in fp16 MFMA
-# (2.5 PFLOP/s), half of the FLOPs each: blended peak 1 / (0.5/5.0 + 0.5/2.5).
+# (2.5 PFLOP/s), half of the FLOPs each.  The fraction is reported against
+# the fp8 dense peak; the blend 1 / (0.5/5.0 + 0.5/2.5) of the two products'
+# peaks is a second, labelled field.
 PEAK_E4M3_BLEND = 1.0 / (0.5 / 5000.0 + 0.5 / 2500.0)
 
 
@@ -291,38 +293,12 @@ def host_tier_staged(torch, wl, reps=5, warmup=2):
 
 def alias_v_leg(torch, sess, wl, qs, ks, vs, out, lse, L, steps, warmup):
     """The same step with V aliasing (attention reads V of whole gathered
-    pages from the pool; compose writes only their K), timed like the main
-    step: compose, append, attention on one stream, layers rotating."""
+    pages from the pool; the assembly writes only their K), timed like the
+    main step without retention."""
     plan = sess.plan(wl.requests, alias_v=True)
-    main_s = torch.cuda.current_stream()
-    E = lambda: torch.cuda.Event(enable_timing=True)
-    ev = [[E() for _ in range(4)] for _ in range(steps)]
-
-    def step(i, rec=None):
-        l = i % L
-        if rec:
-            rec[0].record(main_s)
-        sess.compose(plan, layer=l, stream=main_s)
-        if rec:
-            rec[1].record(main_s)
-        sess.append(plan, ks[l], vs[l], layer=l, stream=main_s)
-        if rec:
-            rec[2].record(main_s)
-        sess.attn(plan, qs[l], out, lse, layer=l, stream=main_s)
-        if rec:
-            rec[3].record(main_s)
-
-    for i in range(warmup):
-        step(i)
-    torch.cuda.synchronize()
-    for i in range(steps):
-        step(i, ev[i])
-    torch.cuda.synchronize()
-    t = np.array([[e[0].elapsed_time(e[1]), e[2].elapsed_time(e[3]), e[0].elapsed_time(e[3])]
-                  for e in ev])
-    res = {"aliased_pages": plan.num_aliased_pages,
-           "compose_us": float(t[:, 0].mean() * 1e3), "attention_us": float(t[:, 1].mean() * 1e3),
-           "compose_append_attention_us": float(t[:, 2].mean() * 1e3)}
+    st, asm, att, _, _ = time_path(torch, sess, plan, qs, ks, vs, out, lse, L, steps, warmup)
+    res = {"aliased_pages": plan.num_aliased_pages, "assembly_us": dist(asm),
+           "attention_us": dist(att), "step_us": dist(st)}
     log(f"[bench] alias_v: {res}")
     return res
 
@@ -356,6 +332,199 @@ def control_plane_replay():
     return out
 
 
+def dist(ms_list):
+    """Event durations (ms) -> mean, median, p10, p90 in microseconds."""
+    a = np.asarray(ms_list, dtype=np.float64) * 1e3
+    if a.size == 0:
+        return {"mean": 0.0, "median": 0.0, "p10": 0.0, "p90": 0.0}
+    return {"mean": float(a.mean()), "median": float(np.median(a)),
+            "p10": float(np.percentile(a, 10)), "p90": float(np.percentile(a, 90))}
+
+
+def attention_flops(plan, m):
+    """4 d H_q per visible (row, key) pair: the method's attention work,
+    masked-out tile work excluded."""
+    pos, _ = plan.compute_positions()
+    kv_lo = plan.row_kv_lo()
+    visible = int((pos.astype(np.int64) - kv_lo + 1).sum())
+    return 4.0 * m.head_dim * m.n_q_heads * visible
+
+
+def attention_kernel_name(plan, m):
+    G = m.n_q_heads // m.n_kv_heads
+    return (f"attn_fp8_kernel<{G}>" if m.kv_dtype == "e4m3"
+            else f"attn_mfma_kernel<{G}, false, {plan.attn_rows_per_item // 32}>")
+
+
+def assembly_kernel_name(m):
+    # the e4m3 page kernel is instantiated for 2, 4 or 8 units per thread
+    units = m.page_size * m.n_kv_heads * 8
+    u = 2 if units <= 512 else 4 if units <= 1024 else 8
+    return (f"page_fp8_assemble_kernel<{u}>" if m.kv_dtype == "e4m3" else
+            f"kv_assemble_kernel<{m.head_dim}, unsigned short>")
+
+
+def attention_peaks(m):
+    """(peak used for the fraction, blended peak or None)."""
+    if m.kv_dtype == "e4m3":
+        return PEAK_MFMA_TFLOPS["fp8"], PEAK_E4M3_BLEND
+    return PEAK_MFMA_TFLOPS[m.act_dtype], None
+
+
+def time_path(torch, sess, plan, qs, ks, vs, out, lse, L, steps, warmup, side=None):
+    """The step: one assembly launch (compose + append) then attention on
+    the current stream, layers rotating over L buffer sets; with a side
+    stream, retention runs there concurrently with attention and is joined
+    at the end of the step.  Returns per-step durations (ms) of the step,
+    the assembly, attention and retention, and the wall time."""
+    main_s = torch.cuda.current_stream()
+    E = lambda: torch.cuda.Event(enable_timing=True)
+    evs = [[E() for _ in range(3)] for _ in range(steps)]
+    evr = [[E(), E()] for _ in range(steps)]
+
+    def step(i, rec=None, recr=None):
+        l = i % L
+        if rec:
+            rec[0].record(main_s)
+        sess.assemble(plan, ks[l], vs[l], layer=l, stream=main_s)
+        if rec:
+            rec[1].record(main_s)
+        if side is not None:
+            side.wait_stream(main_s)
+        sess.attn(plan, qs[l], out, lse, layer=l, stream=main_s)
+        if rec:
+            rec[2].record(main_s)
+        if side is not None:
+            # retain overlaps the MFMA-bound attention rather than competing
+            # with the assembly for HBM bandwidth
+            with torch.cuda.stream(side):
+                if recr:
+                    recr[0].record(side)
+                sess.retain(plan, ks[l], vs[l], layer=l, stream=side)
+                if recr:
+                    recr[1].record(side)
+            main_s.wait_stream(side)
+
+    for i in range(warmup):
+        step(i)
+    torch.cuda.synchronize()
+    end = E()
+    w0 = time.perf_counter()
+    for i in range(steps):
+        step(i, evs[i], evr[i])
+    end.record(main_s)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+    # a step lasts from its first event to the next step's (which follows the
+    # join of the side stream); the last one to the event after the loop
+    starts = [e[0] for e in evs] + [end]
+    step_ms = [starts[i].elapsed_time(starts[i + 1]) for i in range(steps)]
+    asm = [e[0].elapsed_time(e[1]) for e in evs]
+    att = [e[1].elapsed_time(e[2]) for e in evs]
+    ret = [e[0].elapsed_time(e[1]) for e in evr] if side is not None else []
+    return step_ms, asm, att, ret, wall
+
+
+def split_leg(torch, sess, plan, ks, vs, L, steps):
+    """compose then append as two launches, the unfused form of the
+    assembly (same bytes), for reference."""
+    main_s = torch.cuda.current_stream()
+    E = lambda: torch.cuda.Event(enable_timing=True)
+    ev = [[E() for _ in range(3)] for _ in range(steps)]
+    for i in range(4):
+        sess.compose(plan, layer=i % L, stream=main_s)
+        sess.append(plan, ks[i % L], vs[i % L], layer=i % L, stream=main_s)
+    for i in range(steps):
+        l = i % L
+        ev[i][0].record(main_s)
+        sess.compose(plan, layer=l, stream=main_s)
+        ev[i][1].record(main_s)
+        sess.append(plan, ks[l], vs[l], layer=l, stream=main_s)
+        ev[i][2].record(main_s)
+    torch.cuda.synchronize()
+    return {"compose_us": dist([e[0].elapsed_time(e[1]) for e in ev]),
+            "append_us": dist([e[1].elapsed_time(e[2]) for e in ev])}
+
+
+def local_leg(torch, sess, wl, qs, ks, vs, out, lse, L, steps, warmup):
+    """The same batch, pool and inputs under the LOCAL miss scope (missing
+    units' tokens past their recompute window attend within their unit):
+    a second plan, timed like the main step without retention."""
+    import workloads
+    wl_l = workloads.make_workload(wl.cfg.with_(miss_scope="local"))
+    plan = sess.plan(wl_l.requests)
+    m = wl.model
+    st, asm, att, _, _ = time_path(torch, sess, plan, qs, ks, vs, out, lse, L, steps, warmup)
+    flops = attention_flops(plan, m)
+    d_att = dist(att)
+    tf = flops / (d_att["mean"] * 1e-6) / 1e12
+    peak, blend = attention_peaks(m)
+    res = {"ms_per_step": float(np.mean(st)),
+           "value": wl.prompt_tokens / (np.mean(st) * 1e-3),
+           "kernel_us": {"assembly": dist(asm), "attention": d_att},
+           "roofline": {"bound": "mfma", "achieved": tf, "peak": peak, "unit": "TFLOP/s",
+                        "frac": tf / peak, "kernel": attention_kernel_name(plan, m),
+                        "flops_per_launch": flops}}
+    log(f"[bench] local scope: {res}")
+    return res
+
+
+def workload_leg(torch, name, steps, warmup, L=2):
+    """Another workload's assembly + attention step (no retention), with its
+    realized counts next to the sizes the configuration names."""
+    import workloads
+    from paper_2609_32999_amd import staging
+    from paper_2609_32999_amd.session import Session
+    from oracle import pipeline as PL
+    wl = workloads.generate(name)
+    m = wl.model
+    sess = Session(m, wl.n_pool_pages, wl.n_req_pages, n_layers=L)
+    staging.upload_pool(sess, wl, layer=0)
+    for l in range(1, L):
+        sess.pool_k[l].copy_(sess.pool_k[0])
+        sess.pool_v[l].copy_(sess.pool_v[0])
+        if sess.e4m3:
+            sess.pool_scale[l].copy_(sess.pool_scale[0])
+    plan = sess.plan(wl.requests)
+    q, k, v = staging.fresh_inputs(sess, wl, plan)
+    qs = [q] + [q.clone() for _ in range(L - 1)]
+    ks = [k] + [k.clone() for _ in range(L - 1)]
+    vs = [v] + [v.clone() for _ in range(L - 1)]
+    out, lse = sess.new_outputs(plan, with_lse=True)
+    st, asm, att, _, _ = time_path(torch, sess, plan, qs, ks, vs, out, lse, L, steps, warmup)
+    row_bytes = 2 * m.n_kv_heads * m.head_dim * kv_elem_bytes(m.kv_dtype)
+    T = plan.num_compute_tokens
+    asm_bytes = 2 * (plan.num_gather_tokens + T) * row_bytes
+    flops = attention_flops(plan, m)
+    d_asm, d_att = dist(asm), dist(att)
+    tf = flops / (d_att["mean"] * 1e-6) / 1e12
+    gbs = asm_bytes / (d_asm["mean"] * 1e-6) / 1e9
+    peak, blend = attention_peaks(m)
+    c = PL.counts(wl)
+    res = {"workload": f"{wl.name}: {wl.cfg.description}",
+           "ms_per_step": float(np.mean(st)),
+           "value": wl.prompt_tokens / (np.mean(st) * 1e-3),
+           "realized": {"requests": len(wl.requests), "prompt_tokens": wl.prompt_tokens,
+                        "computed_tokens": T, "gathered_tokens": plan.num_gather_tokens,
+                        "visible_pairs": c["visible_pairs"], "attention_flops": flops,
+                        "assembly_bytes": asm_bytes},
+           "kernel_us": {"assembly": d_asm, "attention": d_att},
+           "roofline": {"bound": "mfma", "achieved": tf, "peak": peak, "unit": "TFLOP/s",
+                        "frac": tf / peak, "kernel": attention_kernel_name(plan, m),
+                        "flops_per_launch": flops,
+                        "traffic": profiled_traffic(name, attention_kernel_name(plan, m))},
+           "roofline_assembly": {"bound": "hbm", "achieved": gbs, "peak": PEAK_HBM_GBS,
+                                 "unit": "GB/s", "frac": gbs / PEAK_HBM_GBS,
+                                 "kernel": assembly_kernel_name(m)}}
+    if blend:
+        res["roofline"]["frac_of_blend"] = tf / blend
+        res["roofline"]["blend_peak"] = blend
+    log(f"[bench] leg {name}: {res}")
+    del sess
+    torch.cuda.empty_cache()
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -368,6 +537,10 @@ def main():
                     help="miss scope: global (every missing-unit token attends to the "
                          "whole prompt) or local (missing units attend within themselves "
                          "past their recompute window)")
+    ap.add_argument("--legs", default="local,fp8rag",
+                    help="comma-separated extra legs reported in the same line: local "
+                         "(the batch under the LOCAL miss scope), fp8rag, agent8b, long70b "
+                         "(those workloads' assembly + attention); '' for none")
     ap.add_argument("--no-peaks", dest="peaks", action="store_false",
                     help="skip measuring the achievable copy and bf16 GEMM rates")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -380,6 +553,7 @@ def main():
                          "first (to scale HBM byte counters against a kernel of known "
                          "traffic)")
     args = ap.parse_args()
+    args.legs = [x for x in args.legs.split(",") if x]
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the path "
               "shards by request or KV head with no exchange, see DESIGN.md", file=sys.stderr)
@@ -428,63 +602,22 @@ def main():
 
     main_s = torch.cuda.current_stream()
     side = torch.cuda.Stream()
-    E = lambda: torch.cuda.Event(enable_timing=True)
-    n_ev = args.steps
-    evs = [[E() for _ in range(4)] for _ in range(n_ev)]
-    evr = [[E(), E()] for _ in range(n_ev)]
-
-    def step(i, rec=None, recr=None):
-        # main: compose -> append -> attention.  side: retain, started once
-        # append has been issued so that it overlaps the MFMA-bound attention
-        # rather than competing with compose for HBM bandwidth.
-        l = i % L
-        if rec:
-            rec[0].record(main_s)
-        sess.compose(plan, layer=l, stream=main_s)
-        if rec:
-            rec[1].record(main_s)
-        sess.append(plan, ks[l], vs[l], layer=l, stream=main_s)
-        if rec:
-            rec[2].record(main_s)
-        side.wait_stream(main_s)
-        sess.attn(plan, qs[l], out, lse, layer=l, stream=main_s)
-        if rec:
-            rec[3].record(main_s)
-        with torch.cuda.stream(side):
-            if recr:
-                recr[0].record(side)
-            sess.retain(plan, ks[l], vs[l], layer=l, stream=side)
-            if recr:
-                recr[1].record(side)
-        main_s.wait_stream(side)
-
-    for i in range(args.warmup):
-        step(i)
-    torch.cuda.synchronize()
-    log(f"[bench] warmup done ({args.warmup} steps)")
-    t_start, t_end = E(), E()
-    w0 = time.perf_counter()
-    t_start.record(main_s)
-    for i in range(args.steps):
-        step(i, evs[i], evr[i])
-    t_end.record(main_s)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - w0
-    total_ms = t_start.elapsed_time(t_end)
-    ms = total_ms / args.steps
-    compose_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
-    append_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
-    attn_ms = float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))
-    retain_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evr]))
+    step_ms, asm_ms, attn_ms, retain_ms, wall = time_path(
+        torch, sess, plan, qs, ks, vs, out, lse, L, args.steps, args.warmup, side=side)
+    ms = float(np.mean(step_ms))
+    d_asm, d_attn, d_ret = dist(asm_ms), dist(attn_ms), dist(retain_ms)
     log(f"[bench] timed {args.steps} steps: {ms:.3f} ms/step (wall {wall * 1e3 / args.steps:.3f}); "
-        f"compose {compose_ms * 1e3:.1f} us, append {append_ms * 1e3:.1f} us, "
-        f"attn {attn_ms * 1e3:.1f} us, retain {retain_ms * 1e3:.1f} us")
+        f"assembly {d_asm}, attn {d_attn}, retain {d_ret} (us)")
+
+    # compose and append as two launches (the unfused path), for reference
+    split = split_leg(torch, sess, plan, ks, vs, L, args.steps)
 
     # Outside the step: one compose launch over all layer buffer sets (a
     # unit's cached state is placed for every layer at once), the kernel's
     # steady-state bandwidth without the launch ramp of a single layer.
     sess.compose(plan, layer="all", stream=main_s)
     reps = 5
+    E = lambda: torch.cuda.Event(enable_timing=True)
     ev_a, ev_b = E(), E()
     ev_a.record(main_s)
     for _ in range(reps):
@@ -503,22 +636,16 @@ def main():
         host["staged"] = host_tier_staged(torch, wl)
     gather_bytes = 2 * plan.num_gather_tokens * row_bytes   # read + write
     append_bytes = 2 * T * row_bytes
+    asm_bytes = gather_bytes + append_bytes
     retain_bytes = 2 * plan.num_retain_tokens * row_bytes
-    kv_lo = plan.row_kv_lo()
-    visible = int((pos.astype(np.int64) - kv_lo + 1).sum())
-    attn_flops = 4.0 * m.head_dim * m.n_q_heads * visible
-    attn_tflops = attn_flops / (attn_ms * 1e-3) / 1e12
-    compose_gbs = gather_bytes / (compose_ms * 1e-3) / 1e9
-    peak = PEAK_E4M3_BLEND if m.kv_dtype == "e4m3" else PEAK_MFMA_TFLOPS[m.act_dtype]
+    attn_flops = attention_flops(plan, m)
+    attn_tflops = attn_flops / (d_attn["mean"] * 1e-6) / 1e12
+    asm_gbs = asm_bytes / (d_asm["mean"] * 1e-6) / 1e9
     G = m.n_q_heads // m.n_kv_heads
-    attn_kernel = (f"attn_fp8_kernel<{G}>" if m.kv_dtype == "e4m3"
-                   else f"attn_mfma_kernel<{G}, false, {plan.attn_rows_per_item // 32}>")
-    # the e4m3 page kernel is instantiated for 2, 4 or 8 units per thread
-    units = m.page_size * m.n_kv_heads * 8
-    u = 2 if units <= 512 else 4 if units <= 1024 else 8
-    compose_kernel = (f"page_fp8_kernel<0, {u}>" if m.kv_dtype == "e4m3" else
-                      f"kv_move_kernel<{m.head_dim}, unsigned short, 0>")
+    attn_kernel = attention_kernel_name(plan, m)
+    asm_kernel = assembly_kernel_name(m)
     value = wl.prompt_tokens / (ms * 1e-3)
+    peak, blend = attention_peaks(m)
 
     rec = {
         "metric": "composed-prefill tokens/s per layer",
@@ -538,39 +665,54 @@ def main():
             "seed": wl.seed,
         },
         "computed_tokens_per_s": T / (ms * 1e-3),
-        "assembly_hbm_gbps": compose_gbs,
+        "assembly_hbm_gbps": asm_gbs,
         "attention_tflops": attn_tflops,
-        "kernel_us": {"compose": compose_ms * 1e3, "append": append_ms * 1e3,
-                      "attention": attn_ms * 1e3, "retain_side_stream": retain_ms * 1e3},
+        "kernel_us": {"assembly": d_asm, "attention": d_attn, "retain_side_stream": d_ret,
+                      "step": dist(step_ms)},
         "roofline": {"bound": "mfma", "achieved": attn_tflops, "peak": peak,
                      "unit": "TFLOP/s", "frac": attn_tflops / peak,
                      # the committed profiles are of the GLOBAL scope
                      "traffic": (profiled_traffic(args.workload, attn_kernel)
                                  if args.scope == "global" else None),
-                     "kernel": attn_kernel, "flops_per_launch": attn_flops},
-        "roofline_compose": {"bound": "hbm", "achieved": compose_gbs, "peak": PEAK_HBM_GBS,
-                             "unit": "GB/s", "frac": compose_gbs / PEAK_HBM_GBS,
-                             "bytes_per_launch": gather_bytes,
-                             "traffic": profiled_traffic(args.workload, compose_kernel),
-                             "kernel": compose_kernel},
+                     "kernel": attn_kernel, "flops_per_launch": attn_flops,
+                     "achieved_from": "mean event duration"},
+        "roofline_assembly": {"bound": "hbm", "achieved": asm_gbs, "peak": PEAK_HBM_GBS,
+                              "unit": "GB/s", "frac": asm_gbs / PEAK_HBM_GBS,
+                              "bytes_per_launch": asm_bytes,
+                              "gather_bytes": gather_bytes, "append_bytes": append_bytes,
+                              "traffic": profiled_traffic(args.workload, asm_kernel),
+                              "kernel": asm_kernel,
+                              "frac_at_median": asm_bytes / (d_asm["median"] * 1e-6) / 1e9
+                              / PEAK_HBM_GBS},
+        "compose_append_split": split,
         "compose_all_layers": {"layers": L, "us": compose_all_ms * 1e3,
                                "gbps": L * gather_bytes / (compose_all_ms * 1e-3) / 1e9,
                                "frac": L * gather_bytes / (compose_all_ms * 1e-3) / 1e9 / PEAK_HBM_GBS},
-        "append_gbps": append_bytes / (append_ms * 1e-3) / 1e9,
-        "retain_gbps": retain_bytes / (retain_ms * 1e-3) / 1e9 if retain_ms > 0 else None,
+        "retain_gbps": retain_bytes / (d_ret["mean"] * 1e-6) / 1e9 if d_ret["mean"] > 0 else None,
     }
+    if blend:
+        rec["roofline"]["frac_of_blend"] = attn_tflops / blend
+        rec["roofline"]["blend_peak"] = blend
     if alias:
         rec["alias_v"] = alias
     if host:
         rec["host_tier"] = host
     rec["control_plane"] = control_plane_replay()
+    if args.legs:
+        rec["legs"] = {}
+        if "local" in args.legs and args.scope == "global" and m.kv_dtype != "f32":
+            rec["legs"]["local"] = local_leg(torch, sess, wl, qs, ks, vs, out, lse, L,
+                                             args.steps, args.warmup)
+        for name in ("fp8rag", "agent8b", "long70b"):
+            if name in args.legs and name != args.workload:
+                rec["legs"][name] = workload_leg(torch, name, args.steps, args.warmup)
     if measured:
         rec["measured_peaks"] = measured
         mfma_peak = measured["mfma_loop_tflops"]
         if m.kv_dtype == "e4m3":
-            mfma_peak *= peak / PEAK_MFMA_TFLOPS["bf16"]   # the blend, at the measured clock
+            mfma_peak *= peak / PEAK_MFMA_TFLOPS["bf16"]   # fp8 peak, at the measured clock
         rec["roofline"]["frac_of_measured"] = attn_tflops / mfma_peak
-        rec["roofline_compose"]["frac_of_measured"] = compose_gbs / max(
+        rec["roofline_assembly"]["frac_of_measured"] = asm_gbs / max(
             measured["copy_kernel_gbps"], measured["copy_gbps"])
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle baseline")

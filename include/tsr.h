@@ -346,6 +346,20 @@ tsr_status tsr_attn(const tsr_plan* plan, const void* q, const void* req_k,
                     const void* req_v, const float* req_scale, void* out,
                     float* lse, void* stream);
 
+/* Assembly of one layer's request KV in a single launch: exactly
+ * tsr_compose_kv (n_layers = 1) followed by tsr_append_kv, with the same
+ * results bit for bit, in one kernel whose first workgroups gather the
+ * cached tokens and whose others append the computed rows (Section 5.3:
+ * hits placed with RoPE at their new positions; computed rows placed before
+ * the extend pass).  Both are HBM-bound copies, so one launch spares the
+ * second launch and its ramp.  Arguments as in tsr_compose_kv (pool_*,
+ * pool_scale, req_*, req_scale) and tsr_append_kv (k, v): pool_k/pool_v may
+ * be NULL when the plan gathers nothing, k/v when it computes nothing.
+ * Follow with tsr_attn (or tsr_attn_part / tsr_attn_aliased). */
+tsr_status tsr_assemble_kv(const tsr_plan* plan, const void* pool_k, const void* pool_v,
+                           const float* pool_scale, const void* k, const void* v,
+                           void* req_k, void* req_v, float* req_scale, void* stream);
+
 /* tsr_attn restricted to one part of the items (a tsr_attn_part_id);
  * TSR_ATTN_ALL is tsr_attn.  BEFORE_COMPOSE needs tsr_append_kv of the
  * plan in stream order; AFTER_COMPOSE needs append and compose. */

@@ -11,7 +11,7 @@ from ._binding import (DTYPE_CODES, EXPORTS, TSR_ATTN_AFTER_COMPOSE, TSR_ATTN_AL
                        TSR_ERR_STATE, TSR_ERR_UNSUPPORTED, UnitCache, tsr_copy_blocks,
                        TSR_F32, TSR_HIT, TSR_MISS, TSR_OK, TSR_SCOPE_GLOBAL, TSR_SCOPE_LOCAL,
                        Plan, RequestBatch, TsrError, lib, make_model,
-                       tsr_abi_version, tsr_append_kv, tsr_attn, tsr_attn_part, tsr_compose_kv, tsr_last_error,
+                       tsr_abi_version, tsr_append_kv, tsr_assemble_kv, tsr_attn, tsr_attn_part, tsr_compose_kv, tsr_last_error,
                        tsr_peak_copy, tsr_peak_mfma, tsr_peak_mfma_flops,
                        tsr_plan_create, tsr_plan_workspace_size, tsr_prefill_attn,
                        tsr_retain_kv, tsr_rope_table_bytes, tsr_rope_table_init)
@@ -22,7 +22,7 @@ __all__ = [
     "TSR_ERR_NO_SPACE", "TSR_ERR_OUT_OF_RANGE", "TSR_ERR_STATE", "TSR_ERR_UNSUPPORTED",
     "UnitCache", "tsr_copy_blocks", "TSR_F32", "TSR_HIT", "TSR_MISS", "TSR_OK",
     "TSR_SCOPE_GLOBAL", "TSR_SCOPE_LOCAL", "Plan", "RequestBatch", "TsrError", "lib",
-    "make_model", "tsr_abi_version", "tsr_append_kv", "tsr_attn", "tsr_attn_part", "tsr_compose_kv",
+    "make_model", "tsr_abi_version", "tsr_append_kv", "tsr_assemble_kv", "tsr_attn", "tsr_attn_part", "tsr_compose_kv",
     "tsr_last_error", "tsr_peak_copy", "tsr_peak_mfma", "tsr_peak_mfma_flops",
     "tsr_plan_create", "tsr_plan_workspace_size", "tsr_prefill_attn",
     "tsr_retain_kv", "tsr_rope_table_bytes", "tsr_rope_table_init",

@@ -38,7 +38,7 @@ EXPORTS = (
     "tsr_plan_num_attn_items_part", "tsr_attn_part", "tsr_plan_create_ex",
     "tsr_plan_num_aliased_pages", "tsr_attn_aliased",
     "tsr_plan_compute_positions", "tsr_plan_row_kv_lo", "tsr_plan_destroy", "tsr_compose_kv",
-    "tsr_prefill_attn", "tsr_append_kv", "tsr_attn", "tsr_retain_kv",
+    "tsr_prefill_attn", "tsr_append_kv", "tsr_assemble_kv", "tsr_attn", "tsr_retain_kv",
     "tsr_cache_create", "tsr_cache_destroy", "tsr_cache_reserve", "tsr_cache_publish",
     "tsr_cache_cancel", "tsr_cache_reclaim", "tsr_cache_acquire", "tsr_cache_release",
     "tsr_cache_evict", "tsr_cache_query", "tsr_cache_free_blocks", "tsr_copy_blocks",
@@ -140,6 +140,7 @@ def lib():
             "tsr_prefill_attn": (c_int32, [P, P, P, P, P, P, P, P, P, P]),
             "tsr_retain_kv": (c_int32, [P, P, P, P, P, P, P]),
             "tsr_append_kv": (c_int32, [P, P, P, P, P, P, P]),
+            "tsr_assemble_kv": (c_int32, [P, P, P, P, P, P, P, P, P, P]),
             "tsr_attn": (c_int32, [P, P, P, P, P, P, P, P]),
             "tsr_attn_part": (c_int32, [P, c_int32, P, P, P, P, P, P, P]),
             "tsr_cache_create": (c_int32, [c_int32, POINTER(c_void_p)]),
@@ -386,6 +387,13 @@ def tsr_retain_kv(plan: Plan, k, v, pool_k, pool_v, pool_scale, stream=None) -> 
 def tsr_append_kv(plan: Plan, k, v, req_k, req_v, req_scale=None, stream=None) -> None:
     _check(lib().tsr_append_kv(plan.handle, _ptr(k), _ptr(v), _ptr(req_k), _ptr(req_v),
                                _ptr(req_scale), _stream(stream)))
+
+
+def tsr_assemble_kv(plan: Plan, pool_k, pool_v, pool_scale, k, v, req_k, req_v,
+                    req_scale=None, stream=None) -> None:
+    _check(lib().tsr_assemble_kv(plan.handle, _ptr(pool_k), _ptr(pool_v), _ptr(pool_scale),
+                                 _ptr(k), _ptr(v), _ptr(req_k), _ptr(req_v),
+                                 _ptr(req_scale), _stream(stream)))
 
 
 def tsr_attn(plan: Plan, q, req_k, req_v, req_scale, out, lse=None, stream=None) -> None:

@@ -353,6 +353,29 @@ tsr_status tsr_append_kv(const tsr_plan* p, const void* k, const void* v,
 }
 
 
+tsr_status tsr_assemble_kv(const tsr_plan* p, const void* pool_k, const void* pool_v,
+                           const float* pool_scale, const void* k, const void* v,
+                           void* req_k, void* req_v, float* req_scale, void* stream) {
+  return guarded([&]() -> tsr_status {
+    tsr_status st = check_exec(p);
+    if (st != TSR_OK) return st;
+    if ((st = check_scales(p, pool_scale, req_scale, p->n_gather > 0, true)) != TSR_OK)
+      return st;
+    if (p->n_gather == 0 && p->T == 0) return TSR_OK;
+    if (!req_k || !req_v || (p->n_gather > 0 && (!pool_k || !pool_v)) ||
+        (p->T > 0 && (!k || !v))) {
+      set_error("assemble_kv: a required pointer is NULL");
+      return TSR_ERR_INVALID_ARG;
+    }
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    hipError_t e = is_e4m3(p) ? launch_assemble_e4m3(p, pool_k, pool_v, pool_scale, k, v,
+                                                     req_k, req_v, req_scale, s)
+                              : launch_assemble(p, pool_k, pool_v, k, v, req_k, req_v, s);
+    if (e != hipSuccess) return device_fail("assembly launch", e);
+    return TSR_OK;
+  });
+}
+
 tsr_status tsr_attn_part(const tsr_plan* p, int32_t part, const void* q,
                          const void* req_k, const void* req_v, const float* req_scale,
                          void* out, float* lse, void* stream) {

@@ -43,6 +43,10 @@ namespace tsr {
 namespace {
 
 // ------------------------------------------------------------- fp32 mode
+// The reference mode of the fp32 configurations: operands are fp32 (q_rot
+// and K rounded to fp32 like the storage), the arithmetic is fp64 (scores,
+// softmax statistics and the weighted sum of V), and the output is rounded
+// to fp32 once.  One workgroup per item, scalar code: its job is accuracy.
 template <int D>
 __global__ __launch_bounds__(256) void attn_f32_kernel(
     const float* __restrict__ q, const float* __restrict__ kc,
@@ -52,8 +56,8 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(
     float* __restrict__ out, float* __restrict__ lse, int n_q_heads,
     int n_kv_heads, int log2_page, float scale) {
   __shared__ float qs[D];
-  __shared__ float ps[256];
-  __shared__ float red[8];
+  __shared__ double ps[256];
+  __shared__ double red[8];
   const AttnItem it = items[blockIdx.x];
   if (it.n_rows == 0) return;
   const int t = threadIdx.x;
@@ -62,15 +66,15 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(
   const int page_mask = (1 << log2_page) - 1;
   const int32_t* bt = bts + it.bt_off;
 
-  auto block_max = [&](float v) {
-    for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+  auto block_max = [&](double v) {
+    for (int o = 32; o > 0; o >>= 1) v = fmax(v, __shfl_xor(v, o));
     if ((t & 63) == 0) red[t >> 6] = v;
     __syncthreads();
-    v = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+    v = fmax(fmax(red[0], red[1]), fmax(red[2], red[3]));
     __syncthreads();
     return v;
   };
-  auto block_sum = [&](float v) {
+  auto block_sum = [&](double v) {
     for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
     if ((t & 63) == 0) red[4 + (t >> 6)] = v;
     __syncthreads();
@@ -82,6 +86,7 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(
     const int page = bt[k >> log2_page];
     return base + ((((int64_t)page * n_kv_heads + g) << log2_page) + (k & page_mask)) * D;
   };
+  const double sc = scale;
 
   for (int rr = 0; rr < it.n_rows; ++rr) {
     const int row = it.row0 + rr;
@@ -98,32 +103,32 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(
         qs[t + D / 2] = hi;
       }
       __syncthreads();
-      float m = -INFINITY, l = 0.0f, o = 0.0f;
+      double m = -INFINITY, l = 0.0, o = 0.0;
       for (int k0 = it.kv_lo; k0 <= pos; k0 += 256) {
         const int k = k0 + t;
-        float s = -INFINITY;
+        double s = -INFINITY;
         if (k <= pos) {
           const float* kp = key_row(kc, k);
-          float acc = 0.0f;
-          for (int e = 0; e < D; ++e) acc += qs[e] * kp[e];
-          s = acc * scale;
+          double acc = 0.0;
+          for (int e = 0; e < D; ++e) acc = fma((double)qs[e], (double)kp[e], acc);
+          s = acc * sc;
         }
-        const float mn = fmaxf(m, block_max(s));
-        const float p = (k <= pos) ? expf(s - mn) : 0.0f;
+        const double mn = fmax(m, block_max(s));
+        const double p = (k <= pos) ? exp(s - mn) : 0.0;
         ps[t] = p;
-        const float alpha = expf(m - mn);
+        const double alpha = exp(m - mn);
         l = l * alpha + block_sum(p);
         if (t < D) {
           const int nk = min(256, pos + 1 - k0);
-          float acc = 0.0f;
-          for (int j = 0; j < nk; ++j) acc += ps[j] * key_row(vc, k0 + j)[t];
+          double acc = 0.0;
+          for (int j = 0; j < nk; ++j) acc = fma(ps[j], (double)key_row(vc, k0 + j)[t], acc);
           o = o * alpha + acc;
         }
         m = mn;
         __syncthreads();
       }
-      if (t < D) out[((int64_t)row * n_q_heads + hq) * D + t] = o / l;
-      if (t == 0 && lse) lse[(int64_t)row * n_q_heads + hq] = m + logf(l);
+      if (t < D) out[((int64_t)row * n_q_heads + hq) * D + t] = (float)(o / l);
+      if (t == 0 && lse) lse[(int64_t)row * n_q_heads + hq] = (float)(m + log(l));
       __syncthreads();
     }
   }

@@ -73,8 +73,8 @@ __device__ __forceinline__ uint2 encode8(const float* y) {
 // (instantiated for 2, 4 and 8; each unit holds 16 fp32 values and its raw
 // V, so U sets the kernel's registers and with them its occupancy).
 template <int MODE, int U>
-__global__ __launch_bounds__(256) void page_fp8_kernel(
-    const PageDesc* __restrict__ pages, const float* __restrict__ rope_cos,
+__device__ __forceinline__ void fp8_page(
+    const PageDesc pd, const float* __restrict__ rope_cos,
     const float* __restrict__ rope_sin, const void* __restrict__ src_k,
     const void* __restrict__ src_v, const float* __restrict__ src_scale,
     uint8_t* __restrict__ dst_k, uint8_t* __restrict__ dst_v,
@@ -82,7 +82,6 @@ __global__ __launch_bounds__(256) void page_fp8_kernel(
     int64_t src_layer_stride, int64_t dst_layer_stride,
     int64_t src_scale_stride, int64_t dst_scale_stride) {
   __shared__ float red[2][4];
-  const PageDesc pd = pages[blockIdx.x];
   const int tid = threadIdx.x;
   const int B = 1 << log2_page;
   const int64_t layer = blockIdx.y;
@@ -192,6 +191,41 @@ __global__ __launch_bounds__(256) void page_fp8_kernel(
   }
 }
 
+template <int MODE, int U>
+__global__ __launch_bounds__(256) void page_fp8_kernel(
+    const PageDesc* __restrict__ pages, const float* __restrict__ rope_cos,
+    const float* __restrict__ rope_sin, const void* __restrict__ src_k,
+    const void* __restrict__ src_v, const float* __restrict__ src_scale,
+    uint8_t* __restrict__ dst_k, uint8_t* __restrict__ dst_v,
+    float* __restrict__ dst_scale, int n_kv_heads, int log2_page,
+    int64_t src_layer_stride, int64_t dst_layer_stride,
+    int64_t src_scale_stride, int64_t dst_scale_stride) {
+  fp8_page<MODE, U>(pages[blockIdx.x], rope_cos, rope_sin, src_k, src_v, src_scale, dst_k,
+                    dst_v, dst_scale, n_kv_heads, log2_page, src_layer_stride,
+                    dst_layer_stride, src_scale_stride, dst_scale_stride);
+}
+
+// Assembly of one layer in a single launch: the first n_gpages workgroups
+// compose gathered pages, the rest append computed pages.
+template <int U>
+__global__ __launch_bounds__(256) void page_fp8_assemble_kernel(
+    const PageDesc* __restrict__ gpages, int n_gpages, const PageDesc* __restrict__ apages,
+    const float* __restrict__ rope_cos, const float* __restrict__ rope_sin,
+    const uint8_t* __restrict__ pool_k, const uint8_t* __restrict__ pool_v,
+    const float* __restrict__ pool_scale, const uint16_t* __restrict__ k,
+    const uint16_t* __restrict__ v, uint8_t* __restrict__ req_k,
+    uint8_t* __restrict__ req_v, float* __restrict__ req_scale, int n_kv_heads,
+    int log2_page) {
+  if ((int)blockIdx.x < n_gpages)
+    fp8_page<kFpCompose, U>(gpages[blockIdx.x], rope_cos, rope_sin, pool_k, pool_v,
+                            pool_scale, req_k, req_v, req_scale, n_kv_heads, log2_page,
+                            0, 0, 0, 0);
+  else
+    fp8_page<kFpAppend, U>(apages[blockIdx.x - n_gpages], rope_cos, rope_sin, k, v,
+                           nullptr, req_k, req_v, req_scale, n_kv_heads, log2_page, 0, 0,
+                           0, 0);
+}
+
 int ilog2(int x) {
   int l = 0;
   while ((1 << l) < x) ++l;
@@ -221,6 +255,29 @@ hipError_t launch_pages(const tsr_plan* p, const PageDesc* pages, int n,
 }
 
 }  // namespace
+
+hipError_t launch_assemble_e4m3(const tsr_plan* p, const void* pool_k, const void* pool_v,
+                                const float* pool_scale, const void* k, const void* v,
+                                void* req_k, void* req_v, float* req_scale, hipStream_t s) {
+  const int n = p->n_gpages + p->n_apages;
+  if (n <= 0) return hipSuccess;
+  const tsr_model& m = p->model;
+  const int units = m.page_size * m.n_kv_heads * 8;
+  if (units > 256 * kMaxU) return hipErrorInvalidValue;   // the planner rejects these
+#define TSR_APAGES(UU)                                                                  \
+  hipLaunchKernelGGL((page_fp8_assemble_kernel<UU>), dim3(n), dim3(256), 0, s,          \
+                     p->dev.gpages, p->n_gpages, p->dev.apages, p->dev.rope_cos,         \
+                     p->dev.rope_sin, static_cast<const uint8_t*>(pool_k),               \
+                     static_cast<const uint8_t*>(pool_v), pool_scale,                    \
+                     static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v),   \
+                     static_cast<uint8_t*>(req_k), static_cast<uint8_t*>(req_v), req_scale, \
+                     m.n_kv_heads, ilog2(m.page_size))
+  if (units <= 512) TSR_APAGES(2);
+  else if (units <= 1024) TSR_APAGES(4);
+  else TSR_APAGES(8);
+#undef TSR_APAGES
+  return hipGetLastError();
+}
 
 hipError_t launch_compose_e4m3(const tsr_plan* p, const void* pool_k,
                                const void* pool_v, const float* pool_scale,

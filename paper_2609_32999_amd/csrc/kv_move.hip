@@ -67,9 +67,11 @@ template <> struct Vec8<float> {
 constexpr int kTok = 16;     // descriptors per workgroup
 constexpr int kThreads = 256;
 
+// The tokens of one workgroup: descriptor i = blk * kTok + (thread's token)
+// of `descs` (n of them), moved as MODE says.  No barriers.
 template <int D, typename T, int MODE>
-__global__ __launch_bounds__(kThreads) void kv_move_kernel(
-    const void* __restrict__ descs, int n, const float* __restrict__ rope_cos,
+__device__ __forceinline__ void move_tokens(
+    int blk, const void* __restrict__ descs, int n, const float* __restrict__ rope_cos,
     const float* __restrict__ rope_sin, const T* __restrict__ src_k,
     const T* __restrict__ src_v, T* __restrict__ dst_k, T* __restrict__ dst_v,
     int n_kv_heads, int log2_page, int64_t src_layer_stride,
@@ -81,8 +83,8 @@ __global__ __launch_bounds__(kThreads) void kv_move_kernel(
   const int c = tid % kCh;
   const int tl = (tid / kCh) % kTok;
   const int h0 = tid / (kCh * kTok);
-  const int i = blockIdx.x * kTok + tl;
-  if (i >= n) return;  // this kernel has no barriers
+  const int i = blk * kTok + tl;
+  if (i >= n) return;
 
   const int64_t layer = blockIdx.y;
   src_k += layer * src_layer_stride;
@@ -165,6 +167,38 @@ __global__ __launch_bounds__(kThreads) void kv_move_kernel(
   }
 }
 
+template <int D, typename T, int MODE>
+__global__ __launch_bounds__(kThreads) void kv_move_kernel(
+    const void* __restrict__ descs, int n, const float* __restrict__ rope_cos,
+    const float* __restrict__ rope_sin, const T* __restrict__ src_k,
+    const T* __restrict__ src_v, T* __restrict__ dst_k, T* __restrict__ dst_v,
+    int n_kv_heads, int log2_page, int64_t src_layer_stride,
+    int64_t dst_layer_stride) {
+  move_tokens<D, T, MODE>(blockIdx.x, descs, n, rope_cos, rope_sin, src_k, src_v, dst_k,
+                          dst_v, n_kv_heads, log2_page, src_layer_stride,
+                          dst_layer_stride);
+}
+
+// Assembly of one layer's request KV in a single launch: the first
+// ceil(n_gather / kTok) workgroups compose cached tokens, the rest append
+// the computed rows.  Both movers are bound by HBM bandwidth; one launch
+// spares the second kernel's launch and ramp.
+template <int D, typename T>
+__global__ __launch_bounds__(kThreads) void kv_assemble_kernel(
+    const GatherDesc* __restrict__ gather, int n_gather, const RowDesc* __restrict__ rows,
+    int n_rows, const float* __restrict__ rope_cos, const float* __restrict__ rope_sin,
+    const T* __restrict__ pool_k, const T* __restrict__ pool_v, const T* __restrict__ k,
+    const T* __restrict__ v, T* __restrict__ req_k, T* __restrict__ req_v,
+    int n_kv_heads, int log2_page) {
+  const int gblocks = (n_gather + kTok - 1) / kTok;
+  if ((int)blockIdx.x < gblocks)
+    move_tokens<D, T, kCompose>(blockIdx.x, gather, n_gather, rope_cos, rope_sin, pool_k,
+                                pool_v, req_k, req_v, n_kv_heads, log2_page, 0, 0);
+  else
+    move_tokens<D, T, kAppend>(blockIdx.x - gblocks, rows, n_rows, rope_cos, rope_sin, k,
+                               v, req_k, req_v, n_kv_heads, log2_page, 0, 0);
+}
+
 int ilog2(int x) {
   int l = 0;
   while ((1 << l) < x) ++l;
@@ -207,7 +241,40 @@ hipError_t launch_move(const tsr_plan* p, const void* descs, int n,
   return launch_move_t<uint16_t, MODE>(p, descs, n, sk, sv, dk, dv, n_layers, ss, ds, s);
 }
 
+template <typename T>
+hipError_t launch_assemble_t(const tsr_plan* p, const void* pool_k, const void* pool_v,
+                             const void* k, const void* v, void* req_k, void* req_v,
+                             hipStream_t s) {
+  const int gb = (p->n_gather + kTok - 1) / kTok, ab = (p->T + kTok - 1) / kTok;
+  if (gb + ab == 0) return hipSuccess;
+  const tsr_model& m = p->model;
+  const int lp = ilog2(m.page_size);
+#define TSR_ASM(DIM)                                                                  \
+  hipLaunchKernelGGL((kv_assemble_kernel<DIM, T>), dim3(gb + ab), dim3(kThreads), 0, s, \
+                     p->dev.gather, p->n_gather, p->dev.rows, p->T, p->dev.rope_cos,   \
+                     p->dev.rope_sin, static_cast<const T*>(pool_k),                   \
+                     static_cast<const T*>(pool_v), static_cast<const T*>(k),          \
+                     static_cast<const T*>(v), static_cast<T*>(req_k),                 \
+                     static_cast<T*>(req_v), m.n_kv_heads, lp)
+  switch (m.head_dim) {
+    case 64: TSR_ASM(64); break;
+    case 128: TSR_ASM(128); break;
+    case 256: TSR_ASM(256); break;
+    default: return hipErrorInvalidValue;
+  }
+#undef TSR_ASM
+  return hipGetLastError();
+}
+
 }  // namespace
+
+hipError_t launch_assemble(const tsr_plan* p, const void* pool_k, const void* pool_v,
+                           const void* k, const void* v, void* req_k, void* req_v,
+                           hipStream_t s) {
+  if (p->model.kv_dtype == TSR_F32)
+    return launch_assemble_t<float>(p, pool_k, pool_v, k, v, req_k, req_v, s);
+  return launch_assemble_t<uint16_t>(p, pool_k, pool_v, k, v, req_k, req_v, s);
+}
 
 hipError_t launch_compose(const tsr_plan* p, const void* pool_k,
                           const void* pool_v, void* req_k, void* req_v,

@@ -166,6 +166,12 @@ class Session:
         B.tsr_append_kv(plan, k, v, self.req_k[layer], self.req_v[layer], self._rs(layer),
                         stream or self.stream)
 
+    def assemble(self, plan, k, v, layer: int = 0, stream=None):
+        """compose + append of one layer in one launch (same results)."""
+        B.tsr_assemble_kv(plan, self._pk(layer), self._pv(layer), self._ps(layer), k, v,
+                          self.req_k[layer], self.req_v[layer], self._rs(layer),
+                          stream or self.stream)
+
     def attn(self, plan, q, out, lse=None, layer: int = 0, stream=None, part: int = 0):
         """Attention over the assembled pages; `part` selects all items
         (TSR_ATTN_ALL) or the items before / after compose."""

@@ -11,6 +11,8 @@ import workloads
 from oracle import layout as L
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+# rows of a bf16 attention item with several 32-row blocks
+MULTI_ROWS = 96
 
 
 def _model(wl, **kw):
@@ -88,28 +90,29 @@ def _items_per_kv_head(wl, rows_per_item):
                                         ("agent8b", "local"), ("long70b", "global"),
                                         ("fp8rag", "global"), ("small_f32", "global")])
 def test_attention_row_blocks(name, scope):
-    """bf16 plans put three 32-row blocks in an item unless fewer than 80 % of
-    the items' block x tile slots would hold work; other dtypes use one."""
+    """bf16 plans put MULTI_ROWS // 32 row blocks of 32 rows in an item unless
+    fewer than 80 % of the items' block x tile slots would hold work; other
+    dtypes use one."""
     cfg = workloads.get_config(name)
     if scope != "global":
         cfg = cfg.with_(miss_scope=scope)
     wl = workloads.make_workload(cfg)
     m = wl.model
     n1, _ = _items_per_kv_head(wl, 32)
-    n3, use3 = _items_per_kv_head(wl, 96)
+    n3, use3 = _items_per_kv_head(wl, MULTI_ROWS)
     three = m.kv_dtype == "bf16" and m.act_dtype == "bf16" and use3 >= 0.8
     groups = (m.n_q_heads // m.n_kv_heads) // 4 if m.act_dtype == "bf16" and \
         m.n_q_heads // m.n_kv_heads > 4 else 1
     per = m.n_kv_heads * groups
     plan = _plan(wl)
-    # launch padding only adds items: three row blocks give fewer items than
+    # launch padding only adds items: multi-block items give fewer items than
     # one-block items would need, one row block at least that many
     if three:
         assert n3 * per <= plan.num_attn_items < n1 * per, (plan.num_attn_items, n1, n3, use3)
     else:
         assert plan.num_attn_items >= n1 * per, (plan.num_attn_items, n1, n3, use3)
     assert bool(three) == ((name, scope) in {("rag8b", "global"), ("long70b", "global")})
-    assert plan.attn_rows_per_item == (96 if three else 32)
+    assert plan.attn_rows_per_item == (MULTI_ROWS if three else 32)
 
 
 def _tiny_req(**over):

