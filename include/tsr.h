@@ -223,6 +223,27 @@ tsr_status tsr_plan_create_ex(const tsr_model* model, const tsr_request* reqs,
                               void* dev_workspace, size_t workspace_bytes, void* stream,
                               tsr_plan** out_plan);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation):
+ * tsr_plan_create_ex without a workspace.  The plan's device image is
+ * written (hipMemcpyAsync on `stream`) into a plan area the library owns on
+ * the current device, a static device array of 16 MiB that each GPU holds
+ * until the process ends; the call allocates no device memory.
+ *   - A batch whose image exceeds 16 MiB (tsr_plan_workspace_size) is
+ *     refused with TSR_ERR_OUT_OF_RANGE before any HIP call.
+ *   - Every static plan on a device shares that area: creating one rewrites
+ *     it, and the plans it replaced are refused from then on
+ *     (TSR_ERR_STATE from every entry point that executes a plan).
+ *   - Calls that overlap on one GPU race: work of a previous static plan
+ *     still running when the next static plan's image is copied reads the
+ *     new image.  Order them (one stream, or an event between streams).
+ * Other arguments, checks and results as tsr_plan_create_ex; destroy the
+ * plan with tsr_plan_destroy. */
+tsr_status tsr_plan_create_static(const tsr_model* model, const tsr_request* reqs,
+                                  int32_t n_req, int32_t n_pool_pages, int32_t n_req_pages,
+                                  const tsr_plan_options* options, const void* dev_rope_table,
+                                  void* stream, tsr_plan** out_plan);
+
 /* Number of computed rows T (inputs q/k/v and outputs have T rows). */
 int32_t tsr_plan_num_compute_tokens(const tsr_plan* plan);
 /* Number of cached tokens gathered by tsr_compose_kv. */

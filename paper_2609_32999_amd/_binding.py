@@ -35,7 +35,7 @@ EXPORTS = (
     "tsr_rope_table_init", "tsr_plan_workspace_size", "tsr_plan_create",
     "tsr_plan_num_compute_tokens", "tsr_plan_num_gather_tokens",
     "tsr_plan_num_retain_tokens", "tsr_plan_num_attn_items", "tsr_plan_attn_rows_per_item",
-    "tsr_plan_num_attn_items_part", "tsr_attn_part", "tsr_plan_create_ex",
+    "tsr_plan_num_attn_items_part", "tsr_attn_part", "tsr_plan_create_ex", "tsr_plan_create_static",
     "tsr_plan_num_aliased_pages", "tsr_attn_aliased",
     "tsr_plan_compute_positions", "tsr_plan_row_kv_lo", "tsr_plan_destroy", "tsr_compose_kv",
     "tsr_prefill_attn", "tsr_append_kv", "tsr_assemble_kv", "tsr_attn", "tsr_retain_kv",
@@ -132,6 +132,10 @@ def lib():
             "tsr_plan_create_ex": (c_int32, [POINTER(tsr_model), POINTER(tsr_request), c_int32,
                                              c_int32, c_int32, POINTER(tsr_plan_options), P, P,
                                              c_size_t, P, POINTER(c_void_p)]),
+            "tsr_plan_create_static": (c_int32, [POINTER(tsr_model), POINTER(tsr_request),
+                                                 c_int32, c_int32, c_int32,
+                                                 POINTER(tsr_plan_options), P, P,
+                                                 POINTER(c_void_p)]),
             "tsr_attn_aliased": (c_int32, [P, c_int32, P, P, P, P, P, P, P]),
             "tsr_plan_compute_positions": (c_int32, [P, POINTER(c_int32), POINTER(c_int32)]),
             "tsr_plan_row_kv_lo": (c_int32, [P, POINTER(c_int32)]),
@@ -359,6 +363,22 @@ def tsr_plan_create(model: tsr_model, batch: RequestBatch, n_pool_pages: int,
         _check(lib().tsr_plan_create(ctypes.byref(model), batch.array, batch.n, n_pool_pages,
                                      n_req_pages, _ptr(dev_rope_table), _ptr(dev_workspace),
                                      workspace_bytes, _stream(stream), ctypes.byref(out)))
+    plan = Plan(out.value, model)
+    plan.alias_v = bool(alias_v)
+    return plan
+
+
+def tsr_plan_create_static(model: tsr_model, batch: RequestBatch, n_pool_pages: int,
+                           n_req_pages: int, dev_rope_table, stream=None,
+                           alias_v: bool = False) -> Plan:
+    """A plan whose device image lives in the library's own plan area (no
+    workspace); a later static plan on the same device supersedes it."""
+    out = c_void_p()
+    opts = tsr_plan_options(alias_v=1 if alias_v else 0)
+    _check(lib().tsr_plan_create_static(ctypes.byref(model), batch.array, batch.n,
+                                        n_pool_pages, n_req_pages, ctypes.byref(opts),
+                                        _ptr(dev_rope_table), _stream(stream),
+                                        ctypes.byref(out)))
     plan = Plan(out.value, model)
     plan.alias_v = bool(alias_v)
     return plan

@@ -24,7 +24,7 @@ tsr_status check_exec(const tsr_plan* p) {
     set_error("plan was created without a device workspace (host-only plan)");
     return TSR_ERR_INVALID_ARG;
   }
-  return TSR_OK;
+  return check_static_plan(p);
 }
 
 bool is_e4m3(const tsr_plan* p) { return p->model.kv_dtype == TSR_E4M3; }

@@ -126,6 +126,10 @@ struct tsr_plan {
   size_t off_gpages, off_apages, off_rpages;
   const void* rope_table;   // device
   void* ws;                 // device, NULL for host-only plans
+  // plans made by tsr_plan_create_static: the device and generation of the
+  // shared plan area they were written into (0: a workspace plan)
+  int32_t static_device = 0;
+  uint64_t static_gen = 0;
   tsr::PlanDev dev;
 };
 
@@ -157,6 +161,10 @@ tsr_status guarded(F&& f) {
     return TSR_ERR_INVALID_ARG;
   }
 }
+
+// TSR_ERR_STATE if p is a static plan whose shared area a later static plan
+// on the same device has rewritten.
+tsr_status check_static_plan(const tsr_plan* p);
 
 // Validate a model; on failure returns a status and sets the error.
 tsr_status check_model(const tsr_model* m);

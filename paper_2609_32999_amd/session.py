@@ -115,6 +115,16 @@ class Session:
         plan.batch = batch
         return plan
 
+    def plan_static(self, requests, stream=None, alias_v: bool = False):
+        """A plan in the library's own device plan area (no workspace is
+        allocated); a later static plan on this device supersedes it."""
+        batch = B.RequestBatch(requests)
+        plan = B.tsr_plan_create_static(self.model, batch, self.n_pool_pages,
+                                        self.n_req_pages, self.rope, stream or self.stream,
+                                        alias_v=alias_v)
+        plan.batch = batch
+        return plan
+
     # ---------------------------------------------------------- hot path
     def compose(self, plan, layer: int | None = None, stream=None):
         """Compose one layer (default 0), or all layers when layer == 'all'."""
