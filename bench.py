@@ -291,15 +291,31 @@ def host_tier_staged(torch, wl, reps=5, warmup=2):
     return res
 
 
-def alias_v_leg(torch, sess, wl, qs, ks, vs, out, lse, L, steps, warmup):
-    """The same step with V aliasing (attention reads V of whole gathered
-    pages from the pool; the assembly writes only their K), timed like the
-    main step without retention."""
-    plan = sess.plan(wl.requests, alias_v=True)
-    st, asm, att, _, _ = time_path(torch, sess, plan, qs, ks, vs, out, lse, L, steps, warmup)
-    res = {"aliased_pages": plan.num_aliased_pages, "assembly_us": dist(asm),
-           "attention_us": dist(att), "step_us": dist(st)}
-    log(f"[bench] alias_v: {res}")
+def aliasing_leg(torch, sess, wl, qs, ks, vs, out, lse, L, steps, warmup):
+    """Zero-copy composition against the composed (materialized) path, each
+    timed like the main step without retention: V aliasing (attention reads
+    V of whole gathered pages from the pool), K rotated on load (attention
+    reads their pre-RoPE K from the pool and rotates it while staging the
+    tile), and both (compose leaves those pages alone), under the batch's
+    own miss scope and under the LOCAL scope."""
+    import workloads
+    res = {}
+    for scope in ("global", "local"):
+        reqs = (wl.requests if wl.cfg.miss_scope == scope else
+                workloads.make_workload(wl.cfg.with_(miss_scope=scope)).requests)
+        for mode, kw in (("materialized", {}), ("v", dict(alias_v=True)),
+                         ("k", dict(alias_k=True)), ("kv", dict(alias_v=True, alias_k=True))):
+            plan = sess.plan(reqs, **kw)
+            st, asm, att, _, _ = time_path(torch, sess, plan, qs, ks, vs, out, lse, L, steps,
+                                           warmup)
+            res[f"{scope}_{mode}"] = {
+                "aliased_pages_v": plan.num_aliased_pages,
+                "aliased_pages_k": plan.num_aliased_k_pages,
+                "gathered_tokens_moved": plan.num_gather_tokens,
+                "assembly_us": dist(asm), "attention_us": dist(att), "step_us": dist(st)}
+    log("[bench] aliasing: " + ", ".join(
+        f"{k}: asm {v['assembly_us']['median']:.1f} attn {v['attention_us']['median']:.1f}"
+        for k, v in res.items()))
     return res
 
 
@@ -545,7 +561,8 @@ def main():
                     help="skip measuring the achievable copy and bf16 GEMM rates")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-alias-v", dest="alias_v", action="store_false",
-                    help="skip timing the step with V aliasing")
+                    help="skip timing the step with zero-copy composition (V aliasing, K "
+                         "rotated on load, both)")
     ap.add_argument("--no-host-tier", dest="host_tier", action="store_false",
                     help="skip timing compose and retain against a pool in pinned host memory")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
@@ -626,7 +643,7 @@ def main():
     torch.cuda.synchronize()
     compose_all_ms = ev_a.elapsed_time(ev_b) / reps
 
-    alias = alias_v_leg(torch, sess, wl, qs, ks, vs, out, lse, L, args.steps, args.warmup) \
+    alias = aliasing_leg(torch, sess, wl, qs, ks, vs, out, lse, L, args.steps, args.warmup) \
         if m.kv_dtype == "bf16" and args.alias_v else None
 
     w = kv_elem_bytes(m.kv_dtype)
@@ -694,7 +711,7 @@ def main():
         rec["roofline"]["frac_of_blend"] = attn_tflops / blend
         rec["roofline"]["blend_peak"] = blend
     if alias:
-        rec["alias_v"] = alias
+        rec["zero_copy"] = alias
     if host:
         rec["host_tier"] = host
     rec["control_plane"] = control_plane_replay()

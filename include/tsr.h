@@ -48,7 +48,7 @@
 extern "C" {
 #endif
 
-#define TSR_ABI_VERSION 4
+#define TSR_ABI_VERSION 5
 
 typedef enum {
   TSR_OK = 0,
@@ -209,10 +209,23 @@ tsr_status tsr_plan_create(const tsr_model* model, const tsr_request* reqs,
  *             cached V is used as stored, so results equal the composed
  *             path's bit for bit.  The pool pages must stay unchanged until
  *             attention completes.  bf16 pools only (else UNSUPPORTED).
+ *   alias_k   1: K rotated on load, the other half of a zero-copy
+ *             composition (Section 5.3 places cached keys with RoPE applied
+ *             at their new positions; here the placement happens as
+ *             attention loads them).  For the same request pages as
+ *             alias_v (B gathered tokens of one HIT unit, slot for slot),
+ *             tsr_compose_kv does not write K; attention reads the cached
+ *             pre-RoPE K from the pool page and rotates it at the key's
+ *             prompt position with the same fp32 rotation and bf16 rounding
+ *             as compose, so results equal the composed path's bit for bit.
+ *             With alias_v too, such pages are not touched by compose at
+ *             all.  The pool pages must stay unchanged until attention
+ *             completes.  bf16 pools only (else UNSUPPORTED).
  *   reserved  must be zero. */
 typedef struct {
   int32_t alias_v;
-  int32_t reserved[7];
+  int32_t alias_k;
+  int32_t reserved[6];
 } tsr_plan_options;
 
 /* tsr_plan_create with options; tsr_plan_create is this with NULL.  The
@@ -286,6 +299,9 @@ int32_t tsr_plan_num_attn_items_part(const tsr_plan* plan, int32_t part);
 /* Request pages whose V attention reads from the pool (alias_v plans; 0
  * otherwise). */
 int32_t tsr_plan_num_aliased_pages(const tsr_plan* plan);
+/* Request pages whose K attention reads from the pool and rotates on load
+ * (alias_k plans; 0 otherwise). */
+int32_t tsr_plan_num_aliased_k_pages(const tsr_plan* plan);
 
 /* Prompt position and request index of every computed row, in plan order.
  * host_positions: [T] (required); host_requests: [T] or NULL. */
@@ -388,14 +404,16 @@ tsr_status tsr_attn_part(const tsr_plan* plan, int32_t part, const void* q,
                          const void* req_k, const void* req_v, const float* req_scale,
                          void* out, float* lse, void* stream);
 
-/* Attention of an alias_v plan (one part, or TSR_ATTN_ALL): as tsr_attn_part,
- * with the V of aliased request pages read from pool_v (device, the pool
- * arena tsr_compose_kv read, [n_pool_pages][H_kv][B][d] bf16).  The
- * non-aliased entry points refuse alias_v plans, and this one refuses the
- * others (INVALID_ARG). */
+/* Attention of an alias_v and/or alias_k plan (one part, or TSR_ATTN_ALL):
+ * as tsr_attn_part, with the V of V-aliased request pages read from pool_v
+ * and the K of K-aliased pages read from pool_k and rotated on load (device,
+ * the pool arenas tsr_compose_kv read, [n_pool_pages][H_kv][B][d] bf16).
+ * pool_v is required by alias_v plans and pool_k by alias_k plans (NULL
+ * otherwise).  The non-aliased entry points refuse aliased plans, and this
+ * one refuses the others (INVALID_ARG). */
 tsr_status tsr_attn_aliased(const tsr_plan* plan, int32_t part, const void* q,
-                            const void* req_k, const void* req_v, const void* pool_v,
-                            void* out, float* lse, void* stream);
+                            const void* req_k, const void* req_v, const void* pool_k,
+                            const void* pool_v, void* out, float* lse, void* stream);
 
 /* Retain (Section 5.4): for every MISS unit with retain = 1 and token j:
  *   K_pool[block j/B][slot j%B] = k (before RoPE), V_pool[...] = v

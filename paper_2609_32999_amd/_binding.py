@@ -36,7 +36,7 @@ EXPORTS = (
     "tsr_plan_num_compute_tokens", "tsr_plan_num_gather_tokens",
     "tsr_plan_num_retain_tokens", "tsr_plan_num_attn_items", "tsr_plan_attn_rows_per_item",
     "tsr_plan_num_attn_items_part", "tsr_attn_part", "tsr_plan_create_ex", "tsr_plan_create_static",
-    "tsr_plan_num_aliased_pages", "tsr_attn_aliased",
+    "tsr_plan_num_aliased_pages", "tsr_plan_num_aliased_k_pages", "tsr_attn_aliased",
     "tsr_plan_compute_positions", "tsr_plan_row_kv_lo", "tsr_plan_destroy", "tsr_compose_kv",
     "tsr_prefill_attn", "tsr_append_kv", "tsr_assemble_kv", "tsr_attn", "tsr_retain_kv",
     "tsr_cache_create", "tsr_cache_destroy", "tsr_cache_reserve", "tsr_cache_publish",
@@ -81,7 +81,7 @@ class tsr_request(ctypes.Structure):
 
 
 class tsr_plan_options(ctypes.Structure):
-    _fields_ = [("alias_v", c_int32), ("reserved", c_int32 * 7)]
+    _fields_ = [("alias_v", c_int32), ("alias_k", c_int32), ("reserved", c_int32 * 6)]
 
 
 class tsr_replay_config(ctypes.Structure):
@@ -129,6 +129,7 @@ def lib():
             "tsr_plan_attn_rows_per_item": (c_int32, [P]),
             "tsr_plan_num_attn_items_part": (c_int32, [P, c_int32]),
             "tsr_plan_num_aliased_pages": (c_int32, [P]),
+            "tsr_plan_num_aliased_k_pages": (c_int32, [P]),
             "tsr_plan_create_ex": (c_int32, [POINTER(tsr_model), POINTER(tsr_request), c_int32,
                                              c_int32, c_int32, POINTER(tsr_plan_options), P, P,
                                              c_size_t, P, POINTER(c_void_p)]),
@@ -136,7 +137,7 @@ def lib():
                                                  c_int32, c_int32, c_int32,
                                                  POINTER(tsr_plan_options), P, P,
                                                  POINTER(c_void_p)]),
-            "tsr_attn_aliased": (c_int32, [P, c_int32, P, P, P, P, P, P, P]),
+            "tsr_attn_aliased": (c_int32, [P, c_int32, P, P, P, P, P, P, P, P]),
             "tsr_plan_compute_positions": (c_int32, [P, POINTER(c_int32), POINTER(c_int32)]),
             "tsr_plan_row_kv_lo": (c_int32, [P, POINTER(c_int32)]),
             "tsr_plan_destroy": (None, [P]),
@@ -321,6 +322,10 @@ class Plan:
     def num_aliased_pages(self) -> int:
         return lib().tsr_plan_num_aliased_pages(self.handle)
 
+    @property
+    def num_aliased_k_pages(self) -> int:
+        return lib().tsr_plan_num_aliased_k_pages(self.handle)
+
     def compute_positions(self):
         T = self.num_compute_tokens
         pos = np.empty(max(T, 1), dtype=np.int32)
@@ -351,10 +356,11 @@ class Plan:
 
 def tsr_plan_create(model: tsr_model, batch: RequestBatch, n_pool_pages: int,
                     n_req_pages: int, dev_rope_table=None, dev_workspace=None,
-                    workspace_bytes: int = 0, stream=None, alias_v: bool = False) -> Plan:
+                    workspace_bytes: int = 0, stream=None, alias_v: bool = False,
+                    alias_k: bool = False) -> Plan:
     out = c_void_p()
-    if alias_v:
-        opts = tsr_plan_options(alias_v=1)
+    if alias_v or alias_k:
+        opts = tsr_plan_options(alias_v=int(alias_v), alias_k=int(alias_k))
         _check(lib().tsr_plan_create_ex(ctypes.byref(model), batch.array, batch.n,
                                         n_pool_pages, n_req_pages, ctypes.byref(opts),
                                         _ptr(dev_rope_table), _ptr(dev_workspace),
@@ -365,22 +371,24 @@ def tsr_plan_create(model: tsr_model, batch: RequestBatch, n_pool_pages: int,
                                      workspace_bytes, _stream(stream), ctypes.byref(out)))
     plan = Plan(out.value, model)
     plan.alias_v = bool(alias_v)
+    plan.alias_k = bool(alias_k)
     return plan
 
 
 def tsr_plan_create_static(model: tsr_model, batch: RequestBatch, n_pool_pages: int,
                            n_req_pages: int, dev_rope_table, stream=None,
-                           alias_v: bool = False) -> Plan:
+                           alias_v: bool = False, alias_k: bool = False) -> Plan:
     """A plan whose device image lives in the library's own plan area (no
     workspace); a later static plan on the same device supersedes it."""
     out = c_void_p()
-    opts = tsr_plan_options(alias_v=1 if alias_v else 0)
+    opts = tsr_plan_options(alias_v=int(alias_v), alias_k=int(alias_k))
     _check(lib().tsr_plan_create_static(ctypes.byref(model), batch.array, batch.n,
                                         n_pool_pages, n_req_pages, ctypes.byref(opts),
                                         _ptr(dev_rope_table), _stream(stream),
                                         ctypes.byref(out)))
     plan = Plan(out.value, model)
     plan.alias_v = bool(alias_v)
+    plan.alias_k = bool(alias_k)
     return plan
 
 
@@ -629,7 +637,8 @@ def tsr_replay(cfg: tsr_replay_config, requests, return_routes: bool = False):
     return (stats, routes[:len(requests)].copy()) if return_routes else stats
 
 
-def tsr_attn_aliased(plan: Plan, part: int, q, req_k, req_v, pool_v, out, lse=None,
+def tsr_attn_aliased(plan: Plan, part: int, q, req_k, req_v, pool_k, pool_v, out, lse=None,
                      stream=None) -> None:
     _check(lib().tsr_attn_aliased(plan.handle, part, _ptr(q), _ptr(req_k), _ptr(req_v),
-                                  _ptr(pool_v), _ptr(out), _ptr(lse), _stream(stream)))
+                                  _ptr(pool_k), _ptr(pool_v), _ptr(out), _ptr(lse),
+                                  _stream(stream)))

@@ -47,8 +47,9 @@ tsr_status check_scales(const tsr_plan* p, const float* a, const float* b,
 }
 
 tsr_status attn_common(const tsr_plan* p, int32_t part, const void* q, const void* req_k,
-                       const void* req_v, const void* pool_v, const float* req_scale,
-                       void* out, float* lse, void* stream) {
+                       const void* req_v, const void* pool_k, const void* pool_v,
+                       const float* req_scale, void* out, float* lse, void* stream,
+                       bool aliased_entry) {
   tsr_status st = check_exec(p);
   if (st != TSR_OK) return st;
   if (part < TSR_ATTN_ALL || part > TSR_ATTN_AFTER_COMPOSE) {
@@ -56,9 +57,15 @@ tsr_status attn_common(const tsr_plan* p, int32_t part, const void* q, const voi
     return TSR_ERR_INVALID_ARG;
   }
   if ((st = check_scales(p, nullptr, req_scale, false, true)) != TSR_OK) return st;
-  if (p->alias_v != (pool_v != nullptr)) {
-    set_error(p->alias_v ? "the plan reads V from the pool: use tsr_attn_aliased with pool_v"
-                         : "tsr_attn_aliased needs a plan created with alias_v");
+  const bool aliased = p->alias_v || p->alias_k;
+  if (aliased != aliased_entry) {
+    set_error(aliased ? "the plan reads K or V from the pool: use tsr_attn_aliased"
+                      : "tsr_attn_aliased needs a plan created with alias_v or alias_k");
+    return TSR_ERR_INVALID_ARG;
+  }
+  if (p->alias_v != (pool_v != nullptr) || p->alias_k != (pool_k != nullptr)) {
+    set_error("tsr_attn_aliased: pass pool_v exactly for alias_v plans and pool_k exactly "
+              "for alias_k plans");
     return TSR_ERR_INVALID_ARG;
   }
   if (p->T == 0) return TSR_OK;
@@ -71,7 +78,7 @@ tsr_status attn_common(const tsr_plan* p, int32_t part, const void* q, const voi
   hipStream_t s = static_cast<hipStream_t>(stream);
   hipError_t e = is_e4m3(p)
                      ? launch_attn_e4m3(p, items, n, q, req_k, req_v, req_scale, out, lse, s)
-                     : launch_attn(p, items, n, pool_v, q, req_k, req_v, out, lse, s);
+                     : launch_attn(p, items, n, pool_k, pool_v, q, req_k, req_v, out, lse, s);
   if (e != hipSuccess) return device_fail("attention launch", e);
   return TSR_OK;
 }
@@ -133,7 +140,8 @@ size_t tsr_plan_workspace_size(const tsr_model* model, const tsr_request* reqs,
   size_t bytes = 0;
   guarded([&]() -> tsr_status {
     tsr_plan tmp{};
-    tsr_status st = build_plan(model, reqs, n_req, n_pool_pages, n_req_pages, false, &tmp);
+    tsr_status st = build_plan(model, reqs, n_req, n_pool_pages, n_req_pages, false, false,
+                               &tmp);
     if (st == TSR_OK) bytes = tmp.ws_bytes;
     return st;
   });
@@ -160,7 +168,7 @@ tsr_status tsr_plan_create_ex(const tsr_model* model, const tsr_request* reqs,
       return TSR_ERR_INVALID_ARG;
     }
     *out_plan = nullptr;
-    bool alias_v = false;
+    bool alias_v = false, alias_k = false;
     if (options) {
       for (int32_t r : options->reserved)
         if (r != 0) {
@@ -171,10 +179,16 @@ tsr_status tsr_plan_create_ex(const tsr_model* model, const tsr_request* reqs,
         set_error("tsr_plan_options.alias_v must be 0 or 1");
         return TSR_ERR_INVALID_ARG;
       }
+      if (options->alias_k != 0 && options->alias_k != 1) {
+        set_error("tsr_plan_options.alias_k must be 0 or 1");
+        return TSR_ERR_INVALID_ARG;
+      }
       alias_v = options->alias_v == 1;
+      alias_k = options->alias_k == 1;
     }
     tsr_plan* p = new tsr_plan();
-    tsr_status st = build_plan(model, reqs, n_req, n_pool_pages, n_req_pages, alias_v, p);
+    tsr_status st = build_plan(model, reqs, n_req, n_pool_pages, n_req_pages, alias_v,
+                               alias_k, p);
     if (st != TSR_OK) {
       delete p;
       return st;
@@ -209,6 +223,7 @@ tsr_status tsr_plan_create_ex(const tsr_model* model, const tsr_request* reqs,
         p->dev.items_part[q] = reinterpret_cast<const AttnItem*>(base + p->off_items_part[q]);
       p->dev.block_tables = reinterpret_cast<const int32_t*>(base + p->off_bt);
       p->dev.v_block_tables = reinterpret_cast<const int32_t*>(base + p->off_vbt);
+      p->dev.k_block_tables = reinterpret_cast<const int32_t*>(base + p->off_kbt);
       p->dev.gpages = reinterpret_cast<const PageDesc*>(base + p->off_gpages);
       p->dev.apages = reinterpret_cast<const PageDesc*>(base + p->off_apages);
       p->dev.rpages = reinterpret_cast<const PageDesc*>(base + p->off_rpages);
@@ -230,6 +245,7 @@ int32_t tsr_plan_attn_rows_per_item(const tsr_plan* p) {
   return p ? kTileRows * p->row_blocks : -1;
 }
 int32_t tsr_plan_num_aliased_pages(const tsr_plan* p) { return p ? p->n_aliased : -1; }
+int32_t tsr_plan_num_aliased_k_pages(const tsr_plan* p) { return p ? p->n_aliased_k : -1; }
 
 int32_t tsr_plan_num_attn_items_part(const tsr_plan* p, int32_t part) {
   if (!p || part < TSR_ATTN_ALL || part > TSR_ATTN_AFTER_COMPOSE) return -1;
@@ -312,8 +328,8 @@ tsr_status tsr_prefill_attn(const tsr_plan* p, const void* q, const void* k,
       set_error("prefill_attn: a required pointer is NULL");
       return TSR_ERR_INVALID_ARG;
     }
-    if (p->alias_v) {
-      set_error("the plan reads V from the pool: use tsr_append_kv and tsr_attn_aliased");
+    if (p->alias_v || p->alias_k) {
+      set_error("the plan reads K or V from the pool: use tsr_append_kv and tsr_attn_aliased");
       return TSR_ERR_INVALID_ARG;
     }
     // Every check is above: from here on only a launch failure reported by
@@ -325,7 +341,7 @@ tsr_status tsr_prefill_attn(const tsr_plan* p, const void* q, const void* k,
     if (e != hipSuccess) return device_fail("append launch", e);
     e = is_e4m3(p) ? launch_attn_e4m3(p, p->dev.items, p->n_items, q, req_k, req_v,
                                       req_scale, out, lse, s)
-                   : launch_attn(p, p->dev.items, p->n_items, nullptr, q, req_k, req_v, out,
+                   : launch_attn(p, p->dev.items, p->n_items, nullptr, nullptr, q, req_k, req_v, out,
                                  lse, s);
     if (e != hipSuccess) return device_fail("attention launch", e);
     return TSR_OK;
@@ -380,19 +396,21 @@ tsr_status tsr_attn_part(const tsr_plan* p, int32_t part, const void* q,
                          const void* req_k, const void* req_v, const float* req_scale,
                          void* out, float* lse, void* stream) {
   return guarded([&]() -> tsr_status {
-    return attn_common(p, part, q, req_k, req_v, nullptr, req_scale, out, lse, stream);
+    return attn_common(p, part, q, req_k, req_v, nullptr, nullptr, req_scale, out, lse, stream,
+                       false);
   });
 }
 
 tsr_status tsr_attn_aliased(const tsr_plan* p, int32_t part, const void* q,
-                            const void* req_k, const void* req_v, const void* pool_v,
-                            void* out, float* lse, void* stream) {
+                            const void* req_k, const void* req_v, const void* pool_k,
+                            const void* pool_v, void* out, float* lse, void* stream) {
   return guarded([&]() -> tsr_status {
-    if (!pool_v) {
-      set_error("tsr_attn_aliased: pool_v is NULL");
+    if (!pool_k && !pool_v) {
+      set_error("tsr_attn_aliased: pool_k and pool_v are both NULL");
       return TSR_ERR_INVALID_ARG;
     }
-    return attn_common(p, part, q, req_k, req_v, pool_v, nullptr, out, lse, stream);
+    return attn_common(p, part, q, req_k, req_v, pool_k, pool_v, nullptr, out, lse, stream,
+                       true);
   });
 }
 

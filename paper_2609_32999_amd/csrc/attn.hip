@@ -210,14 +210,21 @@ using MaskBoth = std::integral_constant<int, kMaskBoth>;
 // AV: V aliasing -- the V of a 16-key block comes from the page the V block
 // table names, a pool page when kPoolPageFlag is set (else the request page
 // the K block table names).
+// AK: K rotated on load -- the K of a 16-key block comes from the page the K
+// block table names; a pool page (kPoolPageFlag) holds the cached keys before
+// RoPE, which the staging waves rotate at the keys' positions (fp32 table,
+// no fused multiply-add, bf16 rounding: the arithmetic of compose) and write
+// to LDS in fragment order.
 // R: row blocks per workgroup.  Waves 4 b .. 4 b + 3 own the 32 rows of row
 // block b; the first four waves stage every K/V tile for all of them.
-template <int G, bool AV, int R>
+template <int G, bool AV, bool AK, int R>
 __global__ __launch_bounds__(256 * R, 3) void attn_mfma_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc,
-    const uint16_t* __restrict__ vc, const uint16_t* __restrict__ pool_v,
+    const uint16_t* __restrict__ vc, const uint16_t* __restrict__ pool_k,
+    const uint16_t* __restrict__ pool_v,
     const AttnItem* __restrict__ items, const int32_t* __restrict__ bts,
-    const int32_t* __restrict__ vbts, const RowDesc* __restrict__ rows,
+    const int32_t* __restrict__ vbts, const int32_t* __restrict__ kbts,
+    const RowDesc* __restrict__ rows,
     const float* __restrict__ rope_cos, const float* __restrict__ rope_sin,
     uint16_t* __restrict__ out, float* __restrict__ lse, int n_q_heads,
     int n_kv_heads, int log2_page, float scale, float scale_log2e) {
@@ -242,7 +249,8 @@ __global__ __launch_bounds__(256 * R, 3) void attn_mfma_kernel(
   const int lh = lane >> 5;
   const int g = it.kv_head;
   const int page_mask = (1 << log2_page) - 1;
-  const int32_t* bt = bts + it.bt_off;
+  // the K block table (pool pages flagged when K is rotated on load)
+  const int32_t* bt = (AK ? kbts : bts) + it.bt_off;
 
   const int rbase = 32 * rb;
   const int row = it.row0 + min(rbase + lrow, it.n_rows - 1);
@@ -296,16 +304,24 @@ __global__ __launch_bounds__(256 * R, 3) void attn_mfma_kernel(
   };
   // Issues tile j's loads: K directly into the LDS buffer kt, V into
   // registers (written to LDS as V^T by store_tile).
+  // K rotated on load: the staging thread's key (kk) and 8-dim chunk of each
+  // RoPE half, its raw K, and whether its block is a pool page
+  const int kk = tid & 31, kch = (tid >> 5) & 7;
+  uint4 kraw[2];
+  bool krot = false, kreg = false;
   auto load_tile = [&](int j, int pid, uint8_t* kt) __attribute__((always_inline)) {
     const int key0 = j * kKT;
     const int p0 = __builtin_amdgcn_readlane(pid, 0), p1 = __builtin_amdgcn_readlane(pid, 1);
-    const int64_t b0 = block_base(p0, key0), b1 = block_base(p1, key0 + 16);
+    const int64_t b0 = block_base(p0 & ~kPoolPageFlag, key0);
+    const int64_t b1 = block_base(p1 & ~kPoolPageFlag, key0 + 16);
     int64_t vbase = vb ? b1 : b0;
     const uint16_t* vsrc = vc;
-    if constexpr (AV) {
+    if constexpr (AV || AK) {
+      // the V page: from the V block table (flagged pool pages) with V
+      // aliasing, else the request page of the unflagged block table
       const int kv = key0 + 16 * vb;
-      const int32_t vp = vbts[it.bt_off + min(kv >> log2_page, it.n_pages - 1)];
-      vsrc = (vp & kPoolPageFlag) ? pool_v : vc;
+      const int32_t vp = (AV ? vbts : bts)[it.bt_off + min(kv >> log2_page, it.n_pages - 1)];
+      vsrc = (AV && (vp & kPoolPageFlag)) ? pool_v : vc;
       vbase = block_base(vp & ~kPoolPageFlag, kv);
     }
 #pragma unroll
@@ -319,10 +335,58 @@ __global__ __launch_bounds__(256 * R, 3) void attn_mfma_kernel(
       for (int i = 0; i < 2; ++i)
         if (key0 + 2 * kp + i >= it.kv_len) vr[i] = make_uint4(0, 0, 0, 0);
     }
+    if constexpr (AK) {
+      kreg = ((p0 | p1) & kPoolPageFlag) != 0;
+      if (kreg) {
+        // through registers: rotated (pool block) or copied (request block)
+        // by store_tile
+        const int kb = kk >> 4;
+        const int pg = kb ? p1 : p0;
+        krot = (pg & kPoolPageFlag) != 0;
+        const uint16_t* src = (krot ? pool_k : kc) +
+                              block_base(pg & ~kPoolPageFlag, key0 + kk) + 8 * kch;
+        kraw[0] = *reinterpret_cast<const uint4*>(src);
+        kraw[1] = *reinterpret_cast<const uint4*>(src + kD / 2);
+        return;
+      }
+    }
     const uint16_t* ksrc = kc + (khi ? b1 : b0) + klane;
     const uint32_t kdst = lds_addr(kt) + 2 * w * kKBlk;
     lds_dma16(ksrc, kdst);
     lds_dma16(ksrc + 16, kdst + kKBlk);
+  };
+  // K through registers (rotated on load): to LDS in fragment order, block
+  // kst holding dims 16 kst .. (lane l: key l % 32, dims + 8 (l / 32))
+  auto store_k = [&](int j, uint8_t* kt) __attribute__((always_inline)) {
+    float lo[8], hi[8];
+    const uint32_t wl[4] = {kraw[0].x, kraw[0].y, kraw[0].z, kraw[0].w};
+    const uint32_t wh[4] = {kraw[1].x, kraw[1].y, kraw[1].z, kraw[1].w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      lo[2 * e] = bf16_to_f32(wl[e] & 0xffffu);
+      lo[2 * e + 1] = bf16_to_f32(wl[e] >> 16);
+      hi[2 * e] = bf16_to_f32(wh[e] & 0xffffu);
+      hi[2 * e + 1] = bf16_to_f32(wh[e] >> 16);
+    }
+    uint4 a = kraw[0], b = kraw[1];
+    if (krot) {
+      const int pk = j * kKT + kk;
+      float c[8], sn[8];
+      load8(rope_cos + (int64_t)pk * (kD / 2) + 8 * kch, c);
+      load8(rope_sin + (int64_t)pk * (kD / 2) + 8 * kch, sn);
+      rope_rotate<8>(lo, hi, c, sn);
+      a.x = f32_to_bf16(lo[0]) | (f32_to_bf16(lo[1]) << 16);
+      a.y = f32_to_bf16(lo[2]) | (f32_to_bf16(lo[3]) << 16);
+      a.z = f32_to_bf16(lo[4]) | (f32_to_bf16(lo[5]) << 16);
+      a.w = f32_to_bf16(lo[6]) | (f32_to_bf16(lo[7]) << 16);
+      b.x = f32_to_bf16(hi[0]) | (f32_to_bf16(hi[1]) << 16);
+      b.y = f32_to_bf16(hi[2]) | (f32_to_bf16(hi[3]) << 16);
+      b.z = f32_to_bf16(hi[4]) | (f32_to_bf16(hi[5]) << 16);
+      b.w = f32_to_bf16(hi[6]) | (f32_to_bf16(hi[7]) << 16);
+    }
+    const int lofs = (kk + 32 * (kch & 1)) * 16;
+    *reinterpret_cast<uint4*>(kt + (kch >> 1) * kKBlk + lofs) = a;
+    *reinterpret_cast<uint4*>(kt + (4 + (kch >> 1)) * kKBlk + lofs) = b;
   };
   auto store_tile = [&](uint16_t* vs) __attribute__((always_inline)) {
     const uint32_t* v0 = reinterpret_cast<const uint32_t*>(&vr[0]);
@@ -470,7 +534,10 @@ __global__ __launch_bounds__(256 * R, 3) void attn_mfma_kernel(
         pid = fetch_pages(j + 2);
       }
       if (!SKIP || j < my_ntiles) tile(j, mask_tag, kl[j & 1], vl[j & 1]);
-      if (more) store_tile(vl[(j + 1) & 1]);
+      if (more) {
+        store_tile(vl[(j + 1) & 1]);
+        if (AK && kreg) store_k(j + 1, kl[(j + 1) & 1]);
+      }
       __builtin_amdgcn_s_waitcnt(kWaitVm0);
       __syncthreads();
     }
@@ -512,7 +579,10 @@ __global__ __launch_bounds__(256 * R, 3) void attn_mfma_kernel(
       qraw[ks + 4] = *reinterpret_cast<const uint4*>(qp + d0 + kD / 2);
     }
   }
-  if (stager) store_tile(vl[j0 & 1]);
+  if (stager) {
+    store_tile(vl[j0 & 1]);
+    if (AK && kreg) store_k(j0, kl[j0 & 1]);
+  }
   __builtin_amdgcn_s_waitcnt(kWaitVm0);
   __syncthreads();
   // ---- rotated queries as bf16 B operands: lane = query row, k = head dim
@@ -579,8 +649,9 @@ int ilog2(int x) {
 }  // namespace
 
 hipError_t launch_attn(const tsr_plan* p, const AttnItem* items, int32_t n_items,
-                       const void* pool_v, const void* q, const void* req_k,
-                       const void* req_v, void* out, float* lse, hipStream_t s) {
+                       const void* pool_k, const void* pool_v, const void* q,
+                       const void* req_k, const void* req_v, void* out, float* lse,
+                       hipStream_t s) {
   if (n_items == 0 || p->T == 0) return hipSuccess;
   const tsr_model& m = p->model;
   const int lp = ilog2(m.page_size);
@@ -605,32 +676,34 @@ hipError_t launch_attn(const tsr_plan* p, const AttnItem* items, int32_t n_items
     return hipGetLastError();
   }
   const float sl2e = (float)((double)p->scale * 1.4426950408889634);
-#define TSR_MFMA(GG, AV)                                                           \
+#define TSR_MFMA(GG, AV, AK)                                                       \
   if (p->row_blocks == kMaxRowBlocks)                                              \
-    TSR_MFMA_R(GG, AV, kMaxRowBlocks);                                             \
+    TSR_MFMA_R(GG, AV, AK, kMaxRowBlocks);                                         \
   else                                                                             \
-    TSR_MFMA_R(GG, AV, 1)
-#define TSR_MFMA_R(GG, AV, RB)                                                     \
-  hipLaunchKernelGGL((attn_mfma_kernel<GG, AV, RB>), grid, dim3(256 * (RB)), 0, s, \
+    TSR_MFMA_R(GG, AV, AK, 1)
+#define TSR_MFMA_R(GG, AV, AK, RB)                                                 \
+  hipLaunchKernelGGL((attn_mfma_kernel<GG, AV, AK, RB>), grid, dim3(256 * (RB)), 0, s, \
                      static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(req_k), \
                      static_cast<const uint16_t*>(req_v),                          \
+                     static_cast<const uint16_t*>(pool_k),                         \
                      static_cast<const uint16_t*>(pool_v), items,                  \
-                     p->dev.block_tables, p->dev.v_block_tables, p->dev.rows,       \
-                     p->dev.rope_cos,                                               \
+                     p->dev.block_tables, p->dev.v_block_tables,                    \
+                     p->dev.k_block_tables, p->dev.rows, p->dev.rope_cos,           \
                      p->dev.rope_sin, static_cast<uint16_t*>(out), lse,             \
                      m.n_q_heads, m.n_kv_heads, lp, p->scale, sl2e)
-  const bool av = pool_v != nullptr;
-  switch (G * 2 + (av ? 1 : 0)) {
-    case 2: TSR_MFMA(1, false); break;
-    case 3: TSR_MFMA(1, true); break;
-    case 4: TSR_MFMA(2, false); break;
-    case 5: TSR_MFMA(2, true); break;
-    case 8: TSR_MFMA(4, false); break;
-    case 9: TSR_MFMA(4, true); break;
-    case 16: TSR_MFMA(8, false); break;
-    case 17: TSR_MFMA(8, true); break;
+#define TSR_MFMA_G(GG)                                                             \
+  if (p->alias_v && p->alias_k) TSR_MFMA(GG, true, true);                          \
+  else if (p->alias_v) TSR_MFMA(GG, true, false);                                  \
+  else if (p->alias_k) TSR_MFMA(GG, false, true);                                  \
+  else TSR_MFMA(GG, false, false)
+  switch (G) {
+    case 1: TSR_MFMA_G(1); break;
+    case 2: TSR_MFMA_G(2); break;
+    case 4: TSR_MFMA_G(4); break;
+    case 8: TSR_MFMA_G(8); break;
     default: return hipErrorInvalidValue;
   }
+#undef TSR_MFMA_G
 #undef TSR_MFMA
 #undef TSR_MFMA_R
   return hipGetLastError();

@@ -93,11 +93,13 @@ __device__ __forceinline__ void move_tokens(
   dst_v += layer * dst_layer_stride;
 
   int32_t src, dst, pos = 0;
-  bool move_v = true;         // false: attention reads this token's V from the pool
+  // false: attention reads this token's V (K) from the pool (aliasing)
+  bool move_v = true, move_k = true;
   if constexpr (MODE == kCompose) {
     const GatherDesc gd = static_cast<const GatherDesc*>(descs)[i];
     src = gd.src; dst = gd.dst; pos = gd.pos;
-    move_v = gd.k_only == 0;
+    move_v = (gd.skip & kSkipV) == 0;
+    move_k = (gd.skip & kSkipK) == 0;
   } else if constexpr (MODE == kAppend) {
     const RowDesc rd = static_cast<const RowDesc*>(descs)[i];
     src = i; dst = rd.dst; pos = rd.pos;
@@ -134,8 +136,10 @@ __device__ __forceinline__ void move_tokens(
       const int h = hb + b * kHeadStep;
       if (h < n_kv_heads) {
         const int64_t sb = src_off(h);
-        kl[b].load(src_k + sb + lo);
-        kh[b].load(src_k + sb + hi);
+        if (move_k) {
+          kl[b].load(src_k + sb + lo);
+          kh[b].load(src_k + sb + hi);
+        }
         if (move_v) {
           vl[b].load(src_v + sb + lo);
           vh[b].load(src_v + sb + hi);
@@ -154,7 +158,7 @@ __device__ __forceinline__ void move_tokens(
         if constexpr (MODE == kRetain) {
           kl[b].store(dst_k + db + lo);
           kh[b].store(dst_k + db + hi);
-        } else {
+        } else if (move_k) {
           float a[8], bb[8];
           kl[b].to_f32(a);
           kh[b].to_f32(bb);

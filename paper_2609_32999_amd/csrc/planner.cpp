@@ -92,7 +92,7 @@ tsr_status check_model(const tsr_model* m) {
 
 tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
                       int32_t n_req, int32_t n_pool_pages, int32_t n_req_pages,
-                      bool alias_v, tsr_plan* p) {
+                      bool alias_v, bool alias_k, tsr_plan* p) {
   tsr_status st = check_model(model);
   if (st != TSR_OK) return st;
   if (n_req < 0) return fail(TSR_ERR_INVALID_ARG, "n_req < 0");
@@ -118,13 +118,19 @@ tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
     return fail(TSR_ERR_UNSUPPORTED, "V aliasing is built for bf16 pools only");
   if (alias_v && (int64_t)n_pool_pages >= kPoolPageFlag)
     return fail(TSR_ERR_OUT_OF_RANGE, "V aliasing needs pool page ids below 2^30");
+  p->alias_k = alias_k;
+  p->n_aliased_k = 0;
+  if (alias_k && (m.kv_dtype != TSR_BF16 || m.act_dtype != TSR_BF16))
+    return fail(TSR_ERR_UNSUPPORTED, "K rotated on load is built for bf16 pools only");
+  if (alias_k && (int64_t)n_pool_pages >= kPoolPageFlag)
+    return fail(TSR_ERR_OUT_OF_RANGE, "K aliasing needs pool page ids below 2^30");
 
   const bool e4m3 = m.kv_dtype == TSR_E4M3;
   std::vector<PageDesc> gpages, apages, rpages;
   std::vector<GatherDesc> gather;
   std::vector<RowDesc> rows;
   std::vector<RetainDesc> retain;
-  std::vector<int32_t> bts, vbts;
+  std::vector<int32_t> bts, vbts, kbts;
   std::vector<int32_t> bt_off(n_req), bt_len(n_req), req_row0(n_req + 1, 0);
   // per request, the position ranges [a, b) that compose fills
   std::vector<std::vector<std::pair<int32_t, int32_t>>> gathered(n_req);
@@ -225,6 +231,7 @@ tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
       req_page_used[pg] = 1;
       bts.push_back(pg);
       vbts.push_back(pg);
+      kbts.push_back(pg);
     }
     auto req_slot = [&](int32_t pos) {
       return q.block_table[pos / B] * B + pos % B;
@@ -311,20 +318,31 @@ tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
       if (hit) {
         if (ncomp < u.n_tokens)
           gathered[r].push_back({u.position + ncomp, u.position + u.n_tokens});
-        // V aliasing: a request page that holds B gathered tokens of this
+        // Aliasing: a request page that holds B gathered tokens of this
         // unit, slot for slot (the unit starts on a page boundary), reads
-        // its V from the pool page; compose then writes only its K
-        int32_t ab0 = 0, ab1 = 0;              // aliased unit blocks [ab0, ab1)
-        if (alias_v && u.position % B == 0) {
+        // its V (alias_v) and/or its pre-RoPE K (alias_k, rotated on load)
+        // from the pool page; compose then skips that half (both: the
+        // tokens are not moved at all)
+        int32_t ab0 = 0, ab1 = 0;              // aliasable unit blocks [ab0, ab1)
+        if ((alias_v || alias_k) && u.position % B == 0) {
           ab0 = (ncomp + B - 1) / B;
           ab1 = std::max(ab0, u.n_tokens / B);
-          for (int32_t b = ab0; b < ab1; ++b)
-            vbts[bt_off[r] + u.position / B + b] = u.pool_pages[b] | kPoolPageFlag;
-          p->n_aliased += ab1 - ab0;
+          for (int32_t b = ab0; b < ab1; ++b) {
+            if (alias_v)
+              vbts[bt_off[r] + u.position / B + b] = u.pool_pages[b] | kPoolPageFlag;
+            if (alias_k)
+              kbts[bt_off[r] + u.position / B + b] = u.pool_pages[b] | kPoolPageFlag;
+          }
+          if (alias_v) p->n_aliased += ab1 - ab0;
+          if (alias_k) p->n_aliased_k += ab1 - ab0;
         }
-        for (int32_t j = ncomp; j < u.n_tokens; ++j)
+        const int32_t skip = (alias_v ? kSkipV : 0) | (alias_k ? kSkipK : 0);
+        for (int32_t j = ncomp; j < u.n_tokens; ++j) {
+          const bool aliased = j / B >= ab0 && j / B < ab1;
+          if (aliased && skip == (kSkipV | kSkipK)) continue;   // nothing to move
           gather.push_back({u.pool_pages[j / B] * B + j % B, req_slot(u.position + j),
-                            u.position + j, (j / B >= ab0 && j / B < ab1) ? 1 : 0});
+                            u.position + j, aliased ? skip : 0});
+        }
       } else if (keep) {
         for (int32_t j = 0; j < u.n_tokens; ++j)
           retain.push_back({row0 + j, u.pool_pages[j / B] * B + j % B});
@@ -466,6 +484,7 @@ tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
   }
   p->off_bt = off;      off = align_up(off + bts.size() * sizeof(int32_t), 256);
   p->off_vbt = off;     off = align_up(off + vbts.size() * sizeof(int32_t), 256);
+  p->off_kbt = off;     off = align_up(off + kbts.size() * sizeof(int32_t), 256);
   p->off_gpages = off;  off = align_up(off + gpages.size() * sizeof(PageDesc), 256);
   p->off_apages = off;  off = align_up(off + apages.size() * sizeof(PageDesc), 256);
   p->off_rpages = off;  off = align_up(off + rpages.size() * sizeof(PageDesc), 256);
@@ -485,6 +504,7 @@ tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
     put(p->off_items_part[q], order_part[q].data(), order_part[q].size() * sizeof(AttnItem));
   put(p->off_bt, bts.data(), bts.size() * sizeof(int32_t));
   put(p->off_vbt, vbts.data(), vbts.size() * sizeof(int32_t));
+  put(p->off_kbt, kbts.data(), kbts.size() * sizeof(int32_t));
   put(p->off_gpages, gpages.data(), gpages.size() * sizeof(PageDesc));
   put(p->off_apages, apages.data(), apages.size() * sizeof(PageDesc));
   put(p->off_rpages, rpages.data(), rpages.size() * sizeof(PageDesc));

@@ -37,8 +37,9 @@ struct alignas(16) GatherDesc {
   int32_t src;
   int32_t dst;
   int32_t pos;
-  int32_t k_only;   // 1: V is read from the pool page by attention (aliased)
+  int32_t skip;     // kSkipV / kSkipK: attention reads that half from the pool
 };
+constexpr int32_t kSkipV = 1, kSkipK = 2;
 
 // A computed row: its request slot and prompt position.
 struct alignas(8) RowDesc {
@@ -90,7 +91,8 @@ struct PlanDev {
   const AttnItem* items;
   const AttnItem* items_part[2];
   const int32_t* block_tables;
-  const int32_t* v_block_tables;  // block_tables, with aliased pages flagged
+  const int32_t* v_block_tables;  // block_tables, with V-aliased pages flagged
+  const int32_t* k_block_tables;  // block_tables, with K-aliased pages flagged
   const PageDesc* gpages;  // e4m3 plans only
   const PageDesc* apages;
   const PageDesc* rpages;
@@ -123,6 +125,9 @@ struct tsr_plan {
   size_t off_vbt;
   bool alias_v;               // V of whole gathered pages read from the pool
   int32_t n_aliased;          // request pages whose V is read from the pool
+  bool alias_k;               // K of whole gathered pages rotated on load
+  int32_t n_aliased_k;        // request pages whose K is read from the pool
+  size_t off_kbt;
   size_t off_gpages, off_apages, off_rpages;
   const void* rope_table;   // device
   void* ws;                 // device, NULL for host-only plans
@@ -172,7 +177,7 @@ tsr_status check_model(const tsr_model* m);
 // Build a plan's host part (validation + descriptors + image layout).
 tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
                       int32_t n_req, int32_t n_pool_pages, int32_t n_req_pages,
-                      bool alias_v, tsr_plan* plan);
+                      bool alias_v, bool alias_k, tsr_plan* plan);
 
 // Kernel launchers (return hipSuccess or the launch error).
 hipError_t launch_compose(const tsr_plan* p, const void* pool_k,
@@ -191,8 +196,9 @@ hipError_t launch_assemble_e4m3(const tsr_plan* p, const void* pool_k, const voi
 // Attention launchers run `n_items` items from `items` (a plan's full
 // schedule or one of its parts).
 hipError_t launch_attn(const tsr_plan* p, const AttnItem* items, int32_t n_items,
-                       const void* pool_v, const void* q, const void* req_k,
-                       const void* req_v, void* out, float* lse, hipStream_t s);
+                       const void* pool_k, const void* pool_v, const void* q,
+                       const void* req_k, const void* req_v, void* out, float* lse,
+                       hipStream_t s);
 hipError_t launch_retain(const tsr_plan* p, const void* k, const void* v,
                          void* pool_k, void* pool_v, hipStream_t s);
 

@@ -101,27 +101,29 @@ class Session:
         B.tsr_rope_table_init(self.model, self.rope, nbytes, self.stream)
 
     # ------------------------------------------------------------- plans
-    def plan(self, requests, stream=None, alias_v: bool = False):
+    def plan(self, requests, stream=None, alias_v: bool = False, alias_k: bool = False):
         """Validate and upload a batch's plan; `alias_v` selects V aliasing
-        (attention reads V of whole gathered pages from the pool)."""
+        (attention reads V of whole gathered pages from the pool), `alias_k`
+        K rotated on load (attention reads their pre-RoPE K from the pool)."""
         batch = B.RequestBatch(requests)
         ws_bytes = B.tsr_plan_workspace_size(self.model, batch, self.n_pool_pages,
                                              self.n_req_pages)
         ws = torch.empty(ws_bytes, dtype=torch.uint8, device=self.device)
         plan = B.tsr_plan_create(self.model, batch, self.n_pool_pages, self.n_req_pages,
                                  self.rope, ws, ws_bytes, stream or self.stream,
-                                 alias_v=alias_v)
+                                 alias_v=alias_v, alias_k=alias_k)
         plan.workspace = ws     # keep the workspace alive with the plan
         plan.batch = batch
         return plan
 
-    def plan_static(self, requests, stream=None, alias_v: bool = False):
+    def plan_static(self, requests, stream=None, alias_v: bool = False,
+                    alias_k: bool = False):
         """A plan in the library's own device plan area (no workspace is
         allocated); a later static plan on this device supersedes it."""
         batch = B.RequestBatch(requests)
         plan = B.tsr_plan_create_static(self.model, batch, self.n_pool_pages,
                                         self.n_req_pages, self.rope, stream or self.stream,
-                                        alias_v=alias_v)
+                                        alias_v=alias_v, alias_k=alias_k)
         plan.batch = batch
         return plan
 
@@ -165,7 +167,8 @@ class Session:
         return out, lse
 
     def prefill_attn(self, plan, q, k, v, out, lse=None, layer: int = 0, stream=None):
-        if getattr(plan, "alias_v", False):       # append, then attention with pool V
+        if getattr(plan, "alias_v", False) or getattr(plan, "alias_k", False):
+            # append, then attention with pool K / V
             self.append(plan, k, v, layer=layer, stream=stream)
             self.attn(plan, q, out, lse, layer=layer, stream=stream)
             return
@@ -185,9 +188,12 @@ class Session:
     def attn(self, plan, q, out, lse=None, layer: int = 0, stream=None, part: int = 0):
         """Attention over the assembled pages; `part` selects all items
         (TSR_ATTN_ALL) or the items before / after compose."""
-        if getattr(plan, "alias_v", False):
+        av, ak = getattr(plan, "alias_v", False), getattr(plan, "alias_k", False)
+        if av or ak:
             B.tsr_attn_aliased(plan, part, q, self.req_k[layer], self.req_v[layer],
-                               self._pv(layer), out, lse, stream or self.stream)
+                               self._pk(layer) if ak else None,
+                               self._pv(layer) if av else None, out, lse,
+                               stream or self.stream)
             return
         B.tsr_attn_part(plan, part, q, self.req_k[layer], self.req_v[layer], self._rs(layer),
                         out, lse, stream or self.stream)
