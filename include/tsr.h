@@ -48,7 +48,7 @@
 extern "C" {
 #endif
 
-#define TSR_ABI_VERSION 5
+#define TSR_ABI_VERSION 6
 
 typedef enum {
   TSR_OK = 0,
@@ -221,15 +221,43 @@ tsr_status tsr_plan_create(const tsr_model* model, const tsr_request* reqs,
  *             With alias_v too, such pages are not touched by compose at
  *             all.  The pool pages must stay unchanged until attention
  *             completes.  bf16 pools only (else UNSUPPORTED).
+ *   split_tiles  key-range splitting of long attention items (bf16 plans
+ *             whose items hold one 32-row block; other plans ignore it).
+ *             An item whose keys span more than S tiles of 32 keys runs as
+ *             ceil(tiles / S) items over consecutive key ranges, each
+ *             writing its rows' normalized output and log-sum-exp in fp32
+ *             to a buffer in the plan workspace; a second kernel on the
+ *             same stream merges them (o = sum_c exp(lse_c - lse) o_c,
+ *             lse = log sum_c exp(lse_c)) into out and lse.  Without it a
+ *             launch lasts at least as long as its longest item: under
+ *             TSR_SCOPE_LOCAL the rows after the units attend to the whole
+ *             prompt while most rows attend within a short unit.
+ *               0   automatic: S = the launch's mean key tiles per compute
+ *                   unit (256 units, 32 tiles at least), so only items
+ *                   that would outlast the rest of the launch are split;
+ *                   never for tsr_plan_create_static;
+ *               >0  S = split_tiles;
+ *               -1  never split.
+ *             A plan with split items writes that buffer on every
+ *             attention call: calls that use one plan on streams that
+ *             run concurrently race there.
  *   reserved  must be zero. */
 typedef struct {
   int32_t alias_v;
   int32_t alias_k;
-  int32_t reserved[6];
+  int32_t split_tiles;
+  int32_t reserved[5];
 } tsr_plan_options;
 
+/* tsr_plan_workspace_size for a plan made with `options` (NULL: all zero,
+ * which is what tsr_plan_workspace_size assumes); the key-range split
+ * buffer depends on split_tiles. */
+size_t tsr_plan_workspace_size_ex(const tsr_model* model, const tsr_request* reqs,
+                                  int32_t n_req, int32_t n_pool_pages, int32_t n_req_pages,
+                                  const tsr_plan_options* options);
+
 /* tsr_plan_create with options; tsr_plan_create is this with NULL.  The
- * workspace size does not depend on the options. */
+ * workspace must hold tsr_plan_workspace_size_ex(..., options) bytes. */
 tsr_status tsr_plan_create_ex(const tsr_model* model, const tsr_request* reqs,
                               int32_t n_req, int32_t n_pool_pages, int32_t n_req_pages,
                               const tsr_plan_options* options, const void* dev_rope_table,
@@ -242,7 +270,8 @@ tsr_status tsr_plan_create_ex(const tsr_model* model, const tsr_request* reqs,
  * written (hipMemcpyAsync on `stream`) into a plan area the library owns on
  * the current device, a static device array of 16 MiB that each GPU holds
  * until the process ends; the call allocates no device memory.
- *   - A batch whose image exceeds 16 MiB (tsr_plan_workspace_size) is
+ *   - A batch whose image exceeds 16 MiB (tsr_plan_workspace_size_ex with
+ *     these options; split_tiles = 0 means no key-range splitting here) is
  *     refused with TSR_ERR_OUT_OF_RANGE before any HIP call.
  *   - Every static plan on a device shares that area: creating one rewrites
  *     it, and the plans it replaced are refused from then on
@@ -271,6 +300,9 @@ int32_t tsr_plan_num_attn_items(const tsr_plan* plan);
 /* Most computed rows an attention item of this plan holds: 32, or 96 when
  * the bf16 kernel runs three row blocks per workgroup; -1 for a null plan. */
 int32_t tsr_plan_attn_rows_per_item(const tsr_plan* plan);
+/* Number of attention items whose key range was split (split_tiles), each
+ * merged by the second kernel; 0 when none; -1 for a null plan. */
+int32_t tsr_plan_num_attn_splits(const tsr_plan* plan);
 
 /* The attention items in two parts, so that attention can start while the
  * cached states are still on their way (Section 5.3: cache hits transfer
@@ -354,7 +386,11 @@ tsr_status tsr_compose_kv(const tsr_plan* plan, const void* pool_k,
  *   lse  device [T][H_q] fp32 natural-log sum of exp(scale * s), or NULL.
  * Must run after tsr_compose_kv of the same plan and layer (stream order).
  * bf16: QK^T in bf16 MFMA with fp32 accumulation; probabilities and values
- * enter the PV product as fp16 (|v| must stay below 65504).
+ * enter the PV product as fp16: V values up to 65280 in magnitude (every
+ * bf16 below fp16's maximum) convert exactly; a larger one becomes infinite
+ * and makes the outputs of the rows whose key tiles hold it non-finite (the
+ * input is refused loudly rather than clipped).  e4m3: likewise a V page
+ * scale above 2^7 (stored V beyond fp16's range) makes such outputs NaN.
  * e4m3: computed pages are quantized like composed ones (k after rotation);
  * q_rot is quantized per (row, head) to e4m3 with the smallest power-of-two
  * scale covering the row, QK^T runs in fp8 MFMA, PV in fp16 MFMA.

@@ -32,7 +32,8 @@ TSR_ATTN_ALL, TSR_ATTN_BEFORE_COMPOSE, TSR_ATTN_AFTER_COMPOSE = 0, 1, 2
 # Every symbol include/*.h declares.
 EXPORTS = (
     "tsr_abi_version", "tsr_last_error", "tsr_rope_table_bytes",
-    "tsr_rope_table_init", "tsr_plan_workspace_size", "tsr_plan_create",
+    "tsr_rope_table_init", "tsr_plan_workspace_size", "tsr_plan_workspace_size_ex",
+    "tsr_plan_create", "tsr_plan_num_attn_splits",
     "tsr_plan_num_compute_tokens", "tsr_plan_num_gather_tokens",
     "tsr_plan_num_retain_tokens", "tsr_plan_num_attn_items", "tsr_plan_attn_rows_per_item",
     "tsr_plan_num_attn_items_part", "tsr_attn_part", "tsr_plan_create_ex", "tsr_plan_create_static",
@@ -81,7 +82,8 @@ class tsr_request(ctypes.Structure):
 
 
 class tsr_plan_options(ctypes.Structure):
-    _fields_ = [("alias_v", c_int32), ("alias_k", c_int32), ("reserved", c_int32 * 6)]
+    _fields_ = [("alias_v", c_int32), ("alias_k", c_int32), ("split_tiles", c_int32),
+                ("reserved", c_int32 * 5)]
 
 
 class tsr_replay_config(ctypes.Structure):
@@ -130,6 +132,10 @@ def lib():
             "tsr_plan_num_attn_items_part": (c_int32, [P, c_int32]),
             "tsr_plan_num_aliased_pages": (c_int32, [P]),
             "tsr_plan_num_aliased_k_pages": (c_int32, [P]),
+            "tsr_plan_num_attn_splits": (c_int32, [P]),
+            "tsr_plan_workspace_size_ex": (c_size_t, [POINTER(tsr_model), POINTER(tsr_request),
+                                                      c_int32, c_int32, c_int32,
+                                                      POINTER(tsr_plan_options)]),
             "tsr_plan_create_ex": (c_int32, [POINTER(tsr_model), POINTER(tsr_request), c_int32,
                                              c_int32, c_int32, POINTER(tsr_plan_options), P, P,
                                              c_size_t, P, POINTER(c_void_p)]),
@@ -280,9 +286,12 @@ def tsr_rope_table_init(model: tsr_model, dev_table, table_bytes: int, stream=No
 
 
 def tsr_plan_workspace_size(model: tsr_model, batch: RequestBatch, n_pool_pages: int,
-                            n_req_pages: int) -> int:
-    n = lib().tsr_plan_workspace_size(ctypes.byref(model), batch.array, batch.n,
-                                      n_pool_pages, n_req_pages)
+                            n_req_pages: int, alias_v: bool = False, alias_k: bool = False,
+                            split_tiles: int = 0) -> int:
+    opts = tsr_plan_options(alias_v=int(alias_v), alias_k=int(alias_k),
+                            split_tiles=split_tiles)
+    n = lib().tsr_plan_workspace_size_ex(ctypes.byref(model), batch.array, batch.n,
+                                         n_pool_pages, n_req_pages, ctypes.byref(opts))
     if n == 0:
         raise TsrError(TSR_ERR_INVALID_ARG, tsr_last_error())
     return n
@@ -326,6 +335,10 @@ class Plan:
     def num_aliased_k_pages(self) -> int:
         return lib().tsr_plan_num_aliased_k_pages(self.handle)
 
+    @property
+    def num_attn_splits(self) -> int:
+        return lib().tsr_plan_num_attn_splits(self.handle)
+
     def compute_positions(self):
         T = self.num_compute_tokens
         pos = np.empty(max(T, 1), dtype=np.int32)
@@ -357,10 +370,11 @@ class Plan:
 def tsr_plan_create(model: tsr_model, batch: RequestBatch, n_pool_pages: int,
                     n_req_pages: int, dev_rope_table=None, dev_workspace=None,
                     workspace_bytes: int = 0, stream=None, alias_v: bool = False,
-                    alias_k: bool = False) -> Plan:
+                    alias_k: bool = False, split_tiles: int = 0) -> Plan:
     out = c_void_p()
-    if alias_v or alias_k:
-        opts = tsr_plan_options(alias_v=int(alias_v), alias_k=int(alias_k))
+    if alias_v or alias_k or split_tiles:
+        opts = tsr_plan_options(alias_v=int(alias_v), alias_k=int(alias_k),
+                                split_tiles=split_tiles)
         _check(lib().tsr_plan_create_ex(ctypes.byref(model), batch.array, batch.n,
                                         n_pool_pages, n_req_pages, ctypes.byref(opts),
                                         _ptr(dev_rope_table), _ptr(dev_workspace),
@@ -377,11 +391,13 @@ def tsr_plan_create(model: tsr_model, batch: RequestBatch, n_pool_pages: int,
 
 def tsr_plan_create_static(model: tsr_model, batch: RequestBatch, n_pool_pages: int,
                            n_req_pages: int, dev_rope_table, stream=None,
-                           alias_v: bool = False, alias_k: bool = False) -> Plan:
+                           alias_v: bool = False, alias_k: bool = False,
+                           split_tiles: int = 0) -> Plan:
     """A plan whose device image lives in the library's own plan area (no
     workspace); a later static plan on the same device supersedes it."""
     out = c_void_p()
-    opts = tsr_plan_options(alias_v=int(alias_v), alias_k=int(alias_k))
+    opts = tsr_plan_options(alias_v=int(alias_v), alias_k=int(alias_k),
+                            split_tiles=split_tiles)
     _check(lib().tsr_plan_create_static(ctypes.byref(model), batch.array, batch.n,
                                         n_pool_pages, n_req_pages, ctypes.byref(opts),
                                         _ptr(dev_rope_table), _stream(stream),

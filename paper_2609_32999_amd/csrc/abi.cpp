@@ -78,12 +78,130 @@ tsr_status attn_common(const tsr_plan* p, int32_t part, const void* q, const voi
   hipStream_t s = static_cast<hipStream_t>(stream);
   hipError_t e = is_e4m3(p)
                      ? launch_attn_e4m3(p, items, n, q, req_k, req_v, req_scale, out, lse, s)
-                     : launch_attn(p, items, n, pool_k, pool_v, q, req_k, req_v, out, lse, s);
+                     : launch_attn(p, part, items, n, pool_k, pool_v, q, req_k, req_v, out,
+                                   lse, s);
   if (e != hipSuccess) return device_fail("attention launch", e);
   return TSR_OK;
 }
 
+
+// Options as build_plan takes them; a static plan's automatic split is off
+// (its image must fit the static plan area).
+tsr_status resolve_options(const tsr_plan_options* options, bool static_plan, bool* alias_v,
+                           bool* alias_k, int32_t* split) {
+  *alias_v = *alias_k = false;
+  *split = static_plan ? -1 : 0;
+  if (!options) return TSR_OK;
+  for (int32_t r : options->reserved)
+    if (r != 0) {
+      set_error("tsr_plan_options.reserved must be zero");
+      return TSR_ERR_INVALID_ARG;
+    }
+  if (options->alias_v != 0 && options->alias_v != 1) {
+    set_error("tsr_plan_options.alias_v must be 0 or 1");
+    return TSR_ERR_INVALID_ARG;
+  }
+  if (options->alias_k != 0 && options->alias_k != 1) {
+    set_error("tsr_plan_options.alias_k must be 0 or 1");
+    return TSR_ERR_INVALID_ARG;
+  }
+  if (options->split_tiles < -1) {
+    set_error("tsr_plan_options.split_tiles must be -1, 0 or positive");
+    return TSR_ERR_INVALID_ARG;
+  }
+  *alias_v = options->alias_v == 1;
+  *alias_k = options->alias_k == 1;
+  if (options->split_tiles != 0) *split = options->split_tiles;
+  return TSR_OK;
+}
+
 }  // namespace
+
+size_t plan_workspace_size(const tsr_model* model, const tsr_request* reqs, int32_t n_req,
+                           int32_t n_pool_pages, int32_t n_req_pages,
+                           const tsr_plan_options* options, bool static_plan) {
+  size_t bytes = 0;
+  guarded([&]() -> tsr_status {
+    bool alias_v, alias_k;
+    int32_t split;
+    tsr_status st = resolve_options(options, static_plan, &alias_v, &alias_k, &split);
+    if (st != TSR_OK) return st;
+    tsr_plan tmp{};
+    st = build_plan(model, reqs, n_req, n_pool_pages, n_req_pages, alias_v, alias_k, split,
+                    &tmp);
+    if (st == TSR_OK) bytes = tmp.ws_bytes;
+    return st;
+  });
+  return bytes;
+}
+
+tsr_status create_plan(const tsr_model* model, const tsr_request* reqs, int32_t n_req,
+                       int32_t n_pool_pages, int32_t n_req_pages,
+                       const tsr_plan_options* options, bool static_plan,
+                       const void* dev_rope_table, void* dev_workspace,
+                       size_t workspace_bytes, void* stream, tsr_plan** out_plan) {
+  return guarded([&]() -> tsr_status {
+    if (!out_plan) {
+      set_error("out_plan is NULL");
+      return TSR_ERR_INVALID_ARG;
+    }
+    *out_plan = nullptr;
+    bool alias_v, alias_k;
+    int32_t split;
+    tsr_status st = resolve_options(options, static_plan, &alias_v, &alias_k, &split);
+    if (st != TSR_OK) return st;
+    tsr_plan* p = new tsr_plan();
+    st = build_plan(model, reqs, n_req, n_pool_pages, n_req_pages, alias_v, alias_k, split, p);
+    if (st != TSR_OK) {
+      delete p;
+      return st;
+    }
+    if (dev_workspace) {
+      if (workspace_bytes < p->ws_bytes) {
+        set_error("workspace smaller than tsr_plan_workspace_size_ex() = " +
+                  std::to_string(p->ws_bytes));
+        delete p;
+        return TSR_ERR_INVALID_ARG;
+      }
+      if (!dev_rope_table) {
+        set_error("dev_rope_table is NULL");
+        delete p;
+        return TSR_ERR_INVALID_ARG;
+      }
+      hipError_t e = hipMemcpyAsync(dev_workspace, p->image.data(), p->image_bytes,
+                                    hipMemcpyHostToDevice,
+                                    static_cast<hipStream_t>(stream));
+      if (e != hipSuccess) {
+        delete p;
+        return device_fail("hipMemcpyAsync(plan)", e);
+      }
+      char* base = static_cast<char*>(dev_workspace);
+      const size_t half = (size_t)p->model.max_position * (p->model.head_dim / 2);
+      const float* table = static_cast<const float*>(dev_rope_table);
+      p->dev.gather = reinterpret_cast<const GatherDesc*>(base + p->off_gather);
+      p->dev.rows = reinterpret_cast<const RowDesc*>(base + p->off_rows);
+      p->dev.retain = reinterpret_cast<const RetainDesc*>(base + p->off_retain);
+      p->dev.items = reinterpret_cast<const AttnItem*>(base + p->off_items);
+      for (int q = 0; q < 2; ++q)
+        p->dev.items_part[q] = reinterpret_cast<const AttnItem*>(base + p->off_items_part[q]);
+      p->dev.block_tables = reinterpret_cast<const int32_t*>(base + p->off_bt);
+      p->dev.v_block_tables = reinterpret_cast<const int32_t*>(base + p->off_vbt);
+      p->dev.k_block_tables = reinterpret_cast<const int32_t*>(base + p->off_kbt);
+      p->dev.gpages = reinterpret_cast<const PageDesc*>(base + p->off_gpages);
+      p->dev.apages = reinterpret_cast<const PageDesc*>(base + p->off_apages);
+      p->dev.rpages = reinterpret_cast<const PageDesc*>(base + p->off_rpages);
+      p->dev.combine = reinterpret_cast<const CombineDesc*>(base + p->off_combine);
+      p->dev.split_o = reinterpret_cast<float*>(base + p->off_split_o);
+      p->dev.split_lse = reinterpret_cast<float*>(base + p->off_split_lse);
+      p->dev.rope_cos = table;
+      p->dev.rope_sin = table + half;
+    }
+    p->rope_table = dev_rope_table;
+    p->ws = dev_workspace;
+    *out_plan = p;
+    return TSR_OK;
+  });
+}
 
 void set_error(const std::string& msg) { g_error = msg; }
 
@@ -137,15 +255,13 @@ tsr_status tsr_rope_table_init(const tsr_model* model, void* dev_table,
 size_t tsr_plan_workspace_size(const tsr_model* model, const tsr_request* reqs,
                                int32_t n_req, int32_t n_pool_pages,
                                int32_t n_req_pages) {
-  size_t bytes = 0;
-  guarded([&]() -> tsr_status {
-    tsr_plan tmp{};
-    tsr_status st = build_plan(model, reqs, n_req, n_pool_pages, n_req_pages, false, false,
-                               &tmp);
-    if (st == TSR_OK) bytes = tmp.ws_bytes;
-    return st;
-  });
-  return bytes;
+  return tsr_plan_workspace_size_ex(model, reqs, n_req, n_pool_pages, n_req_pages, nullptr);
+}
+
+size_t tsr_plan_workspace_size_ex(const tsr_model* model, const tsr_request* reqs,
+                                  int32_t n_req, int32_t n_pool_pages, int32_t n_req_pages,
+                                  const tsr_plan_options* options) {
+  return plan_workspace_size(model, reqs, n_req, n_pool_pages, n_req_pages, options, false);
 }
 
 tsr_status tsr_plan_create(const tsr_model* model, const tsr_request* reqs,
@@ -162,79 +278,8 @@ tsr_status tsr_plan_create_ex(const tsr_model* model, const tsr_request* reqs,
                               const tsr_plan_options* options, const void* dev_rope_table,
                               void* dev_workspace, size_t workspace_bytes, void* stream,
                               tsr_plan** out_plan) {
-  return guarded([&]() -> tsr_status {
-    if (!out_plan) {
-      set_error("out_plan is NULL");
-      return TSR_ERR_INVALID_ARG;
-    }
-    *out_plan = nullptr;
-    bool alias_v = false, alias_k = false;
-    if (options) {
-      for (int32_t r : options->reserved)
-        if (r != 0) {
-          set_error("tsr_plan_options.reserved must be zero");
-          return TSR_ERR_INVALID_ARG;
-        }
-      if (options->alias_v != 0 && options->alias_v != 1) {
-        set_error("tsr_plan_options.alias_v must be 0 or 1");
-        return TSR_ERR_INVALID_ARG;
-      }
-      if (options->alias_k != 0 && options->alias_k != 1) {
-        set_error("tsr_plan_options.alias_k must be 0 or 1");
-        return TSR_ERR_INVALID_ARG;
-      }
-      alias_v = options->alias_v == 1;
-      alias_k = options->alias_k == 1;
-    }
-    tsr_plan* p = new tsr_plan();
-    tsr_status st = build_plan(model, reqs, n_req, n_pool_pages, n_req_pages, alias_v,
-                               alias_k, p);
-    if (st != TSR_OK) {
-      delete p;
-      return st;
-    }
-    if (dev_workspace) {
-      if (workspace_bytes < p->ws_bytes) {
-        set_error("workspace smaller than tsr_plan_workspace_size() = " +
-                  std::to_string(p->ws_bytes));
-        delete p;
-        return TSR_ERR_INVALID_ARG;
-      }
-      if (!dev_rope_table) {
-        set_error("dev_rope_table is NULL");
-        delete p;
-        return TSR_ERR_INVALID_ARG;
-      }
-      hipError_t e = hipMemcpyAsync(dev_workspace, p->image.data(), p->ws_bytes,
-                                    hipMemcpyHostToDevice,
-                                    static_cast<hipStream_t>(stream));
-      if (e != hipSuccess) {
-        delete p;
-        return device_fail("hipMemcpyAsync(plan)", e);
-      }
-      char* base = static_cast<char*>(dev_workspace);
-      const size_t half = (size_t)p->model.max_position * (p->model.head_dim / 2);
-      const float* table = static_cast<const float*>(dev_rope_table);
-      p->dev.gather = reinterpret_cast<const GatherDesc*>(base + p->off_gather);
-      p->dev.rows = reinterpret_cast<const RowDesc*>(base + p->off_rows);
-      p->dev.retain = reinterpret_cast<const RetainDesc*>(base + p->off_retain);
-      p->dev.items = reinterpret_cast<const AttnItem*>(base + p->off_items);
-      for (int q = 0; q < 2; ++q)
-        p->dev.items_part[q] = reinterpret_cast<const AttnItem*>(base + p->off_items_part[q]);
-      p->dev.block_tables = reinterpret_cast<const int32_t*>(base + p->off_bt);
-      p->dev.v_block_tables = reinterpret_cast<const int32_t*>(base + p->off_vbt);
-      p->dev.k_block_tables = reinterpret_cast<const int32_t*>(base + p->off_kbt);
-      p->dev.gpages = reinterpret_cast<const PageDesc*>(base + p->off_gpages);
-      p->dev.apages = reinterpret_cast<const PageDesc*>(base + p->off_apages);
-      p->dev.rpages = reinterpret_cast<const PageDesc*>(base + p->off_rpages);
-      p->dev.rope_cos = table;
-      p->dev.rope_sin = table + half;
-    }
-    p->rope_table = dev_rope_table;
-    p->ws = dev_workspace;
-    *out_plan = p;
-    return TSR_OK;
-  });
+  return create_plan(model, reqs, n_req, n_pool_pages, n_req_pages, options, false,
+                     dev_rope_table, dev_workspace, workspace_bytes, stream, out_plan);
 }
 
 int32_t tsr_plan_num_compute_tokens(const tsr_plan* p) { return p ? p->T : -1; }
@@ -245,6 +290,7 @@ int32_t tsr_plan_attn_rows_per_item(const tsr_plan* p) {
   return p ? kTileRows * p->row_blocks : -1;
 }
 int32_t tsr_plan_num_aliased_pages(const tsr_plan* p) { return p ? p->n_aliased : -1; }
+int32_t tsr_plan_num_attn_splits(const tsr_plan* p) { return p ? p->n_combine : -1; }
 int32_t tsr_plan_num_aliased_k_pages(const tsr_plan* p) { return p ? p->n_aliased_k : -1; }
 
 int32_t tsr_plan_num_attn_items_part(const tsr_plan* p, int32_t part) {
@@ -341,7 +387,8 @@ tsr_status tsr_prefill_attn(const tsr_plan* p, const void* q, const void* k,
     if (e != hipSuccess) return device_fail("append launch", e);
     e = is_e4m3(p) ? launch_attn_e4m3(p, p->dev.items, p->n_items, q, req_k, req_v,
                                       req_scale, out, lse, s)
-                   : launch_attn(p, p->dev.items, p->n_items, nullptr, nullptr, q, req_k, req_v, out,
+                   : launch_attn(p, TSR_ATTN_ALL, p->dev.items, p->n_items, nullptr, nullptr, q,
+                                 req_k, req_v, out,
                                  lse, s);
     if (e != hipSuccess) return device_fail("attention launch", e);
     return TSR_OK;

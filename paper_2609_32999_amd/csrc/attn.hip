@@ -7,7 +7,7 @@
 // with q_rot = RoPE(q, p_t) rounded to the activation dtype and keys visible
 // up to and including p_t.
 //
-// Two kernels:
+// Three kernels:
 //   attn_f32_kernel   fp32 reference mode, scalar, one workgroup per item.
 //   attn_mfma_kernel  bf16 mode.  Work item = R row blocks of up to 32
 //                     consecutive computed rows of one request x one KV head
@@ -32,6 +32,9 @@
 //                     16.5 KB of cos/sin rows per row block, 52.5 KB with
 //                     one row block (three 4-wave workgroups per CU) and
 //                     85.5 KB with three (one 12-wave workgroup per CU).
+//                     An item whose key range the plan split writes its
+//                     normalized rows and log-sum-exp in fp32 instead.
+//   attn_merge_kernel merges the key ranges of split items into out, lse.
 #include <cmath>
 #include <type_traits>
 
@@ -196,8 +199,12 @@ __device__ __forceinline__ uint32_t lds_addr(const void* p) {
 }
 
 __device__ __forceinline__ uint32_t pack_f16x2(float a, float b) {
-  // bf16 values convert to fp16 exactly inside fp16's normal range
-  const auto h = __builtin_amdgcn_cvt_pkrtz(a, b);
+  // Round to nearest even: a bf16 value converts to fp16 exactly inside
+  // fp16's normal range, and the largest bf16 below fp16's maximum is
+  // 65280; a larger magnitude (65536 and up) becomes infinite, so outputs
+  // that depend on it are non-finite instead of silently clipped.
+  typedef _Float16 f16x2v __attribute__((ext_vector_type(2)));
+  const f16x2v h = {(_Float16)a, (_Float16)b};
   return __builtin_bit_cast(uint32_t, h);
 }
 
@@ -226,8 +233,9 @@ __global__ __launch_bounds__(256 * R, 3) void attn_mfma_kernel(
     const int32_t* __restrict__ vbts, const int32_t* __restrict__ kbts,
     const RowDesc* __restrict__ rows,
     const float* __restrict__ rope_cos, const float* __restrict__ rope_sin,
-    uint16_t* __restrict__ out, float* __restrict__ lse, int n_q_heads,
-    int n_kv_heads, int log2_page, float scale, float scale_log2e) {
+    uint16_t* __restrict__ out, float* __restrict__ lse, float* __restrict__ split_o,
+    float* __restrict__ split_lse, int n_q_heads, int n_kv_heads, int log2_page, float scale,
+    float scale_log2e) {
   // double-buffered K and V^T tiles
   __shared__ __attribute__((aligned(16))) uint8_t kl[2][kKBytes];
   __shared__ __attribute__((aligned(16))) uint16_t vl[2][kVBytes / 2];
@@ -625,6 +633,23 @@ __global__ __launch_bounds__(256 * R, 3) void attn_mfma_kernel(
   const float lt = l + __shfl_xor(l, 32);
   if (!wave_active || rbase + lrow >= it.n_rows) return;
   const float inv = 1.0f / lt;
+  if constexpr (R == 1) {
+    if (it.part_slot >= 0) {
+      // one key range of a split item: normalized rows and log-sum-exp in
+      // fp32 to the item's slot, merged by attn_merge_kernel
+      const int64_t sr = ((int64_t)it.part_slot * kTileRows + lrow) * kSplitHeads + w;
+      float* po = split_o + sr * kD;
+#pragma unroll
+      for (int db = 0; db < 4; ++db)
+#pragma unroll
+        for (int rg = 0; rg < 4; ++rg)
+          *reinterpret_cast<float4*>(po + 32 * db + 8 * rg + 4 * lh) =
+              make_float4(o[db][4 * rg] * inv, o[db][4 * rg + 1] * inv,
+                          o[db][4 * rg + 2] * inv, o[db][4 * rg + 3] * inv);
+      if (lh == 0) split_lse[sr] = m * scale + logf(lt);
+      return;
+    }
+  }
   const int hq = g * G + (G >= 4 ? it.head0 : 0) + w;
   uint16_t* op = out + ((int64_t)row * n_q_heads + hq) * kD;
 #pragma unroll
@@ -646,12 +671,66 @@ int ilog2(int x) {
   return l;
 }
 
+// Merge of a split item's key ranges (Section 5.3's extend pass over the
+// whole prompt, run as several ranges): for its row r and query head
+// hq0 + hs, from the ranges' normalized outputs o_c and log-sum-exps lse_c,
+//   lse = log sum_c exp(lse_c),   o = sum_c exp(lse_c - lse) o_c,
+// o rounded to bf16 once.  One workgroup per split item, two threads per
+// (row, head), each over half the head dims.
+template <int D>
+__global__ __launch_bounds__(256) void attn_merge_kernel(
+    const CombineDesc* __restrict__ cds, const float* __restrict__ split_o,
+    const float* __restrict__ split_lse, uint16_t* __restrict__ out,
+    float* __restrict__ lse, int n_q_heads) {
+  const CombineDesc cd = cds[blockIdx.x];
+  const int t = threadIdx.x;
+  const int half = t & 1, pair = t >> 1;
+  const int r = pair / kSplitHeads, hs = pair % kSplitHeads;
+  if (r >= cd.n_rows || hs >= cd.n_heads) return;
+  auto slot_row = [&](int c) -> int64_t {
+    return ((int64_t)(cd.slot0 + c) * kTileRows + r) * kSplitHeads + hs;
+  };
+  float mx = -INFINITY;
+  for (int c = 0; c < cd.n_slots; ++c) mx = fmaxf(mx, split_lse[slot_row(c)]);
+  float den = 0.0f;
+  for (int c = 0; c < cd.n_slots; ++c) den += expf(split_lse[slot_row(c)] - mx);
+  const float ltot = mx + logf(den);
+  constexpr int DH = D / 2;
+  float acc[DH];
+#pragma unroll
+  for (int d = 0; d < DH; ++d) acc[d] = 0.0f;
+  for (int c = 0; c < cd.n_slots; ++c) {
+    const float wc = expf(split_lse[slot_row(c)] - ltot);
+    const float* src = split_o + slot_row(c) * D + half * DH;
+#pragma unroll
+    for (int d = 0; d < DH; d += 4) {
+      const float4 v = *reinterpret_cast<const float4*>(src + d);
+      acc[d] = fmaf(wc, v.x, acc[d]);
+      acc[d + 1] = fmaf(wc, v.y, acc[d + 1]);
+      acc[d + 2] = fmaf(wc, v.z, acc[d + 2]);
+      acc[d + 3] = fmaf(wc, v.w, acc[d + 3]);
+    }
+  }
+  const int64_t orow = (int64_t)(cd.row0 + r) * n_q_heads + cd.hq0 + hs;
+  uint16_t* dst = out + orow * D + half * DH;
+#pragma unroll
+  for (int d = 0; d < DH; d += 8) {
+    uint4 v;
+    v.x = f32_to_bf16(acc[d]) | (f32_to_bf16(acc[d + 1]) << 16);
+    v.y = f32_to_bf16(acc[d + 2]) | (f32_to_bf16(acc[d + 3]) << 16);
+    v.z = f32_to_bf16(acc[d + 4]) | (f32_to_bf16(acc[d + 5]) << 16);
+    v.w = f32_to_bf16(acc[d + 6]) | (f32_to_bf16(acc[d + 7]) << 16);
+    *reinterpret_cast<uint4*>(dst + d) = v;
+  }
+  if (lse && half == 0) lse[orow] = ltot;
+}
+
 }  // namespace
 
-hipError_t launch_attn(const tsr_plan* p, const AttnItem* items, int32_t n_items,
-                       const void* pool_k, const void* pool_v, const void* q,
-                       const void* req_k, const void* req_v, void* out, float* lse,
-                       hipStream_t s) {
+hipError_t launch_attn(const tsr_plan* p, int32_t part, const AttnItem* items,
+                       int32_t n_items, const void* pool_k, const void* pool_v,
+                       const void* q, const void* req_k, const void* req_v, void* out,
+                       float* lse, hipStream_t s) {
   if (n_items == 0 || p->T == 0) return hipSuccess;
   const tsr_model& m = p->model;
   const int lp = ilog2(m.page_size);
@@ -690,7 +769,8 @@ hipError_t launch_attn(const tsr_plan* p, const AttnItem* items, int32_t n_items
                      p->dev.block_tables, p->dev.v_block_tables,                    \
                      p->dev.k_block_tables, p->dev.rows, p->dev.rope_cos,           \
                      p->dev.rope_sin, static_cast<uint16_t*>(out), lse,             \
-                     m.n_q_heads, m.n_kv_heads, lp, p->scale, sl2e)
+                     p->dev.split_o, p->dev.split_lse, m.n_q_heads, m.n_kv_heads, lp, \
+                     p->scale, sl2e)
 #define TSR_MFMA_G(GG)                                                             \
   if (p->alias_v && p->alias_k) TSR_MFMA(GG, true, true);                          \
   else if (p->alias_v) TSR_MFMA(GG, true, false);                                  \
@@ -706,6 +786,15 @@ hipError_t launch_attn(const tsr_plan* p, const AttnItem* items, int32_t n_items
 #undef TSR_MFMA_G
 #undef TSR_MFMA
 #undef TSR_MFMA_R
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || p->n_combine == 0) return e;
+  // the split items of this part: part 0's merge descriptors come first
+  const int32_t c0 = part == TSR_ATTN_AFTER_COMPOSE ? p->n_combine_part[0] : 0;
+  const int32_t nc = part == TSR_ATTN_ALL ? p->n_combine : p->n_combine_part[part - 1];
+  if (nc == 0) return hipSuccess;
+  hipLaunchKernelGGL(attn_merge_kernel<kD>, dim3(nc), dim3(256), 0, s, p->dev.combine + c0,
+                     p->dev.split_o, p->dev.split_lse, static_cast<uint16_t*>(out), lse,
+                     m.n_q_heads);
   return hipGetLastError();
 }
 

@@ -9,7 +9,10 @@
 //     (unit block scales); the row's Q scale and each key's page scale are
 //     applied to S afterwards (per lane: one row, four pages per tile);
 //   * V codes are dequantized to fp16 (exact for e4m3 values times a
-//     power-of-two scale inside fp16 range) while being transposed into LDS,
+//     power-of-two scale up to 2^7, the most that keeps every code inside
+//     fp16's range; a page with a larger V scale becomes NaN, so outputs
+//     that depend on it are non-finite rather than silently clipped) while
+//     being transposed into LDS,
 //     and P V runs in fp16 MFMA as in the bf16 kernel, so P keeps fp16
 //     precision (e4m3 P would cost several percent of relative error).
 #include <cmath>
@@ -196,7 +199,10 @@ __global__ __launch_bounds__(256, 3) void attn_fp8_kernel(
     *reinterpret_cast<uint4*>(&kmem[buf][(tid >> 3) * kKStr + (tid & 7) * 16]) = kr;
     // V^T[d][key] in fp16: gather byte e of keys (k0, k1) into one word and
     // convert two codes at a time with the page scale.
-    const float s = vq ? nvs[1] : nvs[0];
+    // a page scale above 2^7 can take codes (|c| <= 448) past fp16's
+    // 65504: such pages are refused loudly, as NaN values
+    const float sp = vq ? nvs[1] : nvs[0];
+    const float s = sp <= 128.0f ? sp : __builtin_nanf("");
     uint16_t* vs = vmem[buf];
 #pragma unroll
     for (int half = 0; half < 2; ++half) {

@@ -57,7 +57,8 @@ extern "C" tsr_status tsr_plan_create_static(const tsr_model* model, const tsr_r
     *out_plan = nullptr;
     // size first, on the host, so an oversized batch is refused before any
     // HIP call
-    const size_t need = tsr_plan_workspace_size(model, reqs, n_req, n_pool_pages, n_req_pages);
+    const size_t need =
+        plan_workspace_size(model, reqs, n_req, n_pool_pages, n_req_pages, options, true);
     if (need == 0) return TSR_ERR_INVALID_ARG;   // error set by the size query
     if (need > kStaticPlanBytes) {
       set_error("plan image of " + std::to_string(need) + " bytes exceeds the static plan "
@@ -80,9 +81,8 @@ extern "C" tsr_status tsr_plan_create_static(const tsr_model* model, const tsr_r
       g_addr[dev] = ptr;
     }
     tsr_plan* p = nullptr;
-    tsr_status st = tsr_plan_create_ex(model, reqs, n_req, n_pool_pages, n_req_pages,
-                                       options, dev_rope_table, g_addr[dev],
-                                       kStaticPlanBytes, stream, &p);
+    tsr_status st = create_plan(model, reqs, n_req, n_pool_pages, n_req_pages, options, true,
+                                dev_rope_table, g_addr[dev], kStaticPlanBytes, stream, &p);
     if (st != TSR_OK) return st;
     p->static_device = dev;
     p->static_gen = g_gen[dev].fetch_add(1) + 1;

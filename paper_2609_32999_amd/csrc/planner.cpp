@@ -92,7 +92,7 @@ tsr_status check_model(const tsr_model* m) {
 
 tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
                       int32_t n_req, int32_t n_pool_pages, int32_t n_req_pages,
-                      bool alias_v, bool alias_k, tsr_plan* p) {
+                      bool alias_v, bool alias_k, int32_t split_tiles, tsr_plan* p) {
   tsr_status st = check_model(model);
   if (st != TSR_OK) return st;
   if (n_req < 0) return fail(TSR_ERR_INVALID_ARG, "n_req < 0");
@@ -403,7 +403,7 @@ tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
             if (iv.first < khi && iv.second > klo) part = 1;
           for (int g = 0; g < Hkv; ++g)
             for (int hs = 0; hs < hsplit; ++hs) {
-              AttnItem a{t0, n, hi + 1, lo, g, bt_off[r], bt_len[r], 4 * hs, kv_lo, {0, 0, 0}};
+              AttnItem a{t0, n, hi + 1, lo, g, bt_off[r], bt_len[r], 4 * hs, kv_lo, -1, {0, 0}};
               items.push_back({a, (int64_t)(hi + 1 - kv_lo), r * Hkv + g, part});
             }
         }
@@ -422,6 +422,74 @@ tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
     p->row_blocks = kMaxRowBlocks;
   } else {
     build_items(1);
+  }
+  // Key-range split (bf16 plans with one row block per item): the launch
+  // lasts as long as its longest item, so an item spanning more than S key
+  // tiles runs as up to n = ceil(tiles / S) items over consecutive key
+  // ranges.  Every range but the first starts on a tile boundary above
+  // kv_lo and at or below the smallest row position, so every row sees at
+  // least one key of every range and only the last range needs the causal
+  // mask; each range writes a split buffer slot and the merge kernel
+  // combines the n slots.  Ranges inherit the item's part (a part-0 item's
+  // ranges read no gathered key either).
+  std::vector<CombineDesc> combine[2];
+  int32_t n_slots = 0;
+  if (split_tiles >= 0 && p->row_blocks == 1 && m.act_dtype == TSR_BF16 &&
+      m.kv_dtype == TSR_BF16 && !items.empty()) {
+    auto tiles_of = [](const AttnItem& a) -> int64_t {
+      return (a.kv_len + kMfmaKeys - 1) / kMfmaKeys - a.kv_lo / kMfmaKeys;
+    };
+    int64_t total = 0;
+    for (const Item& x : items) total += tiles_of(x.it);
+    int64_t S = split_tiles > 0 ? split_tiles
+                                : std::max<int64_t>(kMinSplitTiles,
+                                                    (total + kSplitSlots - 1) / kSplitSlots);
+    auto slots_for = [&](int64_t lim) {
+      int64_t n = 0;
+      for (const Item& x : items) {
+        const int64_t t = tiles_of(x.it);
+        if (t > lim) n += (t + lim - 1) / lim;
+      }
+      return n;
+    };
+    while (slots_for(S) > kMaxSplitSlots) S *= 2;
+    std::vector<Item> split;
+    split.reserve(items.size());
+    for (const Item& x : items) {
+      const AttnItem& a = x.it;
+      const int32_t j0 = a.kv_lo / kMfmaKeys;
+      const int32_t ntl = (a.kv_len + kMfmaKeys - 1) / kMfmaKeys;
+      const int64_t t = ntl - j0;
+      // interior boundaries: strictly increasing in (j0, top] with top the
+      // tile of the smallest row position, so that every range starts at a
+      // key every row sees (no row of a range is left without a visible
+      // key) and only the last range holds keys past a row's position
+      const int32_t top = std::min(ntl - 1, a.min_pos / kMfmaKeys);
+      const int64_t n = std::min<int64_t>((t + S - 1) / S, (int64_t)top - j0 + 1);
+      if (t <= S || n < 2) {
+        split.push_back(x);
+        continue;
+      }
+      std::vector<int32_t> b((size_t)n + 1);
+      b[0] = j0;
+      b[n] = ntl;
+      for (int64_t c = 1; c < n; ++c)
+        b[c] = std::min<int32_t>(top - (int32_t)(n - 1 - c), j0 + (int32_t)((c * t + n / 2) / n));
+      for (int64_t c = 1; c < n; ++c) b[c] = std::max(b[c], b[c - 1] + 1);
+      for (int64_t c = 0; c < n; ++c) {
+        Item y = x;
+        y.it.kv_lo = c == 0 ? a.kv_lo : b[c] * kMfmaKeys;
+        y.it.kv_len = c == n - 1 ? a.kv_len : b[c + 1] * kMfmaKeys;
+        y.it.part_slot = n_slots + (int32_t)c;
+        y.cost = (int64_t)(b[c + 1] - b[c]) * kMfmaKeys;
+        split.push_back(y);
+      }
+      combine[x.part].push_back(CombineDesc{a.row0, a.n_rows, a.kv_head * G + a.head0,
+                                            std::min(G, kSplitHeads), n_slots, (int32_t)n,
+                                            {0, 0}});
+      n_slots += (int32_t)n;
+    }
+    items.swap(split);
   }
   // XCD-aware order: (request, KV head) groups share K/V, so each group is
   // bound to one XCD bin (workgroup w runs on XCD w % kNumXcd); bins are
@@ -459,7 +527,7 @@ tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
     for (size_t i = 0; i < per_bin; ++i)
       for (int b = 0; b < kNumXcd; ++b)
         order.push_back(i < bins[b].size() ? bins[b][i]
-                                           : AttnItem{0, 0, 0, 0, 0, 0, 0, 0, 0, {0, 0, 0}});
+                                           : AttnItem{0, 0, 0, 0, 0, 0, 0, 0, 0, -1, {0, 0}});
     return order;
   };
   const std::vector<AttnItem> order = schedule(-1);
@@ -488,11 +556,21 @@ tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
   p->off_gpages = off;  off = align_up(off + gpages.size() * sizeof(PageDesc), 256);
   p->off_apages = off;  off = align_up(off + apages.size() * sizeof(PageDesc), 256);
   p->off_rpages = off;  off = align_up(off + rpages.size() * sizeof(PageDesc), 256);
+  p->n_combine_part[0] = (int32_t)combine[0].size();
+  p->n_combine_part[1] = (int32_t)combine[1].size();
+  p->n_combine = p->n_combine_part[0] + p->n_combine_part[1];
+  p->n_split_slots = n_slots;
+  p->off_combine = off; off = align_up(off + p->n_combine * sizeof(CombineDesc), 256);
+  // the split buffer is written by the kernels, not uploaded
+  p->image_bytes = std::max<size_t>(off, 256);
+  const size_t slot_rows = (size_t)n_slots * kTileRows * kSplitHeads;
+  p->off_split_o = off;   off = align_up(off + slot_rows * m.head_dim * sizeof(float), 256);
+  p->off_split_lse = off; off = align_up(off + slot_rows * sizeof(float), 256);
   p->n_gpages = (int32_t)gpages.size();
   p->n_apages = (int32_t)apages.size();
   p->n_rpages = (int32_t)rpages.size();
   p->ws_bytes = std::max<size_t>(off, 256);
-  p->image.assign(p->ws_bytes, 0);
+  p->image.assign(p->image_bytes, 0);
   auto put = [&](size_t o, const void* src, size_t n) {
     if (n) std::memcpy(p->image.data() + o, src, n);
   };
@@ -508,6 +586,9 @@ tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
   put(p->off_gpages, gpages.data(), gpages.size() * sizeof(PageDesc));
   put(p->off_apages, apages.data(), apages.size() * sizeof(PageDesc));
   put(p->off_rpages, rpages.data(), rpages.size() * sizeof(PageDesc));
+  put(p->off_combine, combine[0].data(), combine[0].size() * sizeof(CombineDesc));
+  put(p->off_combine + combine[0].size() * sizeof(CombineDesc), combine[1].data(),
+      combine[1].size() * sizeof(CombineDesc));
   return TSR_OK;
 }
 

@@ -80,8 +80,37 @@ struct alignas(16) AttnItem {
   int32_t n_pages;   // entries of that block table
   int32_t head0;     // first query head of the group handled by the item
   int32_t kv_lo;     // first visible key of every row (0 unless unit-local)
-  int32_t pad[3];
+  // -1: the item writes out/lse; else the slot of the split buffer its
+  // normalized rows and log-sum-exp go to (one key range of a split item)
+  int32_t part_slot;
+  int32_t pad[2];
 };
+
+// A split item: its rows were computed over n_slots consecutive key ranges,
+// slots slot0 .. slot0 + n_slots - 1 of the split buffer; the merge kernel
+// writes rows row0 .. row0 + n_rows - 1 of query heads hq0 .. hq0 + n_heads - 1.
+struct alignas(16) CombineDesc {
+  int32_t row0;
+  int32_t n_rows;
+  int32_t hq0;
+  int32_t n_heads;
+  int32_t slot0;
+  int32_t n_slots;
+  int32_t pad[2];
+};
+// Split buffer slot: kTileRows rows x 4 query heads x head_dim fp32
+// (normalized output), then kTileRows x 4 fp32 log-sum-exp per slot.
+constexpr int kSplitHeads = 4;
+// The automatic key-range split caps items at the launch's mean key tiles
+// per compute unit (256 on MI355X): a longer item would outlast the launch
+// even with a compute unit to itself.  (Capping at the mean per workgroup
+// slot, three per unit, split the RAG-8B batch under the LOCAL scope into
+// 256 more items and did not shorten it: that launch is bound by its total
+// work, not by its longest item.)
+constexpr int kSplitSlots = 256;
+constexpr int kMinSplitTiles = 32;
+// At most this many split buffer slots (64 KiB each at head_dim 128).
+constexpr int kMaxSplitSlots = 4096;
 
 // Device-side view of a plan (pointers into the caller's workspace).
 struct PlanDev {
@@ -98,6 +127,9 @@ struct PlanDev {
   const PageDesc* rpages;
   const float* rope_cos;   // [max_position][d/2]
   const float* rope_sin;   // [max_position][d/2]
+  const CombineDesc* combine;   // split items, those of part 0 first
+  float* split_o;          // [slots][kTileRows][kSplitHeads][d]
+  float* split_lse;        // [slots][kTileRows][kSplitHeads]
 };
 
 }  // namespace tsr
@@ -117,6 +149,12 @@ struct tsr_plan {
   int32_t n_items_part[2];
   int32_t max_kv_len;
   int32_t row_blocks;       // row blocks per attention item (1 or kMaxRowBlocks)
+  // key-range split items: merge descriptors (part 0's first) and buffer
+  int32_t n_combine;
+  int32_t n_combine_part[2];
+  int32_t n_split_slots;
+  size_t off_combine, off_split_o, off_split_lse;
+  size_t image_bytes;       // bytes of the image uploaded (the split buffer follows)
   int32_t n_gpages, n_apages, n_rpages;   // e4m3 plans only
   std::vector<int32_t> row_pos, row_req, row_lo;
   std::vector<char> image;  // host copy of the device image
@@ -175,9 +213,22 @@ tsr_status check_static_plan(const tsr_plan* p);
 tsr_status check_model(const tsr_model* m);
 
 // Build a plan's host part (validation + descriptors + image layout).
+// split_tiles: > 0 split items longer than that many 32-key tiles, 0 the
+// automatic threshold, < 0 never (see tsr_plan_options).
 tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
                       int32_t n_req, int32_t n_pool_pages, int32_t n_req_pages,
-                      bool alias_v, bool alias_k, tsr_plan* plan);
+                      bool alias_v, bool alias_k, int32_t split_tiles, tsr_plan* plan);
+
+// tsr_plan_workspace_size_ex / tsr_plan_create_ex; static_plan: the plan
+// goes to the static plan area (automatic key-range splitting off).
+size_t plan_workspace_size(const tsr_model* model, const tsr_request* reqs, int32_t n_req,
+                           int32_t n_pool_pages, int32_t n_req_pages,
+                           const tsr_plan_options* options, bool static_plan);
+tsr_status create_plan(const tsr_model* model, const tsr_request* reqs, int32_t n_req,
+                       int32_t n_pool_pages, int32_t n_req_pages,
+                       const tsr_plan_options* options, bool static_plan,
+                       const void* dev_rope_table, void* dev_workspace,
+                       size_t workspace_bytes, void* stream, tsr_plan** out_plan);
 
 // Kernel launchers (return hipSuccess or the launch error).
 hipError_t launch_compose(const tsr_plan* p, const void* pool_k,
@@ -194,11 +245,13 @@ hipError_t launch_assemble_e4m3(const tsr_plan* p, const void* pool_k, const voi
                                 const float* pool_scale, const void* k, const void* v,
                                 void* req_k, void* req_v, float* req_scale, hipStream_t s);
 // Attention launchers run `n_items` items from `items` (a plan's full
-// schedule or one of its parts).
-hipError_t launch_attn(const tsr_plan* p, const AttnItem* items, int32_t n_items,
-                       const void* pool_k, const void* pool_v, const void* q,
-                       const void* req_k, const void* req_v, void* out, float* lse,
-                       hipStream_t s);
+// schedule or one of its parts); `part` (TSR_ATTN_ALL or one of the two
+// parts) selects which split items the merge kernel that follows (bf16
+// plans with split items) completes.
+hipError_t launch_attn(const tsr_plan* p, int32_t part, const AttnItem* items,
+                       int32_t n_items, const void* pool_k, const void* pool_v,
+                       const void* q, const void* req_k, const void* req_v, void* out,
+                       float* lse, hipStream_t s);
 hipError_t launch_retain(const tsr_plan* p, const void* k, const void* v,
                          void* pool_k, void* pool_v, hipStream_t s);
 

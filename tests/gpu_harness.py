@@ -65,12 +65,12 @@ def say(msg: str) -> None:
 class GpuRun:
     """Runs compose -> prefill_attn -> retain on a workload (one layer)."""
 
-    def __init__(self, wl, with_lse=True, pool="device", assemble=False):
+    def __init__(self, wl, with_lse=True, pool="device", assemble=False, split_tiles=0):
         self.wl = wl
         m = wl.model
         say(f"[gpu] workload={wl.name} seed={wl.seed} H={m.n_q_heads}/{m.n_kv_heads} "
             f"d={m.head_dim} {m.kv_dtype} prompt_tokens={wl.prompt_tokens} pool={pool} "
-            f"assemble={assemble}")
+            f"assemble={assemble} split_tiles={split_tiles}")
         s = Session(m, wl.n_pool_pages, wl.n_req_pages, pool=pool)
         self.sess = s
         for t in (s.pool_k, s.pool_v, s.req_k, s.req_v):
@@ -82,7 +82,7 @@ class GpuRun:
         self.pool_k0 = s.pool_k.clone()
         self.pool_v0 = s.pool_v.clone()
         self.pool_s0 = s.pool_scale.clone() if s.e4m3 else None
-        self.plan = s.plan(wl.requests)
+        self.plan = s.plan(wl.requests, split_tiles=split_tiles)
         self.q, self.k, self.v = staging.fresh_inputs(s, wl, self.plan)
         self.pos, self.req = self.plan.compute_positions()
         if assemble:            # compose + append in one launch, then attention
@@ -105,7 +105,8 @@ class GpuRun:
         s.retain(self.plan, self.k, self.v)
         torch.cuda.synchronize()
         say(f"[gpu] ran T={self.plan.num_compute_tokens} gather={self.plan.num_gather_tokens} "
-            f"retain={self.plan.num_retain_tokens} items={self.plan.num_attn_items}")
+            f"retain={self.plan.num_retain_tokens} items={self.plan.num_attn_items} "
+            f"splits={self.plan.num_attn_splits}")
 
     def request_kv(self, r):
         return staging.request_kv(self.sess, self.wl, r)

@@ -44,7 +44,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_abi_version():
-    assert P.tsr_abi_version() == 5
+    assert P.tsr_abi_version() == 6
 
 
 @pytest.mark.parametrize("name", ["tiny", "small_bf16", "small_f32", "small_bf16_g8",
@@ -376,3 +376,48 @@ def test_peak_kernels_validate_before_launch():
         with pytest.raises(P.TsrError) as e:
             P.tsr_peak_copy(dst, src, n)
         assert e.value.status == P.TSR_ERR_INVALID_ARG
+
+
+def _split_plans(name, scope, *splits):
+    wl = workloads.make_workload(workloads.get_config(name).with_(miss_scope=scope))
+    m, batch = _model(wl), P.RequestBatch(wl.requests)
+    plans = [P.tsr_plan_create(m, batch, wl.n_pool_pages, wl.n_req_pages, split_tiles=s)
+             for s in splits]
+    sizes = [P.tsr_plan_workspace_size(m, batch, wl.n_pool_pages, wl.n_req_pages,
+                                       split_tiles=s) for s in splits]
+    return wl, plans, sizes
+
+
+def test_split_option_counts_and_workspace():
+    """Forced key-range splitting adds items and split-buffer slots (at
+    least two 64 KiB slots per split item at head_dim 128); -1 never splits;
+    values below -1 are refused."""
+    wl, (never, forced), (ws_never, ws_forced) = _split_plans("small_bf16", "local", -1, 2)
+    assert never.num_attn_splits == 0
+    assert forced.num_attn_splits > 0
+    assert forced.num_attn_items > never.num_attn_items
+    slot = 32 * 4 * wl.model.head_dim * 4
+    assert ws_forced >= ws_never + 2 * slot * forced.num_attn_splits
+    with pytest.raises(P.TsrError):
+        _split_plans("small_bf16", "local", -2)
+
+
+@pytest.mark.parametrize("name", ["small_fp8", "small_f32"])
+def test_split_ignored_outside_bf16(name):
+    _, (plan,), _ = _split_plans(name, "local", 2)
+    assert plan.num_attn_splits == 0
+
+
+def test_split_automatic_threshold():
+    """Automatic splitting caps items at the launch's mean key tiles per
+    compute unit: the RAG batch under the LOCAL scope (its longest items,
+    the suffix rows, hold 163 tiles against a mean of 288 per unit) is not
+    split; one request of it alone is (its suffix rows then far exceed the
+    mean); under the GLOBAL scope items hold three row blocks and never are."""
+    wl, (local,), _ = _split_plans("rag8b", "local", 0)
+    assert local.attn_rows_per_item == 32 and local.num_attn_splits == 0
+    one = P.tsr_plan_create(_model(wl), P.RequestBatch(wl.requests[:1]), wl.n_pool_pages,
+                            wl.n_req_pages)
+    assert one.attn_rows_per_item == 32 and one.num_attn_splits > 0
+    _, (glob,), _ = _split_plans("rag8b", "global", 0)
+    assert glob.attn_rows_per_item == 96 and glob.num_attn_splits == 0
