@@ -293,12 +293,13 @@ int32_t tsr_plan_num_gather_tokens(const tsr_plan* plan);
 /* Number of tokens written by tsr_retain_kv. */
 int32_t tsr_plan_num_retain_tokens(const tsr_plan* plan);
 /* Number of attention work items (row tile x KV head, plus launch padding).
- * A row tile holds up to 32 consecutive computed rows, or up to 96 in bf16
- * plans whose runs of rows with a common first visible key are long enough
- * (the bf16 kernel then runs three 32-row blocks per workgroup). */
+ * A row tile holds up to 32 consecutive computed rows, or up to 96 in plans
+ * with bf16 activations and bf16 or e4m3 KV whose runs of rows with a
+ * common first visible key are long enough (the MFMA kernels then run
+ * three 32-row blocks per workgroup). */
 int32_t tsr_plan_num_attn_items(const tsr_plan* plan);
 /* Most computed rows an attention item of this plan holds: 32, or 96 when
- * the bf16 kernel runs three row blocks per workgroup; -1 for a null plan. */
+ * the MFMA kernel runs three row blocks per workgroup; -1 for a null plan. */
 int32_t tsr_plan_attn_rows_per_item(const tsr_plan* plan);
 /* Number of attention items whose key range was split (split_tiles), each
  * merged by the second kernel; 0 when none; -1 for a null plan. */

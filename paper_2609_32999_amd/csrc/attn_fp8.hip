@@ -56,8 +56,12 @@ __device__ __forceinline__ int page_scale_exp(float amax) {
   return mfr <= 0.875f ? e - 9 : e - 8;
 }
 
-template <int G>
-__global__ __launch_bounds__(256, 3) void attn_fp8_kernel(
+// R: row blocks per workgroup.  Waves 4 b .. 4 b + 3 own the 32 rows of
+// row block b; the first four waves stage every K/V tile for all of them
+// (three row blocks share each staged tile, which cuts the KV reads per row
+// threefold).
+template <int G, int R>
+__global__ __launch_bounds__(256 * R, 3) void attn_fp8_kernel(
     const uint16_t* __restrict__ q, const uint8_t* __restrict__ kc,
     const uint8_t* __restrict__ vc, const float* __restrict__ scales,
     const AttnItem* __restrict__ items, const int32_t* __restrict__ bts,
@@ -68,31 +72,45 @@ __global__ __launch_bounds__(256, 3) void attn_fp8_kernel(
   constexpr int HPW = 1;  // query heads per wave
   __shared__ __attribute__((aligned(16))) uint8_t kmem[2][kKBytes];
   __shared__ __attribute__((aligned(16))) uint16_t vmem[2][kVElems];
-  // cos (dims 0 .. d/2-1) and sin (d/2 ..) at each row's position, loaded
-  // once and shared by the four head waves (rows padded by 4 floats so
-  // that the 32 rows of a fragment read fall in different banks)
-  __shared__ __attribute__((aligned(16))) float rl[32][kD + 4];
+  // K page scales of each staged tile's two 16-key blocks
+  __shared__ float kscl[2][2];
+  // cos (dims 0 .. d/2-1) and sin (d/2 ..) at each row's position, per row
+  // block, loaded once and shared by its four head waves (rows padded by 4
+  // floats so that the 32 rows of a fragment read fall in different banks)
+  __shared__ __attribute__((aligned(16))) float rl[R][32][kD + 4];
 
   const AttnItem it = items[blockIdx.x];
   if (it.n_rows == 0) return;
   const int tid = threadIdx.x;
-  const int w = tid >> 6;
+  const int wg = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int w = wg & 3;                  // query head slot
+  const int rb = wg >> 2;                // row block
+  const bool stager = wg < 4;            // waves that stage K and V
   const int lane = tid & 63;
   const int lrow = lane & 31;
   const int lh = lane >> 5;
   const int g = it.kv_head;
   const int page_mask = (1 << log2_page) - 1;
   const int32_t* bt = bts + it.bt_off;
-  const int row = it.row0 + min(lrow, it.n_rows - 1);
+  const int rbase = 32 * rb;
+  const int row = it.row0 + min(rbase + lrow, it.n_rows - 1);
   const int pos = rows[row].pos;
   {
-    const int lr = tid >> 3, c8 = 8 * (tid & 7);
-    const int ppos = rows[it.row0 + min(lr, it.n_rows - 1)].pos;
+    const int t = tid & 255, lr = t >> 3, c8 = 8 * (t & 7);
+    const int ppos = rows[it.row0 + min(rbase + lr, it.n_rows - 1)].pos;
     float c[8], sn[8];
     load8(rope_cos + (int64_t)ppos * (kD / 2) + c8, c);
     load8(rope_sin + (int64_t)ppos * (kD / 2) + c8, sn);
-    store8(&rl[lr][c8], c);
-    store8(&rl[lr][kD / 2 + c8], sn);
+    store8(&rl[rb][lr][c8], c);
+    store8(&rl[rb][lr][kD / 2 + c8], sn);
+  }
+  // key tiles this wave's rows need: up to their largest position
+  int my_ntiles = 1 << 30;
+  if constexpr (R > 1) {
+    int wmax = rbase + lrow < it.n_rows ? pos : -1;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) wmax = max(wmax, __shfl_xor(wmax, o));
+    my_ntiles = __builtin_amdgcn_readfirstlane(wmax + kKT) / kKT;
   }
   __syncthreads();
 
@@ -114,8 +132,8 @@ __global__ __launch_bounds__(256, 3) void attn_fp8_kernel(
       float cs[8], sn[8];
       load8(qp + d0, lo + 8 * c);
       load8(qp + d0 + kD / 2, hi + 8 * c);
-      load8(&rl[lrow][d0], cs);
-      load8(&rl[lrow][kD / 2 + d0], sn);
+      load8(&rl[rb][lrow][d0], cs);
+      load8(&rl[rb][lrow][kD / 2 + d0], sn);
       rope_rotate<8>(lo + 8 * c, hi + 8 * c, cs, sn);
     }
     float amax = 0.0f;
@@ -170,7 +188,6 @@ __global__ __launch_bounds__(256, 3) void attn_fp8_kernel(
   const int vc8 = (tid >> 4) * 8;
   const int vcol = 16 * vq + ((vk >> 2) & 1) * 8 + ((vk >> 3) & 1) * 4 + (vk & 3);   // permuted
   float nks[2], nvs[2];   // page scales of the staged tile (uniform)
-  float tks[2];           // K page scales of the tile being computed
   auto load_tile = [&](int j) {
     const int key0 = j * kKT;
     int64_t base[2];
@@ -197,6 +214,10 @@ __global__ __launch_bounds__(256, 3) void attn_fp8_kernel(
   };
   auto store_tile = [&](int buf) {
     *reinterpret_cast<uint4*>(&kmem[buf][(tid >> 3) * kKStr + (tid & 7) * 16]) = kr;
+    if (tid == 0) {
+      kscl[buf][0] = nks[0];
+      kscl[buf][1] = nks[1];
+    }
     // V^T[d][key] in fp16: gather byte e of keys (k0, k1) into one word and
     // convert two codes at a time with the page scale.
     // a page scale above 2^7 can take codes (|c| <= 448) past fp16's
@@ -260,7 +281,7 @@ __global__ __launch_bounds__(256, 3) void attn_fp8_kernel(
     for (int i = 0; i < HPW; ++i) {
       float f[2];
 #pragma unroll
-      for (int b = 0; b < 2; ++b) f[b] = qs[i] * tks[b] * scale_log2e;
+      for (int b = 0; b < 2; ++b) f[b] = qs[i] * kscl[j & 1][b] * scale_log2e;
       if constexpr (MASK != 0) {
         // score r holds key j kKT + 8 (r / 4) + 4 lh + r % 4: compare its
         // in-tile offset with the row's bounds moved to the same origin
@@ -332,37 +353,49 @@ __global__ __launch_bounds__(256, 3) void attn_fp8_kernel(
   const int j0 = it.kv_lo / kKT;
   const int jlo = (it.kv_lo + kKT - 1) / kKT;
   const int nfull = min(ntiles, (it.min_pos + 1) / kKT);
-  load_tile(j0);
-  store_tile(j0 & 1);
-#pragma unroll
-  for (int b = 0; b < 2; ++b) tks[b] = nks[b];
+  if (stager) {
+    load_tile(j0);
+    store_tile(j0 & 1);
+  }
   __syncthreads();
   // Three loops (masked head, unmasked body, masked tail) rather than one
   // loop that picks the masked or unmasked tile per iteration: with both
   // variants in one loop body the compiler kept about 90 more registers
-  // live.
+  // live.  Tiles past a row block's last row are fully masked for it and
+  // skipped (only in the masked tail).
   auto run_tiles = [&](int ja, int jb, auto mask_tag) __attribute__((always_inline)) {
     for (int j = ja; j < jb; ++j) {
       const bool more = j + 1 < ntiles;
       if (more) load_tile(j + 1);
-      tile(j, mask_tag);
+      if (j < my_ntiles) tile(j, mask_tag);
       if (more) store_tile((j + 1) & 1);
-#pragma unroll
-      for (int b = 0; b < 2; ++b) tks[b] = nks[b];
+      __syncthreads();
+    }
+  };
+  // the waves of the other row blocks stage nothing
+  auto run_tiles_ns = [&](int ja, int jb, auto mask_tag) __attribute__((always_inline)) {
+    for (int j = ja; j < jb; ++j) {
+      if (j < my_ntiles) tile(j, mask_tag);
       __syncthreads();
     }
   };
   const int jl = min(ntiles, max(j0, jlo));
-  run_tiles(j0, jl, std::integral_constant<int, 2>{});
-  run_tiles(jl, max(jl, nfull), std::integral_constant<int, 0>{});
-  run_tiles(max(jl, nfull), ntiles, std::integral_constant<int, 1>{});
+  if (stager) {
+    run_tiles(j0, jl, std::integral_constant<int, 2>{});
+    run_tiles(jl, max(jl, nfull), std::integral_constant<int, 0>{});
+    run_tiles(max(jl, nfull), ntiles, std::integral_constant<int, 1>{});
+  } else {
+    run_tiles_ns(j0, jl, std::integral_constant<int, 2>{});
+    run_tiles_ns(jl, max(jl, nfull), std::integral_constant<int, 0>{});
+    run_tiles_ns(max(jl, nfull), ntiles, std::integral_constant<int, 1>{});
+  }
 
   // ---- epilogue
 #pragma unroll
   for (int i = 0; i < HPW; ++i) {
     if (!wave_active[i]) continue;
     const float lt = l[i] + __shfl_xor(l[i], 32);
-    if (lrow >= it.n_rows) continue;
+    if (rbase + lrow >= it.n_rows) continue;
     const float inv = 1.0f / lt;
     const int hq = g * G + (G >= 4 ? it.head0 : 0) + w + 4 * i;
     uint16_t* op = out + ((int64_t)row * n_q_heads + hq) * kD;
@@ -400,7 +433,12 @@ hipError_t launch_attn_e4m3(const tsr_plan* p, const AttnItem* items, int32_t n_
   const int G = m.n_q_heads / m.n_kv_heads;
   const float sl2e = (float)((double)p->scale * 1.4426950408889634);
 #define TSR_FP8(GG)                                                                   \
-  hipLaunchKernelGGL(attn_fp8_kernel<GG>, dim3(n_items), dim3(256), 0, s,             \
+  if (p->row_blocks == kMaxRowBlocks)                                                 \
+    TSR_FP8_R(GG, kMaxRowBlocks);                                                     \
+  else                                                                                \
+    TSR_FP8_R(GG, 1)
+#define TSR_FP8_R(GG, RB)                                                             \
+  hipLaunchKernelGGL((attn_fp8_kernel<GG, RB>), dim3(n_items), dim3(256 * (RB)), 0, s, \
                      static_cast<const uint16_t*>(q), static_cast<const uint8_t*>(req_k), \
                      static_cast<const uint8_t*>(req_v), req_scale, items,            \
                      p->dev.block_tables, p->dev.rows, p->dev.rope_cos,               \
@@ -414,6 +452,7 @@ hipError_t launch_attn_e4m3(const tsr_plan* p, const AttnItem* items, int32_t n_
     default: return hipErrorInvalidValue;
   }
 #undef TSR_FP8
+#undef TSR_FP8_R
   return hipGetLastError();
 }
 

@@ -412,12 +412,12 @@ tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
     }
     return slots ? (double)need / (double)slots : 1.0;
   };
-  // The bf16 MFMA kernel runs kMaxRowBlocks row blocks per workgroup (its
-  // K/V staging then serves three times the rows) unless short runs of rows
-  // (unit-local attention) would leave too many row blocks idle; the other
-  // kernels take one row block.
+  // The MFMA kernels (bf16 and e4m3 KV) run kMaxRowBlocks row blocks per
+  // workgroup (their K/V staging then serves three times the rows) unless
+  // short runs of rows (unit-local attention) would leave too many row
+  // blocks idle; the fp32 kernel takes one row block.
   p->row_blocks = 1;
-  if (m.act_dtype == TSR_BF16 && m.kv_dtype == TSR_BF16 &&
+  if (m.act_dtype == TSR_BF16 && (m.kv_dtype == TSR_BF16 || m.kv_dtype == TSR_E4M3) &&
       build_items(kMaxRowBlocks) >= kMinRowBlockUse) {
     p->row_blocks = kMaxRowBlocks;
   } else {

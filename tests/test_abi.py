@@ -100,7 +100,7 @@ def test_attention_row_blocks(name, scope):
     m = wl.model
     n1, _ = _items_per_kv_head(wl, 32)
     n3, use3 = _items_per_kv_head(wl, MULTI_ROWS)
-    three = m.kv_dtype == "bf16" and m.act_dtype == "bf16" and use3 >= 0.8
+    three = m.kv_dtype in ("bf16", "e4m3") and m.act_dtype == "bf16" and use3 >= 0.8
     groups = (m.n_q_heads // m.n_kv_heads) // 4 if m.act_dtype == "bf16" and \
         m.n_q_heads // m.n_kv_heads > 4 else 1
     per = m.n_kv_heads * groups
@@ -111,7 +111,8 @@ def test_attention_row_blocks(name, scope):
         assert n3 * per <= plan.num_attn_items < n1 * per, (plan.num_attn_items, n1, n3, use3)
     else:
         assert plan.num_attn_items >= n1 * per, (plan.num_attn_items, n1, n3, use3)
-    assert bool(three) == ((name, scope) in {("rag8b", "global"), ("long70b", "global")})
+    assert bool(three) == ((name, scope) in {("rag8b", "global"), ("long70b", "global"),
+                                             ("fp8rag", "global")})
     assert plan.attn_rows_per_item == (MULTI_ROWS if three else 32)
 
 
