@@ -368,7 +368,7 @@ def attention_flops(plan, m):
 
 def attention_kernel_name(plan, m):
     G = m.n_q_heads // m.n_kv_heads
-    return (f"attn_fp8_kernel<{G}>" if m.kv_dtype == "e4m3"
+    return (f"attn_fp8_kernel<{G}, {plan.attn_rows_per_item // 32}>" if m.kv_dtype == "e4m3"
             else f"attn_mfma_kernel<{G}, {str(plan.alias_v).lower()}, "
                  f"{str(plan.alias_k).lower()}, {plan.attn_rows_per_item // 32}>")
 

@@ -388,10 +388,11 @@ tsr_status tsr_compose_kv(const tsr_plan* plan, const void* pool_k,
  * Must run after tsr_compose_kv of the same plan and layer (stream order).
  * bf16: QK^T in bf16 MFMA with fp32 accumulation; probabilities and values
  * enter the PV product as fp16: V values up to 65280 in magnitude (every
- * bf16 below fp16's maximum) convert exactly; a larger one becomes infinite
- * and makes the outputs of the rows whose key tiles hold it non-finite (the
- * input is refused loudly rather than clipped).  e4m3: likewise a V page
- * scale above 2^7 (stored V beyond fp16's range) makes such outputs NaN.
+ * bf16 below fp16's maximum) convert exactly; a larger one is staged as NaN
+ * (with the values staged beside it) and makes the outputs of the rows whose
+ * key tiles hold it non-finite: the input is refused loudly rather than
+ * clipped.  e4m3: likewise a V page scale above 2^7 (stored V beyond fp16's
+ * range) makes such outputs NaN.
  * e4m3: computed pages are quantized like composed ones (k after rotation);
  * q_rot is quantized per (row, head) to e4m3 with the smallest power-of-two
  * scale covering the row, QK^T runs in fp8 MFMA, PV in fp16 MFMA.

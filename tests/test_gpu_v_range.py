@@ -1,15 +1,14 @@
 """V beyond fp16's range (the P V product runs in fp16): refused loudly.
 
-A bf16 V of magnitude 65536 or more converts to an infinite fp16 value and
-an e4m3 page whose V scale exceeds 2^7 dequantizes to NaN, so the outputs
-of rows that read such a value are non-finite instead of silently clipped.
+A bf16 V of magnitude 65536 or more is staged as NaN and an e4m3 page whose
+V scale exceeds 2^7 dequantizes to NaN, so the outputs of rows that read
+such a value are non-finite instead of silently clipped.
 The oracle (fp64) stays finite on the same input; the test checks that the
 kernel's output is non-finite where the value is read (rows at or after
 its position, heads of its KV head -- every head for e4m3, whose page
 scale covers all KV heads of a page) and finite for the other KV heads and
 requests.  (Earlier rows of a row block that loads the value's key tile
-may turn non-finite too: a masked probability of 0 times an infinite value
-is NaN.)"""
+may turn non-finite too: a masked probability of 0 times NaN is NaN.)"""
 import numpy as np
 import pytest
 import torch
