@@ -1,9 +1,9 @@
 """Benchmark of the composed-prefill hot path on one MI355X.
 
-A step is one attention layer of one batch: compose (gather + RoPE
-re-rotation of cached units) -> append + causal GQA prefill attention of the
-computed rows (main stream), with retention of computed units running
-concurrently on a side stream and joined at the end of the step.  Steps
+A step is one attention layer of one batch: assembly (compose -- gather +
+RoPE re-rotation of cached units -- and append of the computed rows, one
+launch) -> causal GQA prefill attention of the computed rows -> retention
+of the computed units, in stream order.  Steps
 rotate over --layers distinct layer buffer sets (pool, request KV, inputs),
 as consecutive model layers would, so one layer's data is not served from
 the previous step's caches.
@@ -388,39 +388,31 @@ def attention_peaks(m):
     return PEAK_MFMA_TFLOPS[m.act_dtype], None
 
 
-def time_path(torch, sess, plan, qs, ks, vs, out, lse, L, steps, warmup, side=None):
-    """The step: one assembly launch (compose + append) then attention on
-    the current stream, layers rotating over L buffer sets; with a side
-    stream, retention runs there concurrently with attention and is joined
-    at the end of the step.  Returns per-step durations (ms) of the step,
-    the assembly, attention and retention, and the wall time."""
+def time_path(torch, sess, plan, qs, ks, vs, out, lse, L, steps, warmup):
+    """The step, on one stream: one assembly launch (compose + append),
+    attention, then retention of the computed units, layers rotating over L
+    buffer sets.  (Retention on a second stream beside attention gave the
+    same step time: its workgroups wait for compute units the attention
+    workgroups hold, and it slowed attention by as much as it saved.)
+    Returns per-step durations (ms) of the step, the assembly, attention and
+    retention, and the wall time."""
     main_s = torch.cuda.current_stream()
     E = lambda: torch.cuda.Event(enable_timing=True)
-    evs = [[E() for _ in range(3)] for _ in range(steps)]
-    evr = [[E(), E()] for _ in range(steps)]
+    evs = [[E() for _ in range(4)] for _ in range(steps)]
 
-    def step(i, rec=None, recr=None):
+    def step(i, rec=None):
         l = i % L
         if rec:
             rec[0].record(main_s)
         sess.assemble(plan, ks[l], vs[l], layer=l, stream=main_s)
         if rec:
             rec[1].record(main_s)
-        if side is not None:
-            side.wait_stream(main_s)
         sess.attn(plan, qs[l], out, lse, layer=l, stream=main_s)
         if rec:
             rec[2].record(main_s)
-        if side is not None:
-            # retain overlaps the MFMA-bound attention rather than competing
-            # with the assembly for HBM bandwidth
-            with torch.cuda.stream(side):
-                if recr:
-                    recr[0].record(side)
-                sess.retain(plan, ks[l], vs[l], layer=l, stream=side)
-                if recr:
-                    recr[1].record(side)
-            main_s.wait_stream(side)
+        sess.retain(plan, ks[l], vs[l], layer=l, stream=main_s)
+        if rec:
+            rec[3].record(main_s)
 
     for i in range(warmup):
         step(i)
@@ -428,17 +420,17 @@ def time_path(torch, sess, plan, qs, ks, vs, out, lse, L, steps, warmup, side=No
     end = E()
     w0 = time.perf_counter()
     for i in range(steps):
-        step(i, evs[i], evr[i])
+        step(i, evs[i])
     end.record(main_s)
     torch.cuda.synchronize()
     wall = time.perf_counter() - w0
-    # a step lasts from its first event to the next step's (which follows the
-    # join of the side stream); the last one to the event after the loop
+    # a step lasts from its first event to the next step's; the last one to
+    # the event after the loop
     starts = [e[0] for e in evs] + [end]
     step_ms = [starts[i].elapsed_time(starts[i + 1]) for i in range(steps)]
     asm = [e[0].elapsed_time(e[1]) for e in evs]
     att = [e[1].elapsed_time(e[2]) for e in evs]
-    ret = [e[0].elapsed_time(e[1]) for e in evr] if side is not None else []
+    ret = [e[2].elapsed_time(e[3]) for e in evs]
     return step_ms, asm, att, ret, wall
 
 
@@ -619,9 +611,8 @@ def main():
         f"items={plan.num_attn_items}")
 
     main_s = torch.cuda.current_stream()
-    side = torch.cuda.Stream()
     step_ms, asm_ms, attn_ms, retain_ms, wall = time_path(
-        torch, sess, plan, qs, ks, vs, out, lse, L, args.steps, args.warmup, side=side)
+        torch, sess, plan, qs, ks, vs, out, lse, L, args.steps, args.warmup)
     ms = float(np.mean(step_ms))
     d_asm, d_attn, d_ret = dist(asm_ms), dist(attn_ms), dist(retain_ms)
     log(f"[bench] timed {args.steps} steps: {ms:.3f} ms/step (wall {wall * 1e3 / args.steps:.3f}); "
@@ -685,7 +676,7 @@ def main():
         "computed_tokens_per_s": T / (ms * 1e-3),
         "assembly_hbm_gbps": asm_gbs,
         "attention_tflops": attn_tflops,
-        "kernel_us": {"assembly": d_asm, "attention": d_attn, "retain_side_stream": d_ret,
+        "kernel_us": {"assembly": d_asm, "attention": d_attn, "retain": d_ret,
                       "step": dist(step_ms)},
         "roofline": {"bound": "mfma", "achieved": attn_tflops, "peak": peak,
                      "unit": "TFLOP/s", "frac": attn_tflops / peak,
