@@ -44,6 +44,23 @@ def test_staged_hits_match_the_oracle(name, over):
         assert q["state"] == 2 and q["leases"] == 0, (uid, q)
 
 
+@pytest.mark.slow
+def test_staged_hits_full_size_rag8b():
+    """The full RAG-8B batch through the host tier: every hit staged from
+    the pinned host cache by the copy engines, then compose, attention and
+    retain against the staging arena; every request's K/V and attention
+    (every head) against the oracle, retained units written back and
+    published."""
+    wl = workloads.generate("rag8b")
+    run = StagedRun(wl, n_layers=1)
+    assert not run.prep.fallbacks and not run.prep.declined
+    run.check_staged_bytes()
+    for r in range(len(wl.requests)):
+        check_request(run, r)
+    n_ret = sum(len(b) for (_, _, b, _) in run.reservations)
+    assert n_ret > 0 and run.check_published() == n_ret
+
+
 @pytest.mark.parametrize("name", ["small_bf16", "small_fp8"])
 def test_failed_and_overflowing_hits_fall_back_to_text(name):
     wl = workloads.generate(name)
