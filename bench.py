@@ -546,10 +546,10 @@ def main():
                     help="miss scope: global (every missing-unit token attends to the "
                          "whole prompt) or local (missing units attend within themselves "
                          "past their recompute window)")
-    ap.add_argument("--legs", default="local,fp8rag",
+    ap.add_argument("--legs", default="local,fp8rag,agent8b,long70b",
                     help="comma-separated extra legs reported in the same line: local "
                          "(the batch under the LOCAL miss scope), fp8rag, agent8b, long70b "
-                         "(those workloads' assembly + attention); '' for none")
+                         "(those workloads' assembly + attention + retain); '' for none")
     ap.add_argument("--no-peaks", dest="peaks", action="store_false",
                     help="skip measuring the achievable copy and bf16 GEMM rates")
     ap.add_argument("--no-cpu-baseline", action="store_true")

@@ -50,14 +50,15 @@ MODES = {"v": dict(alias_v=True), "k": dict(alias_k=True),
 
 
 class Run:
-    def __init__(self, wl, mode=None, assemble=False):
+    def __init__(self, wl, mode=None, assemble=False, split_tiles=0):
         m = wl.model
         self.wl = wl
         s = self.sess = Session(m, wl.n_pool_pages, wl.n_req_pages)
         for t in (s.pool_k, s.pool_v, s.req_k, s.req_v):
             fill_sentinel(t)
         staging.upload_pool(s, wl)
-        self.plan = p = s.plan(wl.requests, **(MODES[mode] if mode else {}))
+        self.plan = p = s.plan(wl.requests, split_tiles=split_tiles,
+                               **(MODES[mode] if mode else {}))
         q, k, v = staging.fresh_inputs(s, wl, p)
         self.pos, self.req = p.compute_positions()
         self.out, self.lse = s.new_outputs(p, True)
@@ -126,3 +127,19 @@ def test_aliasing_three_row_blocks(mode):
     rng = np.random.default_rng(43)
     for r in range(len(wl.requests)):
         check_request(run, r, kv_heads=[int(rng.integers(wl.model.n_kv_heads))], check_kv=False)
+
+
+@pytest.mark.parametrize("mode", ["v", "k", "kv"])
+def test_aliasing_with_key_range_split(mode):
+    """Aliased plans whose items are split by key range (two-tile ranges
+    under the LOCAL scope): bit-equal to the composed plan split the same
+    way, and the oracle."""
+    wl = workloads.make_workload(workloads.get_config("small_bf16").with_(
+        **{**ALIGNED, "miss_scope": "local"}))
+    pages = aliased_pages(wl)
+    ref = Run(wl, split_tiles=2)
+    run = Run(wl, mode, assemble=(mode == "kv"), split_tiles=2)
+    assert run.plan.num_attn_splits > 0 and run.plan.num_attn_splits == ref.plan.num_attn_splits
+    _check_against_composed(wl, run, ref, mode, pages)
+    for r in range(len(wl.requests)):
+        check_request(run, r, check_kv=False)
