@@ -248,7 +248,14 @@ __global__ __launch_bounds__(256 * R, 3) void attn_mfma_kernel(
   // block: loaded once and shared by the block's four head waves (rows
   // padded by 4 floats so that the 32 rows of a fragment read fall in
   // different banks)
-  __shared__ __attribute__((aligned(16))) float rl[R][kTileRows][kD + 4];
+  // With K rotated on load the rotated queries move to LDS after the
+  // prologue (8 KB per wave, over the cos/sin rows): the staging waves' K
+  // rotation needs the 32 registers they would hold, which otherwise spill.
+  constexpr int kRlBytes = R * kTileRows * (kD + 4) * 4;
+  constexpr bool kQinLds = AK;
+  constexpr int kQBytes = kQinLds ? 4 * R * 8 * 1024 : 0;
+  __shared__ __attribute__((aligned(16))) uint8_t pro[kRlBytes > kQBytes ? kRlBytes : kQBytes];
+  auto rl = reinterpret_cast<float (*)[kTileRows][kD + 4]>(pro);
 
   const AttnItem it = items[blockIdx.x];
   if (it.n_rows == 0) return;
@@ -283,6 +290,16 @@ __global__ __launch_bounds__(256 * R, 3) void attn_mfma_kernel(
   const bool wave_active = G >= 4 || w < G;
 
   bf16x8 qf[8];
+  const uint8_t* qlds = pro + (tid >> 6) * 8192;
+  auto qfrag = [&](int kst) __attribute__((always_inline)) -> bf16x8 {
+    if constexpr (kQinLds) {
+      Frag f;
+      f.u = *reinterpret_cast<const uint4*>(qlds + kst * 1024 + lane * 16);
+      return f.b;
+    } else {
+      return qf[kst];
+    }
+  };
   f32x16 o[4];
 #pragma unroll
   for (int db = 0; db < 4; ++db)
@@ -434,7 +451,7 @@ __global__ __launch_bounds__(256 * R, 3) void attn_mfma_kernel(
     for (int kst = 0; kst < 8; ++kst) {
       Frag a;
       a.u = *reinterpret_cast<const uint4*>(ks + kst * kKBlk + lane * 16);
-      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a.b, qf[kst], s, 0, 0, 0);
+      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a.b, qfrag(kst), s, 0, 0, 0);
     }
     // keep four LDS fragment reads in flight ahead of the MFMAs
     // (scheduling groups: 0x100 = LDS read, 0x008 = MFMA)
@@ -484,7 +501,7 @@ __global__ __launch_bounds__(256 * R, 3) void attn_mfma_kernel(
       for (int kst = 0; kst < 8; ++kst) {
         Frag a;
         a.u = *reinterpret_cast<const uint4*>(ks + kst * kKBlk + lane * 16);
-        s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a.b, qf[kst], s, 0, 0, 0);
+        s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a.b, qfrag(kst), s, 0, 0, 0);
       }
       if constexpr (MASK != kNoMask) {
         const int dhi = pos_l - j * kKT;
@@ -630,6 +647,15 @@ __global__ __launch_bounds__(256 * R, 3) void attn_mfma_kernel(
     }
     qf[ks] = a.b;
     qf[ks + 4] = b.b;
+  }
+  if constexpr (kQinLds) {
+    __syncthreads();   // every wave has read its cos/sin rows
+#pragma unroll
+    for (int kst = 0; kst < 8; ++kst) {
+      Frag f;
+      f.b = qf[kst];
+      *reinterpret_cast<uint4*>(pro + (tid >> 6) * 8192 + kst * 1024 + lane * 16) = f.u;
+    }
   }
   if (stager) {
     run_tiles(j0, jlo, MaskBoth{}, std::false_type{});
