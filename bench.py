@@ -368,9 +368,12 @@ def attention_flops(plan, m):
 
 def attention_kernel_name(plan, m):
     G = m.n_q_heads // m.n_kv_heads
-    return (f"attn_fp8_kernel<{G}, {plan.attn_rows_per_item // 32}>" if m.kv_dtype == "e4m3"
-            else f"attn_mfma_kernel<{G}, {str(plan.alias_v).lower()}, "
-                 f"{str(plan.alias_k).lower()}, {plan.attn_rows_per_item // 32}>")
+    if m.kv_dtype == "e4m3":
+        return f"attn_fp8_kernel<{G}, {plan.attn_rows_per_item // 32}>"
+    if plan.attn_rows_per_item == 64:       # the pipelined kernel
+        return f"attn_pipe_kernel<{G}, {str(plan.alias_v).lower()}>"
+    return (f"attn_mfma_kernel<{G}, {str(plan.alias_v).lower()}, "
+            f"{str(plan.alias_k).lower()}, {plan.attn_rows_per_item // 32}>")
 
 
 def assembly_kernel_name(m):
@@ -484,7 +487,6 @@ def workload_leg(torch, name, steps, warmup, L=2):
     import workloads
     from paper_2609_32999_amd import staging
     from paper_2609_32999_amd.session import Session
-    from oracle import pipeline as PL
     wl = workloads.generate(name)
     m = wl.model
     sess = Session(m, wl.n_pool_pages, wl.n_req_pages, n_layers=L)
@@ -509,13 +511,13 @@ def workload_leg(torch, name, steps, warmup, L=2):
     tf = flops / (d_att["mean"] * 1e-6) / 1e12
     gbs = asm_bytes / (d_asm["mean"] * 1e-6) / 1e9
     peak, blend = attention_peaks(m)
-    c = PL.counts(wl)
     res = {"workload": f"{wl.name}: {wl.cfg.description}",
            "ms_per_step": float(np.mean(st)),
            "value": wl.prompt_tokens / (np.mean(st) * 1e-3),
            "realized": {"requests": len(wl.requests), "prompt_tokens": wl.prompt_tokens,
                         "computed_tokens": T, "gathered_tokens": plan.num_gather_tokens,
-                        "visible_pairs": c["visible_pairs"], "attention_flops": flops,
+                        "visible_pairs": int(flops / (4 * m.head_dim * m.n_q_heads)),
+                        "attention_flops": flops,
                         "assembly_bytes": asm_bytes},
            "kernel_us": {"assembly": d_asm, "attention": d_att},
            "roofline": {"bound": "mfma", "achieved": tf, "peak": peak, "unit": "TFLOP/s",
@@ -558,6 +560,9 @@ def main():
                          "rotated on load, both)")
     ap.add_argument("--no-host-tier", dest="host_tier", action="store_false",
                     help="skip timing compose and retain against a pool in pinned host memory")
+    ap.add_argument("--attn-kernel", type=int, default=0, choices=[0, 1, 2],
+                    help="bf16 attention kernel of the main plan: 0 automatic, 1 the "
+                         "pipelined kernel, 2 the row-block kernel")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="run one launch of libtsr's plain copy kernel of this size "
                          "first (to scale HBM byte counters against a kernel of known "
@@ -598,7 +603,7 @@ def main():
     for l in range(1, L):
         sess.pool_k[l].copy_(sess.pool_k[0])
         sess.pool_v[l].copy_(sess.pool_v[0])
-    plan = sess.plan(wl.requests)
+    plan = sess.plan(wl.requests, attn_kernel=args.attn_kernel)
     q, k, v = staging.fresh_inputs(sess, wl, plan)
     qs = [q] + [q.clone() for _ in range(L - 1)]
     ks = [k] + [k.clone() for _ in range(L - 1)]
@@ -608,7 +613,7 @@ def main():
     T = plan.num_compute_tokens
     torch.cuda.synchronize()
     log(f"[bench] plan T={T} gather={plan.num_gather_tokens} retain={plan.num_retain_tokens} "
-        f"items={plan.num_attn_items}")
+        f"items={plan.num_attn_items} rows/item={plan.attn_rows_per_item}")
 
     main_s = torch.cuda.current_stream()
     step_ms, asm_ms, attn_ms, retain_ms, wall = time_path(

@@ -48,7 +48,7 @@
 extern "C" {
 #endif
 
-#define TSR_ABI_VERSION 6
+#define TSR_ABI_VERSION 7
 
 typedef enum {
   TSR_OK = 0,
@@ -241,12 +241,25 @@ tsr_status tsr_plan_create(const tsr_model* model, const tsr_request* reqs,
  *             A plan with split items writes that buffer on every
  *             attention call: calls that use one plan on streams that
  *             run concurrently race there.
+ *   attn_kernel  which bf16 attention kernel the plan schedules for
+ *             (plans with bf16 activations and bf16 KV; others ignore it):
+ *               0   automatic: the row-block kernel (2), the faster of
+ *                   the two on every batch measured;
+ *               1   the pipelined kernel: items of up to two 32-row blocks,
+ *                   eight waves per workgroup, the QK^T products of the
+ *                   next key tile under the softmax of this one.  It
+ *                   applies without alias_k and when no item spans more
+ *                   than 65,536 keys; otherwise TSR_ERR_UNSUPPORTED;
+ *               2   the row-block kernel: items of one or three 32-row
+ *                   blocks (the only kernel for alias_k plans and for the
+ *                   key-range split).
  *   reserved  must be zero. */
 typedef struct {
   int32_t alias_v;
   int32_t alias_k;
   int32_t split_tiles;
-  int32_t reserved[5];
+  int32_t attn_kernel;
+  int32_t reserved[4];
 } tsr_plan_options;
 
 /* tsr_plan_workspace_size for a plan made with `options` (NULL: all zero,
@@ -293,13 +306,14 @@ int32_t tsr_plan_num_gather_tokens(const tsr_plan* plan);
 /* Number of tokens written by tsr_retain_kv. */
 int32_t tsr_plan_num_retain_tokens(const tsr_plan* plan);
 /* Number of attention work items (row tile x KV head, plus launch padding).
- * A row tile holds up to 32 consecutive computed rows, or up to 96 in plans
- * with bf16 activations and bf16 or e4m3 KV whose runs of rows with a
- * common first visible key are long enough (the MFMA kernels then run
- * three 32-row blocks per workgroup). */
+ * A row tile holds up to 32 consecutive computed rows, or up to 64 (the
+ * pipelined bf16 kernel) or 96 (the row-block kernels of bf16 and e4m3 KV)
+ * in plans whose runs of rows with a common first visible key are long
+ * enough. */
 int32_t tsr_plan_num_attn_items(const tsr_plan* plan);
-/* Most computed rows an attention item of this plan holds: 32, or 96 when
- * the MFMA kernel runs three row blocks per workgroup; -1 for a null plan. */
+/* Most computed rows an attention item of this plan holds: 32, 64 (the
+ * pipelined bf16 kernel) or 96 (three row blocks per workgroup); -1 for a
+ * null plan. */
 int32_t tsr_plan_attn_rows_per_item(const tsr_plan* plan);
 /* Number of attention items whose key range was split (split_tiles), each
  * merged by the second kernel; 0 when none; -1 for a null plan. */

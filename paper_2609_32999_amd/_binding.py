@@ -83,7 +83,7 @@ class tsr_request(ctypes.Structure):
 
 class tsr_plan_options(ctypes.Structure):
     _fields_ = [("alias_v", c_int32), ("alias_k", c_int32), ("split_tiles", c_int32),
-                ("reserved", c_int32 * 5)]
+                ("attn_kernel", c_int32), ("reserved", c_int32 * 4)]
 
 
 class tsr_replay_config(ctypes.Structure):
@@ -287,9 +287,9 @@ def tsr_rope_table_init(model: tsr_model, dev_table, table_bytes: int, stream=No
 
 def tsr_plan_workspace_size(model: tsr_model, batch: RequestBatch, n_pool_pages: int,
                             n_req_pages: int, alias_v: bool = False, alias_k: bool = False,
-                            split_tiles: int = 0) -> int:
+                            split_tiles: int = 0, attn_kernel: int = 0) -> int:
     opts = tsr_plan_options(alias_v=int(alias_v), alias_k=int(alias_k),
-                            split_tiles=split_tiles)
+                            split_tiles=split_tiles, attn_kernel=attn_kernel)
     n = lib().tsr_plan_workspace_size_ex(ctypes.byref(model), batch.array, batch.n,
                                          n_pool_pages, n_req_pages, ctypes.byref(opts))
     if n == 0:
@@ -370,11 +370,11 @@ class Plan:
 def tsr_plan_create(model: tsr_model, batch: RequestBatch, n_pool_pages: int,
                     n_req_pages: int, dev_rope_table=None, dev_workspace=None,
                     workspace_bytes: int = 0, stream=None, alias_v: bool = False,
-                    alias_k: bool = False, split_tiles: int = 0) -> Plan:
+                    alias_k: bool = False, split_tiles: int = 0, attn_kernel: int = 0) -> Plan:
     out = c_void_p()
-    if alias_v or alias_k or split_tiles:
+    if alias_v or alias_k or split_tiles or attn_kernel:
         opts = tsr_plan_options(alias_v=int(alias_v), alias_k=int(alias_k),
-                                split_tiles=split_tiles)
+                                split_tiles=split_tiles, attn_kernel=attn_kernel)
         _check(lib().tsr_plan_create_ex(ctypes.byref(model), batch.array, batch.n,
                                         n_pool_pages, n_req_pages, ctypes.byref(opts),
                                         _ptr(dev_rope_table), _ptr(dev_workspace),
@@ -392,12 +392,12 @@ def tsr_plan_create(model: tsr_model, batch: RequestBatch, n_pool_pages: int,
 def tsr_plan_create_static(model: tsr_model, batch: RequestBatch, n_pool_pages: int,
                            n_req_pages: int, dev_rope_table, stream=None,
                            alias_v: bool = False, alias_k: bool = False,
-                           split_tiles: int = 0) -> Plan:
+                           split_tiles: int = 0, attn_kernel: int = 0) -> Plan:
     """A plan whose device image lives in the library's own plan area (no
     workspace); a later static plan on the same device supersedes it."""
     out = c_void_p()
     opts = tsr_plan_options(alias_v=int(alias_v), alias_k=int(alias_k),
-                            split_tiles=split_tiles)
+                            split_tiles=split_tiles, attn_kernel=attn_kernel)
     _check(lib().tsr_plan_create_static(ctypes.byref(model), batch.array, batch.n,
                                         n_pool_pages, n_req_pages, ctypes.byref(opts),
                                         _ptr(dev_rope_table), _stream(stream),

@@ -88,9 +88,10 @@ tsr_status attn_common(const tsr_plan* p, int32_t part, const void* q, const voi
 // Options as build_plan takes them; a static plan's automatic split is off
 // (its image must fit the static plan area).
 tsr_status resolve_options(const tsr_plan_options* options, bool static_plan, bool* alias_v,
-                           bool* alias_k, int32_t* split) {
+                           bool* alias_k, int32_t* split, int32_t* attn_kernel) {
   *alias_v = *alias_k = false;
   *split = static_plan ? -1 : 0;
+  *attn_kernel = 0;
   if (!options) return TSR_OK;
   for (int32_t r : options->reserved)
     if (r != 0) {
@@ -109,9 +110,14 @@ tsr_status resolve_options(const tsr_plan_options* options, bool static_plan, bo
     set_error("tsr_plan_options.split_tiles must be -1, 0 or positive");
     return TSR_ERR_INVALID_ARG;
   }
+  if (options->attn_kernel < 0 || options->attn_kernel > 2) {
+    set_error("tsr_plan_options.attn_kernel must be 0, 1 or 2");
+    return TSR_ERR_INVALID_ARG;
+  }
   *alias_v = options->alias_v == 1;
   *alias_k = options->alias_k == 1;
   if (options->split_tiles != 0) *split = options->split_tiles;
+  *attn_kernel = options->attn_kernel;
   return TSR_OK;
 }
 
@@ -123,12 +129,13 @@ size_t plan_workspace_size(const tsr_model* model, const tsr_request* reqs, int3
   size_t bytes = 0;
   guarded([&]() -> tsr_status {
     bool alias_v, alias_k;
-    int32_t split;
-    tsr_status st = resolve_options(options, static_plan, &alias_v, &alias_k, &split);
+    int32_t split, attn_kernel;
+    tsr_status st =
+        resolve_options(options, static_plan, &alias_v, &alias_k, &split, &attn_kernel);
     if (st != TSR_OK) return st;
     tsr_plan tmp{};
     st = build_plan(model, reqs, n_req, n_pool_pages, n_req_pages, alias_v, alias_k, split,
-                    &tmp);
+                    attn_kernel, &tmp);
     if (st == TSR_OK) bytes = tmp.ws_bytes;
     return st;
   });
@@ -147,11 +154,13 @@ tsr_status create_plan(const tsr_model* model, const tsr_request* reqs, int32_t 
     }
     *out_plan = nullptr;
     bool alias_v, alias_k;
-    int32_t split;
-    tsr_status st = resolve_options(options, static_plan, &alias_v, &alias_k, &split);
+    int32_t split, attn_kernel;
+    tsr_status st =
+        resolve_options(options, static_plan, &alias_v, &alias_k, &split, &attn_kernel);
     if (st != TSR_OK) return st;
     tsr_plan* p = new tsr_plan();
-    st = build_plan(model, reqs, n_req, n_pool_pages, n_req_pages, alias_v, alias_k, split, p);
+    st = build_plan(model, reqs, n_req, n_pool_pages, n_req_pages, alias_v, alias_k, split,
+                    attn_kernel, p);
     if (st != TSR_OK) {
       delete p;
       return st;

@@ -38,6 +38,7 @@
 #include <cmath>
 #include <type_traits>
 
+#include "attn_common.h"
 #include "kernels_common.h"
 #include "tsr_internal.h"
 
@@ -138,66 +139,6 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(
 }
 
 // ------------------------------------------------------------- bf16 mode
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
-typedef float f32x16 __attribute__((ext_vector_type(16)));
-
-
-
-union Frag {
-  uint4 u;
-  uint32_t w[4];
-  bf16x8 b;
-  f16x8 h;
-};
-
-
-constexpr int kD = 128;
-// Keys per tile.  32-key tiles keep a wave's registers under 168 (three
-// waves per SIMD) and a workgroup's LDS under 53 KB (three workgroups per
-// CU): the kernel is bound by latency, and the third wave per SIMD hides
-// more of it than the per-tile overhead costs.
-constexpr int kKT = 32;
-// V^T rows (fp16) are 16-byte aligned and hold each 16-key step permuted as
-// keys [0..3, 8..11, 4..7, 12..15], so that the eight keys a lane feeds to
-// the PV MFMA (4h .. 4h+3 and 8+4h .. 8+4h+3 for half-wave h, the order in
-// which the S^T accumulators hand out P^T) are one 16-byte LDS read.
-constexpr int kVStr = kKT + 8;         // fp16 elements per V^T row in LDS
-// A K tile sits in LDS in the order the QK^T MFMAs consume it: one 1 KB
-// block per 16-dim step kst, in which lane l's 16 bytes (at l * 16) are
-// K[l % 32][16 kst + 8 (l / 32) .. + 8].  Fragment reads are then
-// lane-contiguous (no bank conflicts, immediate offsets), and one direct
-// global->LDS load of 16 bytes per lane fills one block.
-constexpr int kKBlk = 1024;
-constexpr int kKBytes = 8 * kKBlk;
-constexpr int kVBytes = kD * kVStr * 2;
-// s_waitcnt immediate that waits for every outstanding vector memory
-// access (direct global->LDS loads included) and leaves the other counters.
-constexpr int kWaitVm0 = 0x0F70;
-// Lazy rescale threshold (log2 units): P may grow to 2^kLazy before the
-// running max is moved.
-constexpr float kLazy = 8.0f;
-constexpr float kLazySum = 256.0f;   // 2^kLazy
-
-// Direct global->LDS load of 16 bytes per lane: lane l's bytes land at LDS
-// address lds + 16 l (lds wave-uniform).  Written as assembly so that the
-// compiler does not take the LDS write for a possible alias of the LDS reads
-// that follow it (it would wait for the load before each of them); callers
-// wait for these loads themselves (s_waitcnt vmcnt) before the barrier that
-// hands the buffer to the workgroup.  M0 holds no other value in the
-// kernels that use this.
-#pragma clang diagnostic push
-#pragma clang diagnostic ignored "-Winline-asm"
-__device__ __forceinline__ void lds_dma16(const void* src, uint32_t lds) {
-  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
-               :: "v"(src), "s"(lds) : "m0");
-}
-#pragma clang diagnostic pop
-
-__device__ __forceinline__ uint32_t lds_addr(const void* p) {
-  return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const void*)p;
-}
-
 __device__ __forceinline__ uint32_t pack_f16x2(float a, float b) {
   // bf16 values convert to fp16 exactly inside fp16's normal range (the
   // largest bf16 below fp16's maximum is 65280); the staging code refuses
@@ -642,8 +583,8 @@ __global__ __launch_bounds__(256 * R, 3) void attn_mfma_kernel(
     Frag a, b;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      a.w[e] = f32_to_bf16(lo[2 * e]) | (f32_to_bf16(lo[2 * e + 1]) << 16);
-      b.w[e] = f32_to_bf16(hi[2 * e]) | (f32_to_bf16(hi[2 * e + 1]) << 16);
+      a.w[e] = pack_bf16x2(lo[2 * e], lo[2 * e + 1]);
+      b.w[e] = pack_bf16x2(hi[2 * e], hi[2 * e + 1]);
     }
     qf[ks] = a.b;
     qf[ks + 4] = b.b;
@@ -696,8 +637,8 @@ __global__ __launch_bounds__(256 * R, 3) void attn_mfma_kernel(
     for (int rg = 0; rg < 4; ++rg) {
       const int d0 = 32 * db + 8 * rg + 4 * lh;
       uint2 v;
-      v.x = f32_to_bf16(o[db][4 * rg] * inv) | (f32_to_bf16(o[db][4 * rg + 1] * inv) << 16);
-      v.y = f32_to_bf16(o[db][4 * rg + 2] * inv) | (f32_to_bf16(o[db][4 * rg + 3] * inv) << 16);
+      v.x = pack_bf16x2(o[db][4 * rg] * inv, o[db][4 * rg + 1] * inv);
+      v.y = pack_bf16x2(o[db][4 * rg + 2] * inv, o[db][4 * rg + 3] * inv);
       *reinterpret_cast<uint2*>(op + d0) = v;
     }
   if (lse && lh == 0) lse[(int64_t)row * n_q_heads + hq] = m * scale + logf(lt);
@@ -792,6 +733,8 @@ hipError_t launch_attn(const tsr_plan* p, int32_t part, const AttnItem* items,
 #undef TSR_F32K
     return hipGetLastError();
   }
+  if (p->row_blocks == kPipeRowBlocks)
+    return launch_attn_pipe(p, items, n_items, pool_v, q, req_k, req_v, out, lse, s);
   const float sl2e = (float)((double)p->scale * 1.4426950408889634);
 #define TSR_MFMA(GG, AV, AK)                                                       \
   if (p->row_blocks == kMaxRowBlocks)                                              \

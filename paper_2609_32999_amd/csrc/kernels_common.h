@@ -19,6 +19,15 @@ __device__ __forceinline__ uint32_t f32_to_bf16(float f) {
   return u >> 16;
 }
 
+// Two fp32 values -> packed bf16 pair (lo in bits 0..15), round to nearest
+// even in hardware (v_cvt_pk_bf16_f32): one instruction per pair, the same
+// bits as f32_to_bf16 for every finite input.
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+  const bf16x2_t h = {(__bf16)lo, (__bf16)hi};
+  return __builtin_bit_cast(uint32_t, h);
+}
+
 // Rotate n pairs (lo[i], hi[i]) by angles with cosine c[i] and sine s[i]:
 //   lo' = lo*c - hi*s,  hi' = hi*c + lo*s
 // Each product is rounded to fp32 and then added once (no fused

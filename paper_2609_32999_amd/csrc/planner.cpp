@@ -92,7 +92,8 @@ tsr_status check_model(const tsr_model* m) {
 
 tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
                       int32_t n_req, int32_t n_pool_pages, int32_t n_req_pages,
-                      bool alias_v, bool alias_k, int32_t split_tiles, tsr_plan* p) {
+                      bool alias_v, bool alias_k, int32_t split_tiles, int32_t attn_kernel,
+                      tsr_plan* p) {
   tsr_status st = check_model(model);
   if (st != TSR_OK) return st;
   if (n_req < 0) return fail(TSR_ERR_INVALID_ARG, "n_req < 0");
@@ -371,12 +372,14 @@ tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
   struct Item { AttnItem it; int64_t cost; int group; int part; };
   std::vector<Item> items;
   int32_t max_kv = 0;
+  int64_t max_blocks = 0;   // most 16-key blocks an item's key tiles span
   // Builds the items for row blocks of kTileRows rows, rb per item; returns
   // the share of the items' (row block x key tile) slots that hold keys a
   // row block needs (a row block skips the tiles past its last row).
   auto build_items = [&](int rb) -> double {
     items.clear();
     max_kv = 0;
+    max_blocks = 0;
     const int32_t tile_rows = kTileRows * rb;
     int64_t need = 0, slots = 0;
     for (int r = 0; r < n_req; ++r) {
@@ -390,6 +393,7 @@ tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
           const int32_t lo = p->row_pos[t0], hi = p->row_pos[t0 + n - 1];
           max_kv = std::max(max_kv, hi + 1);
           const int32_t t_lo = kv_lo / kMfmaKeys;
+          max_blocks = std::max<int64_t>(max_blocks, 2 * ((int64_t)hi / kMfmaKeys + 1 - t_lo));
           slots += (int64_t)rb * (hi / kMfmaKeys + 1 - t_lo);
           for (int32_t b0 = 0; b0 < n; b0 += kTileRows)
             need += p->row_pos[t0 + std::min(n, b0 + kTileRows) - 1] / kMfmaKeys + 1 - t_lo;
@@ -416,9 +420,32 @@ tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
   // workgroup (their K/V staging then serves three times the rows) unless
   // short runs of rows (unit-local attention) would leave too many row
   // blocks idle; the fp32 kernel takes one row block.
+  // attn_kernel == 1 (bf16 KV only) asks for the pipelined kernel
+  // (attn_pipe.hip, two row blocks per item); it cannot rotate K on load
+  // and its page-id table bounds an item's keys.  Measured on the RAG
+  // batches it is slower than the row-block kernel, which stays the
+  // automatic choice.
   p->row_blocks = 1;
-  if (m.act_dtype == TSR_BF16 && (m.kv_dtype == TSR_BF16 || m.kv_dtype == TSR_E4M3) &&
-      build_items(kMaxRowBlocks) >= kMinRowBlockUse) {
+  const bool bf16_kv = m.act_dtype == TSR_BF16 && m.kv_dtype == TSR_BF16;
+  auto split_threshold = [&](int64_t total_tiles) -> int64_t {
+    return split_tiles > 0 ? split_tiles
+                           : std::max<int64_t>(kMinSplitTiles,
+                                               (total_tiles + kSplitSlots - 1) / kSplitSlots);
+  };
+  bool pipe = false;
+  if (bf16_kv && attn_kernel == 1) {
+    build_items(kPipeRowBlocks);
+    if (alias_k || max_blocks > kPipeMaxBlocks)
+      return fail(TSR_ERR_UNSUPPORTED,
+                  alias_k ? "the pipelined attention kernel does not rotate K on load"
+                          : "an attention item spans more keys than the pipelined kernel takes");
+    pipe = true;
+  }
+  if (pipe) {
+    p->row_blocks = kPipeRowBlocks;
+  } else if (m.act_dtype == TSR_BF16 &&
+             (m.kv_dtype == TSR_BF16 || m.kv_dtype == TSR_E4M3) &&
+             build_items(kMaxRowBlocks) >= kMinRowBlockUse) {
     p->row_blocks = kMaxRowBlocks;
   } else {
     build_items(1);
@@ -441,9 +468,7 @@ tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
     };
     int64_t total = 0;
     for (const Item& x : items) total += tiles_of(x.it);
-    int64_t S = split_tiles > 0 ? split_tiles
-                                : std::max<int64_t>(kMinSplitTiles,
-                                                    (total + kSplitSlots - 1) / kSplitSlots);
+    int64_t S = split_threshold(total);
     auto slots_for = [&](int64_t lim) {
       int64_t n = 0;
       for (const Item& x : items) {

@@ -22,6 +22,11 @@ constexpr int kTileRows = 32;
 // tile slots hold work.
 constexpr int kMaxRowBlocks = 3;
 constexpr double kMinRowBlockUse = 0.8;
+// Row blocks per item of the pipelined bf16 kernel (attn_pipe.hip), and
+// the most 16-key blocks an item of it may span (their page ids sit in
+// LDS: 65,536 keys).
+constexpr int kPipeRowBlocks = 2;
+constexpr int kPipeMaxBlocks = 4096;
 // Keys per attention KV tile (granularity of the host-tier split of items).
 constexpr int kKvTile = 64;
 // Keys per tile of the bf16 MFMA attention kernel.
@@ -148,7 +153,7 @@ struct tsr_plan {
   // [0] none (runnable before compose), [1] some; each scheduled on its own
   int32_t n_items_part[2];
   int32_t max_kv_len;
-  int32_t row_blocks;       // row blocks per attention item (1 or kMaxRowBlocks)
+  int32_t row_blocks;       // row blocks per attention item (1, kPipeRowBlocks or kMaxRowBlocks)
   // key-range split items: merge descriptors (part 0's first) and buffer
   int32_t n_combine;
   int32_t n_combine_part[2];
@@ -217,7 +222,8 @@ tsr_status check_model(const tsr_model* m);
 // automatic threshold, < 0 never (see tsr_plan_options).
 tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
                       int32_t n_req, int32_t n_pool_pages, int32_t n_req_pages,
-                      bool alias_v, bool alias_k, int32_t split_tiles, tsr_plan* plan);
+                      bool alias_v, bool alias_k, int32_t split_tiles, int32_t attn_kernel,
+                      tsr_plan* plan);
 
 // tsr_plan_workspace_size_ex / tsr_plan_create_ex; static_plan: the plan
 // goes to the static plan area (automatic key-range splitting off).
@@ -252,6 +258,10 @@ hipError_t launch_attn(const tsr_plan* p, int32_t part, const AttnItem* items,
                        int32_t n_items, const void* pool_k, const void* pool_v,
                        const void* q, const void* req_k, const void* req_v, void* out,
                        float* lse, hipStream_t s);
+// the pipelined bf16 kernel (plans with row_blocks == kPipeRowBlocks)
+hipError_t launch_attn_pipe(const tsr_plan* p, const AttnItem* items, int32_t n_items,
+                            const void* pool_v, const void* q, const void* req_k,
+                            const void* req_v, void* out, float* lse, hipStream_t s);
 hipError_t launch_retain(const tsr_plan* p, const void* k, const void* v,
                          void* pool_k, void* pool_v, hipStream_t s);
 

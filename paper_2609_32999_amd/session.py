@@ -102,32 +102,36 @@ class Session:
 
     # ------------------------------------------------------------- plans
     def plan(self, requests, stream=None, alias_v: bool = False, alias_k: bool = False,
-             split_tiles: int = 0):
+             split_tiles: int = 0, attn_kernel: int = 0):
         """Validate and upload a batch's plan; `alias_v` selects V aliasing
         (attention reads V of whole gathered pages from the pool), `alias_k`
         K rotated on load (attention reads their pre-RoPE K from the pool),
         `split_tiles` the key-range split of long attention items (0
-        automatic, > 0 the most 32-key tiles an item keeps, -1 never)."""
+        automatic, > 0 the most 32-key tiles an item keeps, -1 never),
+        `attn_kernel` the bf16 attention kernel (0 automatic, 1 pipelined,
+        2 row-block)."""
         batch = B.RequestBatch(requests)
         ws_bytes = B.tsr_plan_workspace_size(self.model, batch, self.n_pool_pages,
-                                             self.n_req_pages, alias_v, alias_k, split_tiles)
+                                             self.n_req_pages, alias_v, alias_k, split_tiles,
+                                             attn_kernel)
         ws = torch.empty(ws_bytes, dtype=torch.uint8, device=self.device)
         plan = B.tsr_plan_create(self.model, batch, self.n_pool_pages, self.n_req_pages,
                                  self.rope, ws, ws_bytes, stream or self.stream,
-                                 alias_v=alias_v, alias_k=alias_k, split_tiles=split_tiles)
+                                 alias_v=alias_v, alias_k=alias_k, split_tiles=split_tiles,
+                                 attn_kernel=attn_kernel)
         plan.workspace = ws     # keep the workspace alive with the plan
         plan.batch = batch
         return plan
 
     def plan_static(self, requests, stream=None, alias_v: bool = False,
-                    alias_k: bool = False, split_tiles: int = 0):
+                    alias_k: bool = False, split_tiles: int = 0, attn_kernel: int = 0):
         """A plan in the library's own device plan area (no workspace is
         allocated); a later static plan on this device supersedes it."""
         batch = B.RequestBatch(requests)
         plan = B.tsr_plan_create_static(self.model, batch, self.n_pool_pages,
                                         self.n_req_pages, self.rope, stream or self.stream,
                                         alias_v=alias_v, alias_k=alias_k,
-                                        split_tiles=split_tiles)
+                                        split_tiles=split_tiles, attn_kernel=attn_kernel)
         plan.batch = batch
         return plan
 

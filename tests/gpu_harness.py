@@ -65,12 +65,14 @@ def say(msg: str) -> None:
 class GpuRun:
     """Runs compose -> prefill_attn -> retain on a workload (one layer)."""
 
-    def __init__(self, wl, with_lse=True, pool="device", assemble=False, split_tiles=0):
+    def __init__(self, wl, with_lse=True, pool="device", assemble=False, split_tiles=0,
+                 attn_kernel=0, alias_v=False):
         self.wl = wl
         m = wl.model
         say(f"[gpu] workload={wl.name} seed={wl.seed} H={m.n_q_heads}/{m.n_kv_heads} "
             f"d={m.head_dim} {m.kv_dtype} prompt_tokens={wl.prompt_tokens} pool={pool} "
-            f"assemble={assemble} split_tiles={split_tiles}")
+            f"assemble={assemble} split_tiles={split_tiles} attn_kernel={attn_kernel} "
+            f"alias_v={alias_v}")
         s = Session(m, wl.n_pool_pages, wl.n_req_pages, pool=pool)
         self.sess = s
         for t in (s.pool_k, s.pool_v, s.req_k, s.req_v):
@@ -82,7 +84,8 @@ class GpuRun:
         self.pool_k0 = s.pool_k.clone()
         self.pool_v0 = s.pool_v.clone()
         self.pool_s0 = s.pool_scale.clone() if s.e4m3 else None
-        self.plan = s.plan(wl.requests, split_tiles=split_tiles)
+        self.plan = s.plan(wl.requests, split_tiles=split_tiles, attn_kernel=attn_kernel,
+                           alias_v=alias_v)
         self.q, self.k, self.v = staging.fresh_inputs(s, wl, self.plan)
         self.pos, self.req = self.plan.compute_positions()
         if assemble:            # compose + append in one launch, then attention
@@ -106,7 +109,7 @@ class GpuRun:
         torch.cuda.synchronize()
         say(f"[gpu] ran T={self.plan.num_compute_tokens} gather={self.plan.num_gather_tokens} "
             f"retain={self.plan.num_retain_tokens} items={self.plan.num_attn_items} "
-            f"splits={self.plan.num_attn_splits}")
+            f"rows/item={self.plan.attn_rows_per_item} splits={self.plan.num_attn_splits}")
 
     def request_kv(self, r):
         return staging.request_kv(self.sess, self.wl, r)

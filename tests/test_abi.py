@@ -44,7 +44,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_abi_version():
-    assert P.tsr_abi_version() == 6
+    assert P.tsr_abi_version() == 7
 
 
 @pytest.mark.parametrize("name", ["tiny", "small_bf16", "small_f32", "small_bf16_g8",
@@ -90,30 +90,54 @@ def _items_per_kv_head(wl, rows_per_item):
                                         ("agent8b", "local"), ("long70b", "global"),
                                         ("fp8rag", "global"), ("small_f32", "global")])
 def test_attention_row_blocks(name, scope):
-    """bf16 plans put MULTI_ROWS // 32 row blocks of 32 rows in an item unless
-    fewer than 80 % of the items' block x tile slots would hold work; other
-    dtypes use one."""
+    """Rows per attention item.  bf16 and e4m3 KV: three 32-row blocks
+    unless fewer than 80 % of the items' block x tile slots would hold
+    work, then one; fp32: one."""
     cfg = workloads.get_config(name)
     if scope != "global":
         cfg = cfg.with_(miss_scope=scope)
     wl = workloads.make_workload(cfg)
     m = wl.model
     n1, _ = _items_per_kv_head(wl, 32)
-    n3, use3 = _items_per_kv_head(wl, MULTI_ROWS)
-    three = m.kv_dtype in ("bf16", "e4m3") and m.act_dtype == "bf16" and use3 >= 0.8
-    groups = (m.n_q_heads // m.n_kv_heads) // 4 if m.act_dtype == "bf16" and \
+    n3, use3 = _items_per_kv_head(wl, 96)
+    bf16_act = m.act_dtype == "bf16"
+    if bf16_act and m.kv_dtype in ("bf16", "e4m3") and use3 >= 0.8:
+        rows, n = 96, n3
+    else:
+        rows, n = 32, n1
+    groups = (m.n_q_heads // m.n_kv_heads) // 4 if bf16_act and \
         m.n_q_heads // m.n_kv_heads > 4 else 1
     per = m.n_kv_heads * groups
     plan = _plan(wl)
     # launch padding only adds items: multi-block items give fewer items than
     # one-block items would need, one row block at least that many
-    if three:
-        assert n3 * per <= plan.num_attn_items < n1 * per, (plan.num_attn_items, n1, n3, use3)
+    if rows > 32:
+        assert n * per <= plan.num_attn_items < n1 * per, (plan.num_attn_items, n1, n, rows)
     else:
         assert plan.num_attn_items >= n1 * per, (plan.num_attn_items, n1, n3, use3)
-    assert bool(three) == ((name, scope) in {("rag8b", "global"), ("long70b", "global"),
-                                             ("fp8rag", "global")})
-    assert plan.attn_rows_per_item == (MULTI_ROWS if three else 32)
+    assert plan.attn_rows_per_item == rows
+    expect = {("rag8b", "global"): 96, ("long70b", "global"): 96, ("fp8rag", "global"): 96}
+    assert rows == expect.get((name, scope), 32)
+
+
+@pytest.mark.parametrize("name", ["rag8b", "small_bf16"])
+def test_attention_kernel_option(name):
+    """attn_kernel: 1 asks for the pipelined kernel (64-row items, refused
+    where it does not apply: K rotated on load), 2 for the row-block
+    kernel, 0 (automatic) for the row-block kernel, anything else is an
+    invalid argument."""
+    wl = workloads.generate(name)
+    mk = lambda **kw: P.tsr_plan_create(_model(wl), P.RequestBatch(wl.requests),
+                                        wl.n_pool_pages, wl.n_req_pages, **kw)
+    assert mk(attn_kernel=1).attn_rows_per_item == 64
+    assert mk(attn_kernel=2).attn_rows_per_item in (32, 96)
+    assert mk().attn_rows_per_item == mk(attn_kernel=2).attn_rows_per_item
+    with pytest.raises(P.TsrError) as e:
+        mk(attn_kernel=1, alias_k=True)
+    assert e.value.status == P.TSR_ERR_UNSUPPORTED
+    with pytest.raises(P.TsrError) as e:
+        mk(attn_kernel=3)
+    assert e.value.status == P.TSR_ERR_INVALID_ARG
 
 
 def _tiny_req(**over):
@@ -414,7 +438,8 @@ def test_split_automatic_threshold():
     compute unit: the RAG batch under the LOCAL scope (its longest items,
     the suffix rows, hold 163 tiles against a mean of 288 per unit) is not
     split; one request of it alone is (its suffix rows then far exceed the
-    mean); under the GLOBAL scope items hold three row blocks and never are."""
+    mean); under the GLOBAL scope items hold three row blocks and never
+    are."""
     wl, (local,), _ = _split_plans("rag8b", "local", 0)
     assert local.attn_rows_per_item == 32 and local.num_attn_splits == 0
     one = P.tsr_plan_create(_model(wl), P.RequestBatch(wl.requests[:1]), wl.n_pool_pages,

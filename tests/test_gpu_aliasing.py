@@ -50,14 +50,14 @@ MODES = {"v": dict(alias_v=True), "k": dict(alias_k=True),
 
 
 class Run:
-    def __init__(self, wl, mode=None, assemble=False, split_tiles=0):
+    def __init__(self, wl, mode=None, assemble=False, split_tiles=0, attn_kernel=0):
         m = wl.model
         self.wl = wl
         s = self.sess = Session(m, wl.n_pool_pages, wl.n_req_pages)
         for t in (s.pool_k, s.pool_v, s.req_k, s.req_v):
             fill_sentinel(t)
         staging.upload_pool(s, wl)
-        self.plan = p = s.plan(wl.requests, split_tiles=split_tiles,
+        self.plan = p = s.plan(wl.requests, split_tiles=split_tiles, attn_kernel=attn_kernel,
                                **(MODES[mode] if mode else {}))
         q, k, v = staging.fresh_inputs(s, wl, p)
         self.pos, self.req = p.compute_positions()
@@ -100,8 +100,11 @@ def test_aliasing_equals_composed_path(name, over, mode):
     wl = workloads.make_workload(workloads.get_config(name).with_(**over))
     pages = aliased_pages(wl)
     say(f"[gpu] aliasing {mode}: workload={wl.name} seed={wl.seed} aliased pages={len(pages)}")
-    ref = Run(wl)
-    run = Run(wl, mode, assemble=(mode == "kv"))
+    # the same kernel on both sides (K rotated on load runs on the row-block
+    # kernel only)
+    kern = 2 if "k" in mode else 0
+    ref = Run(wl, attn_kernel=kern)
+    run = Run(wl, mode, assemble=(mode == "kv"), attn_kernel=kern)
     assert len(pages) > 0
     assert run.plan.num_aliased_pages == (len(pages) if "v" in mode else 0)
     assert run.plan.num_aliased_k_pages == (len(pages) if "k" in mode else 0)
@@ -119,8 +122,8 @@ def test_aliasing_three_row_blocks(mode):
     wl = workloads.make_workload(workloads.get_config("rag8b").with_(n_requests=2))
     pages = aliased_pages(wl)
     say(f"[gpu] aliasing {mode}: workload={wl.name} seed={wl.seed} aliased pages={len(pages)}")
-    ref = Run(wl)
-    run = Run(wl, mode, assemble=True)
+    ref = Run(wl, attn_kernel=2)
+    run = Run(wl, mode, assemble=True, attn_kernel=2)
     assert run.plan.attn_rows_per_item > 32
     assert len(pages) > 0
     _check_against_composed(wl, run, ref, mode, pages)
@@ -137,8 +140,8 @@ def test_aliasing_with_key_range_split(mode):
     wl = workloads.make_workload(workloads.get_config("small_bf16").with_(
         **{**ALIGNED, "miss_scope": "local"}))
     pages = aliased_pages(wl)
-    ref = Run(wl, split_tiles=2)
-    run = Run(wl, mode, assemble=(mode == "kv"), split_tiles=2)
+    ref = Run(wl, split_tiles=2, attn_kernel=2)
+    run = Run(wl, mode, assemble=(mode == "kv"), split_tiles=2, attn_kernel=2)
     assert run.plan.num_attn_splits > 0 and run.plan.num_attn_splits == ref.plan.num_attn_splits
     _check_against_composed(wl, run, ref, mode, pages)
     for r in range(len(wl.requests)):
