@@ -243,16 +243,22 @@ tsr_status tsr_plan_create(const tsr_model* model, const tsr_request* reqs,
  *             run concurrently race there.
  *   attn_kernel  which bf16 attention kernel the plan schedules for
  *             (plans with bf16 activations and bf16 KV; others ignore it):
- *               0   automatic: the row-block kernel (2), the faster of
- *                   the two on every batch measured;
+ *               0   automatic: the row-block kernel's rule (2), the faster
+ *                   choice on every batch measured;
  *               1   the pipelined kernel: items of up to two 32-row blocks,
  *                   eight waves per workgroup, the QK^T products of the
  *                   next key tile under the softmax of this one.  It
  *                   applies without alias_k and when no item spans more
  *                   than 65,536 keys; otherwise TSR_ERR_UNSUPPORTED;
- *               2   the row-block kernel: items of one or three 32-row
- *                   blocks (the only kernel for alias_k plans and for the
- *                   key-range split).
+ *               2   the row-block kernel: items of three 32-row blocks,
+ *                   cut from each request's rows grouped by first visible
+ *                   key, when at least 60 % of their row-block x key-tile
+ *                   slots hold work and there are at least 256 of them
+ *                   (one per compute unit); else of one row block;
+ *               3   the row-block kernel, three row blocks;
+ *               4   the row-block kernel, one row block.
+ *             The row-block kernel is the only one for alias_k plans and
+ *             for the key-range split.
  *   reserved  must be zero. */
 typedef struct {
   int32_t alias_v;

@@ -110,8 +110,8 @@ tsr_status resolve_options(const tsr_plan_options* options, bool static_plan, bo
     set_error("tsr_plan_options.split_tiles must be -1, 0 or positive");
     return TSR_ERR_INVALID_ARG;
   }
-  if (options->attn_kernel < 0 || options->attn_kernel > 2) {
-    set_error("tsr_plan_options.attn_kernel must be 0, 1 or 2");
+  if (options->attn_kernel < 0 || options->attn_kernel > 4) {
+    set_error("tsr_plan_options.attn_kernel must be 0 .. 4");
     return TSR_ERR_INVALID_ARG;
   }
   *alias_v = options->alias_v == 1;
@@ -189,6 +189,7 @@ tsr_status create_plan(const tsr_model* model, const tsr_request* reqs, int32_t 
       const float* table = static_cast<const float*>(dev_rope_table);
       p->dev.gather = reinterpret_cast<const GatherDesc*>(base + p->off_gather);
       p->dev.rows = reinterpret_cast<const RowDesc*>(base + p->off_rows);
+      p->dev.attn_rows = reinterpret_cast<const AttnRow*>(base + p->off_attn_rows);
       p->dev.retain = reinterpret_cast<const RetainDesc*>(base + p->off_retain);
       p->dev.items = reinterpret_cast<const AttnItem*>(base + p->off_items);
       for (int q = 0; q < 2; ++q)
@@ -299,7 +300,7 @@ int32_t tsr_plan_attn_rows_per_item(const tsr_plan* p) {
   return p ? kTileRows * p->row_blocks : -1;
 }
 int32_t tsr_plan_num_aliased_pages(const tsr_plan* p) { return p ? p->n_aliased : -1; }
-int32_t tsr_plan_num_attn_splits(const tsr_plan* p) { return p ? p->n_combine : -1; }
+int32_t tsr_plan_num_attn_splits(const tsr_plan* p) { return p ? p->n_split_items : -1; }
 int32_t tsr_plan_num_aliased_k_pages(const tsr_plan* p) { return p ? p->n_aliased_k : -1; }
 
 int32_t tsr_plan_num_attn_items_part(const tsr_plan* p, int32_t part) {

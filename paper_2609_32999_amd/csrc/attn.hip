@@ -10,8 +10,10 @@
 // Three kernels:
 //   attn_f32_kernel   fp32 reference mode, scalar, one workgroup per item.
 //   attn_mfma_kernel  bf16 mode.  Work item = R row blocks of up to 32
-//                     consecutive computed rows of one request x one KV head
-//                     (R = 1 or 3, chosen per plan); the query heads of that
+//                     rows of one request x one KV head (R = 1 or 3, chosen
+//                     per plan), consecutive in the plan's item row order
+//                     (AttnRow: with R = 3 the rows of each request grouped
+//                     by first visible key); the query heads of that
 //                     KV head are packed into the workgroup (four waves per
 //                     row block, one head each; G = 8 takes two items), so
 //                     every K/V tile staged in LDS feeds all of them.  Per
@@ -33,7 +35,8 @@
 //                     one row block (three 4-wave workgroups per CU) and
 //                     85.5 KB with three (one 12-wave workgroup per CU).
 //                     An item whose key range the plan split writes its
-//                     normalized rows and log-sum-exp in fp32 instead.
+//                     normalized rows and log-sum-exp in fp32 instead (one
+//                     split buffer slot per row block).
 //   attn_merge_kernel merges the key ranges of split items into out, lse.
 #include <cmath>
 #include <type_traits>
@@ -177,7 +180,7 @@ __global__ __launch_bounds__(256 * R, 3) void attn_mfma_kernel(
     const uint16_t* __restrict__ pool_v,
     const AttnItem* __restrict__ items, const int32_t* __restrict__ bts,
     const int32_t* __restrict__ vbts, const int32_t* __restrict__ kbts,
-    const RowDesc* __restrict__ rows,
+    const AttnRow* __restrict__ arows,
     const float* __restrict__ rope_cos, const float* __restrict__ rope_sin,
     uint16_t* __restrict__ out, float* __restrict__ lse, float* __restrict__ split_o,
     float* __restrict__ split_lse, int n_q_heads, int n_kv_heads, int log2_page, float scale,
@@ -214,8 +217,11 @@ __global__ __launch_bounds__(256 * R, 3) void attn_mfma_kernel(
   const int32_t* bt = (AK ? kbts : bts) + it.bt_off;
 
   const int rbase = 32 * rb;
-  const int row = it.row0 + min(rbase + lrow, it.n_rows - 1);
-  const int pos = rows[row].pos;
+  // item rows are entries of arows: the computed row (q, out, lse) and
+  // its position
+  const AttnRow ar = arows[it.row0 + min(rbase + lrow, it.n_rows - 1)];
+  const int row = ar.row;
+  const int pos = ar.pos;
   const int pos_l = pos - 4 * lh;   // position less the lane's key offset in a tile
   // key tiles this wave's rows need: up to their largest position
   int my_ntiles = 0;
@@ -540,7 +546,7 @@ __global__ __launch_bounds__(256 * R, 3) void attn_mfma_kernel(
   // and every wave loads its raw queries; the rotation follows the barrier.
   {
     const int t = tid & 255, lr = t >> 3, c8 = 8 * (t & 7);
-    const int ppos = rows[it.row0 + min(rbase + lr, it.n_rows - 1)].pos;
+    const int ppos = arows[it.row0 + min(rbase + lr, it.n_rows - 1)].pos;
     float c[8], sn[8];
     load8(rope_cos + (int64_t)ppos * (kD / 2) + c8, c);
     load8(rope_sin + (int64_t)ppos * (kD / 2) + c8, sn);
@@ -612,11 +618,12 @@ __global__ __launch_bounds__(256 * R, 3) void attn_mfma_kernel(
   const float lt = l + __shfl_xor(l, 32);
   if (!wave_active || rbase + lrow >= it.n_rows) return;
   const float inv = 1.0f / lt;
-  if constexpr (R == 1) {
+  {
     if (it.part_slot >= 0) {
       // one key range of a split item: normalized rows and log-sum-exp in
-      // fp32 to the item's slot, merged by attn_merge_kernel
-      const int64_t sr = ((int64_t)it.part_slot * kTileRows + lrow) * kSplitHeads + w;
+      // fp32 to this row block's slot, merged by attn_merge_kernel
+      const int64_t slot = it.part_slot + (int64_t)rb * it.n_parts;
+      const int64_t sr = (slot * kTileRows + lrow) * kSplitHeads + w;
       float* po = split_o + sr * kD;
 #pragma unroll
       for (int db = 0; db < 4; ++db)
@@ -654,13 +661,14 @@ int ilog2(int x) {
 // whole prompt, run as several ranges): for its row r and query head
 // hq0 + hs, from the ranges' normalized outputs o_c and log-sum-exps lse_c,
 //   lse = log sum_c exp(lse_c),   o = sum_c exp(lse_c - lse) o_c,
-// o rounded to bf16 once.  One workgroup per split item, two threads per
-// (row, head), each over half the head dims.
+// o rounded to bf16 once.  One workgroup per row block of a split item (its
+// rows are AttnRow entries), two threads per (row, head), each over half the
+// head dims.
 template <int D>
 __global__ __launch_bounds__(256) void attn_merge_kernel(
-    const CombineDesc* __restrict__ cds, const float* __restrict__ split_o,
-    const float* __restrict__ split_lse, uint16_t* __restrict__ out,
-    float* __restrict__ lse, int n_q_heads) {
+    const CombineDesc* __restrict__ cds, const AttnRow* __restrict__ arows,
+    const float* __restrict__ split_o, const float* __restrict__ split_lse,
+    uint16_t* __restrict__ out, float* __restrict__ lse, int n_q_heads) {
   const CombineDesc cd = cds[blockIdx.x];
   const int t = threadIdx.x;
   const int half = t & 1, pair = t >> 1;
@@ -690,7 +698,7 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(
       acc[d + 3] = fmaf(wc, v.w, acc[d + 3]);
     }
   }
-  const int64_t orow = (int64_t)(cd.row0 + r) * n_q_heads + cd.hq0 + hs;
+  const int64_t orow = (int64_t)arows[cd.row0 + r].row * n_q_heads + cd.hq0 + hs;
   uint16_t* dst = out + orow * D + half * DH;
 #pragma unroll
   for (int d = 0; d < DH; d += 8) {
@@ -748,7 +756,7 @@ hipError_t launch_attn(const tsr_plan* p, int32_t part, const AttnItem* items,
                      static_cast<const uint16_t*>(pool_k),                         \
                      static_cast<const uint16_t*>(pool_v), items,                  \
                      p->dev.block_tables, p->dev.v_block_tables,                    \
-                     p->dev.k_block_tables, p->dev.rows, p->dev.rope_cos,           \
+                     p->dev.k_block_tables, p->dev.attn_rows, p->dev.rope_cos,      \
                      p->dev.rope_sin, static_cast<uint16_t*>(out), lse,             \
                      p->dev.split_o, p->dev.split_lse, m.n_q_heads, m.n_kv_heads, lp, \
                      p->scale, sl2e)
@@ -774,7 +782,7 @@ hipError_t launch_attn(const tsr_plan* p, int32_t part, const AttnItem* items,
   const int32_t nc = part == TSR_ATTN_ALL ? p->n_combine : p->n_combine_part[part - 1];
   if (nc == 0) return hipSuccess;
   hipLaunchKernelGGL(attn_merge_kernel<kD>, dim3(nc), dim3(256), 0, s, p->dev.combine + c0,
-                     p->dev.split_o, p->dev.split_lse, static_cast<uint16_t*>(out), lse,
+                     p->dev.attn_rows, p->dev.split_o, p->dev.split_lse, static_cast<uint16_t*>(out), lse,
                      m.n_q_heads);
   return hipGetLastError();
 }

@@ -369,6 +369,19 @@ tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
   // K/V tiles (adjacent in the launch order, so the repeat reads hit L2).
   const int G = m.n_q_heads / Hkv;
   const int hsplit = (m.act_dtype == TSR_BF16 && G > 4) ? G / 4 : 1;
+  // Row order of the items: the computed order, or (grouped) each
+  // request's rows stably sorted by first visible key.  Under the LOCAL
+  // scope the rows that see the whole prompt (text, recompute windows) come
+  // in short runs between the unit-local rows of missed units; grouped,
+  // they fill whole row blocks (their positions stay ascending, so an
+  // item's first and last rows still bound its positions).
+  const int32_t T = (int32_t)rows.size();
+  std::vector<int32_t> ord((size_t)T), grouped((size_t)T);
+  std::iota(ord.begin(), ord.end(), 0);
+  std::iota(grouped.begin(), grouped.end(), 0);
+  for (int r = 0; r < n_req; ++r)
+    std::stable_sort(grouped.begin() + req_row0[r], grouped.begin() + req_row0[r + 1],
+                     [&](int32_t a, int32_t b) { return p->row_lo[a] < p->row_lo[b]; });
   struct Item { AttnItem it; int64_t cost; int group; int part; };
   std::vector<Item> items;
   int32_t max_kv = 0;
@@ -376,7 +389,11 @@ tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
   // Builds the items for row blocks of kTileRows rows, rb per item; returns
   // the share of the items' (row block x key tile) slots that hold keys a
   // row block needs (a row block skips the tiles past its last row).
-  auto build_items = [&](int rb) -> double {
+  auto build_items = [&](int rb, bool group_rows = false) -> double {
+    if (group_rows) ord = grouped;
+    else std::iota(ord.begin(), ord.end(), 0);
+    const auto pos_at = [&](int32_t i) { return p->row_pos[ord[i]]; };
+    const auto lo_at = [&](int32_t i) { return p->row_lo[ord[i]]; };
     items.clear();
     max_kv = 0;
     max_blocks = 0;
@@ -386,17 +403,17 @@ tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
       // runs of consecutive rows with the same first visible key
       for (int32_t a0 = req_row0[r]; a0 < req_row0[r + 1];) {
         int32_t a1 = a0 + 1;
-        while (a1 < req_row0[r + 1] && p->row_lo[a1] == p->row_lo[a0]) ++a1;
-        const int32_t kv_lo = p->row_lo[a0];
+        while (a1 < req_row0[r + 1] && lo_at(a1) == lo_at(a0)) ++a1;
+        const int32_t kv_lo = lo_at(a0);
         for (int32_t t0 = a0; t0 < a1; t0 += tile_rows) {
           const int32_t n = std::min(tile_rows, a1 - t0);
-          const int32_t lo = p->row_pos[t0], hi = p->row_pos[t0 + n - 1];
+          const int32_t lo = pos_at(t0), hi = pos_at(t0 + n - 1);
           max_kv = std::max(max_kv, hi + 1);
           const int32_t t_lo = kv_lo / kMfmaKeys;
           max_blocks = std::max<int64_t>(max_blocks, 2 * ((int64_t)hi / kMfmaKeys + 1 - t_lo));
           slots += (int64_t)rb * (hi / kMfmaKeys + 1 - t_lo);
           for (int32_t b0 = 0; b0 < n; b0 += kTileRows)
-            need += p->row_pos[t0 + std::min(n, b0 + kTileRows) - 1] / kMfmaKeys + 1 - t_lo;
+            need += pos_at(t0 + std::min(n, b0 + kTileRows) - 1) / kMfmaKeys + 1 - t_lo;
           // part 1 if a gathered position lies in the key tiles the kernels
           // load for this item (masked keys included): [tile of kv_lo, end
           // of the tile of hi]
@@ -407,7 +424,7 @@ tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
             if (iv.first < khi && iv.second > klo) part = 1;
           for (int g = 0; g < Hkv; ++g)
             for (int hs = 0; hs < hsplit; ++hs) {
-              AttnItem a{t0, n, hi + 1, lo, g, bt_off[r], bt_len[r], 4 * hs, kv_lo, -1, {0, 0}};
+              AttnItem a{t0, n, hi + 1, lo, g, bt_off[r], bt_len[r], 4 * hs, kv_lo, -1, 0, 0};
               items.push_back({a, (int64_t)(hi + 1 - kv_lo), r * Hkv + g, part});
             }
         }
@@ -419,12 +436,17 @@ tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
   // The MFMA kernels (bf16 and e4m3 KV) run kMaxRowBlocks row blocks per
   // workgroup (their K/V staging then serves three times the rows) unless
   // short runs of rows (unit-local attention) would leave too many row
-  // blocks idle; the fp32 kernel takes one row block.
-  // attn_kernel == 1 (bf16 KV only) asks for the pipelined kernel
-  // (attn_pipe.hip, two row blocks per item); it cannot rotate K on load
-  // and its page-id table bounds an item's keys.  Measured on the RAG
-  // batches it is slower than the row-block kernel, which stays the
-  // automatic choice.
+  // blocks idle, or the batch has fewer such items than the GPU has compute
+  // units (one three-row-block workgroup fills a unit; one-row-block
+  // workgroups run three to a unit); the fp32 kernel takes one row block.
+  // The bf16 row-block kernel cuts its three-row-block items from rows
+  // grouped by first visible key (AttnRow order); one-row-block plans keep
+  // the computed order.
+  // attn_kernel (bf16 KV only): 1 the pipelined kernel (attn_pipe.hip, two
+  // row blocks per item; it cannot rotate K on load and its page-id table
+  // bounds an item's keys; measured slower than the row-block kernel on the
+  // RAG batches), 2 the row-block kernel under the rule above (as 0),
+  // 3 / 4 the row-block kernel with three / one row blocks.
   p->row_blocks = 1;
   const bool bf16_kv = m.act_dtype == TSR_BF16 && m.kv_dtype == TSR_BF16;
   auto split_threshold = [&](int64_t total_tiles) -> int64_t {
@@ -432,37 +454,45 @@ tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
                            : std::max<int64_t>(kMinSplitTiles,
                                                (total_tiles + kSplitSlots - 1) / kSplitSlots);
   };
-  bool pipe = false;
+  const bool mfma = m.act_dtype == TSR_BF16 &&
+                    (m.kv_dtype == TSR_BF16 || m.kv_dtype == TSR_E4M3);
   if (bf16_kv && attn_kernel == 1) {
     build_items(kPipeRowBlocks);
     if (alias_k || max_blocks > kPipeMaxBlocks)
       return fail(TSR_ERR_UNSUPPORTED,
                   alias_k ? "the pipelined attention kernel does not rotate K on load"
                           : "an attention item spans more keys than the pipelined kernel takes");
-    pipe = true;
-  }
-  if (pipe) {
     p->row_blocks = kPipeRowBlocks;
-  } else if (m.act_dtype == TSR_BF16 &&
-             (m.kv_dtype == TSR_BF16 || m.kv_dtype == TSR_E4M3) &&
-             build_items(kMaxRowBlocks) >= kMinRowBlockUse) {
+  } else if (bf16_kv && attn_kernel == 3) {
+    build_items(kMaxRowBlocks, true);
+    p->row_blocks = kMaxRowBlocks;
+  } else if (bf16_kv && attn_kernel == 4) {
+    build_items(1);
+  } else if (mfma && build_items(kMaxRowBlocks, bf16_kv) >=
+                         (bf16_kv ? kMinGroupedRowBlockUse : kMinRowBlockUse) &&
+             (!bf16_kv || (int64_t)items.size() >= kNumCus)) {
     p->row_blocks = kMaxRowBlocks;
   } else {
     build_items(1);
   }
-  // Key-range split (bf16 plans with one row block per item): the launch
+  p->rows_grouped = !std::is_sorted(ord.begin(), ord.end());
+  std::vector<AttnRow> attn_rows((size_t)T);
+  for (int32_t i = 0; i < T; ++i) attn_rows[i] = AttnRow{ord[i], p->row_pos[ord[i]]};
+  // Key-range split (bf16 plans of the row-block kernel): the launch
   // lasts as long as its longest item, so an item spanning more than S key
   // tiles runs as up to n = ceil(tiles / S) items over consecutive key
   // ranges.  Every range but the first starts on a tile boundary above
   // kv_lo and at or below the smallest row position, so every row sees at
   // least one key of every range and only the last range needs the causal
-  // mask; each range writes a split buffer slot and the merge kernel
-  // combines the n slots.  Ranges inherit the item's part (a part-0 item's
-  // ranges read no gathered key either).
+  // mask; each range writes one split buffer slot per row block (a row
+  // block's n ranges in consecutive slots) and the merge kernel combines
+  // each row block's n slots.  Ranges inherit the item's part (a part-0
+  // item's ranges read no gathered key either).
   std::vector<CombineDesc> combine[2];
-  int32_t n_slots = 0;
-  if (split_tiles >= 0 && p->row_blocks == 1 && m.act_dtype == TSR_BF16 &&
-      m.kv_dtype == TSR_BF16 && !items.empty()) {
+  int32_t n_slots = 0, n_split_items = 0;
+  const int rb_split = p->row_blocks;
+  if (split_tiles >= 0 && (rb_split == 1 || rb_split == kMaxRowBlocks) &&
+      m.act_dtype == TSR_BF16 && m.kv_dtype == TSR_BF16 && !items.empty()) {
     auto tiles_of = [](const AttnItem& a) -> int64_t {
       return (a.kv_len + kMfmaKeys - 1) / kMfmaKeys - a.kv_lo / kMfmaKeys;
     };
@@ -473,7 +503,7 @@ tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
       int64_t n = 0;
       for (const Item& x : items) {
         const int64_t t = tiles_of(x.it);
-        if (t > lim) n += (t + lim - 1) / lim;
+        if (t > lim) n += rb_split * ((t + lim - 1) / lim);
       }
       return n;
     };
@@ -506,13 +536,20 @@ tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
         y.it.kv_lo = c == 0 ? a.kv_lo : b[c] * kMfmaKeys;
         y.it.kv_len = c == n - 1 ? a.kv_len : b[c + 1] * kMfmaKeys;
         y.it.part_slot = n_slots + (int32_t)c;
+        y.it.n_parts = (int32_t)n;
         y.cost = (int64_t)(b[c + 1] - b[c]) * kMfmaKeys;
         split.push_back(y);
       }
-      combine[x.part].push_back(CombineDesc{a.row0, a.n_rows, a.kv_head * G + a.head0,
-                                            std::min(G, kSplitHeads), n_slots, (int32_t)n,
-                                            {0, 0}});
-      n_slots += (int32_t)n;
+      for (int blk = 0; blk < rb_split; ++blk) {
+        const int32_t nr = std::min(kTileRows, a.n_rows - kTileRows * blk);
+        if (nr > 0)
+          combine[x.part].push_back(CombineDesc{a.row0 + kTileRows * blk, nr,
+                                                a.kv_head * G + a.head0,
+                                                std::min(G, kSplitHeads),
+                                                n_slots + blk * (int32_t)n, (int32_t)n, {0, 0}});
+      }
+      n_slots += rb_split * (int32_t)n;
+      ++n_split_items;
     }
     items.swap(split);
   }
@@ -552,7 +589,7 @@ tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
     for (size_t i = 0; i < per_bin; ++i)
       for (int b = 0; b < kNumXcd; ++b)
         order.push_back(i < bins[b].size() ? bins[b][i]
-                                           : AttnItem{0, 0, 0, 0, 0, 0, 0, 0, 0, -1, {0, 0}});
+                                           : AttnItem{0, 0, 0, 0, 0, 0, 0, 0, 0, -1, 0, 0});
     return order;
   };
   const std::vector<AttnItem> order = schedule(-1);
@@ -569,6 +606,7 @@ tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
   size_t off = 0;
   p->off_gather = off;  off = align_up(off + gather.size() * sizeof(GatherDesc), 256);
   p->off_rows = off;    off = align_up(off + rows.size() * sizeof(RowDesc), 256);
+  p->off_attn_rows = off; off = align_up(off + attn_rows.size() * sizeof(AttnRow), 256);
   p->off_retain = off;  off = align_up(off + retain.size() * sizeof(RetainDesc), 256);
   p->off_items = off;   off = align_up(off + order.size() * sizeof(AttnItem), 256);
   for (int q = 0; q < 2; ++q) {
@@ -585,6 +623,7 @@ tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
   p->n_combine_part[1] = (int32_t)combine[1].size();
   p->n_combine = p->n_combine_part[0] + p->n_combine_part[1];
   p->n_split_slots = n_slots;
+  p->n_split_items = n_split_items;
   p->off_combine = off; off = align_up(off + p->n_combine * sizeof(CombineDesc), 256);
   // the split buffer is written by the kernels, not uploaded
   p->image_bytes = std::max<size_t>(off, 256);
@@ -601,6 +640,7 @@ tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
   };
   put(p->off_gather, gather.data(), gather.size() * sizeof(GatherDesc));
   put(p->off_rows, rows.data(), rows.size() * sizeof(RowDesc));
+  put(p->off_attn_rows, attn_rows.data(), attn_rows.size() * sizeof(AttnRow));
   put(p->off_retain, retain.data(), retain.size() * sizeof(RetainDesc));
   put(p->off_items, order.data(), order.size() * sizeof(AttnItem));
   for (int q = 0; q < 2; ++q)

@@ -15,13 +15,21 @@
 
 namespace tsr {
 
-// Rows of one attention row block: consecutive computed rows of one request.
+// Rows of one attention row block: consecutive rows of one request (in the
+// computed order, or for the three-row-block bf16 kernel in AttnRow order).
 constexpr int kTileRows = 32;
 // Row blocks per bf16 attention item (one workgroup of 4 waves per row
 // block), used when at least kMinRowBlockUse of the item's row-block x key
 // tile slots hold work.
 constexpr int kMaxRowBlocks = 3;
 constexpr double kMinRowBlockUse = 0.8;
+// The bf16 row-block kernel's threshold, over rows grouped by first visible
+// key (AttnRow order).  Measured on the LOCAL-scope RAG and agent batches
+// (slot use 0.70 and 0.78): three row blocks 13 % and 23 % faster than one;
+// at 0.62 (the RAG batch without grouping) the two were level.
+constexpr double kMinGroupedRowBlockUse = 0.6;
+// Compute units of the GPU (MI355X).
+constexpr int kNumCus = 256;
 // Row blocks per item of the pipelined bf16 kernel (attn_pipe.hip), and
 // the most 16-key blocks an item of it may span (their page ids sit in
 // LDS: 65,536 keys).
@@ -49,6 +57,17 @@ constexpr int32_t kSkipV = 1, kSkipK = 2;
 // A computed row: its request slot and prompt position.
 struct alignas(8) RowDesc {
   int32_t dst;
+  int32_t pos;
+};
+
+// A row of the bf16 row-block attention, in item order: its computed row
+// (index of q, out and lse) and prompt position.  Plans of three row blocks
+// order each request's rows by their first visible key (positions still
+// ascending within each group), so that the rows that see the whole prompt
+// (text, recompute windows) form full row blocks even where unit-local
+// rows separate them; other plans keep the computed order.
+struct alignas(8) AttnRow {
+  int32_t row;
   int32_t pos;
 };
 
@@ -85,15 +104,19 @@ struct alignas(16) AttnItem {
   int32_t n_pages;   // entries of that block table
   int32_t head0;     // first query head of the group handled by the item
   int32_t kv_lo;     // first visible key of every row (0 unless unit-local)
-  // -1: the item writes out/lse; else the slot of the split buffer its
-  // normalized rows and log-sum-exp go to (one key range of a split item)
+  // -1: the item writes out/lse; else one key range c of a split item of
+  // n_parts ranges: row block b's normalized rows and log-sum-exp go to
+  // split buffer slot part_slot + b * n_parts (each row block's ranges sit
+  // in consecutive slots)
   int32_t part_slot;
-  int32_t pad[2];
+  int32_t n_parts;
+  int32_t pad;
 };
 
-// A split item: its rows were computed over n_slots consecutive key ranges,
-// slots slot0 .. slot0 + n_slots - 1 of the split buffer; the merge kernel
-// writes rows row0 .. row0 + n_rows - 1 of query heads hq0 .. hq0 + n_heads - 1.
+// A row block of a split item: its rows were computed over n_slots
+// consecutive key ranges, slots slot0 .. slot0 + n_slots - 1 of the split
+// buffer; the merge kernel writes the rows of AttnRow entries row0 ..
+// row0 + n_rows - 1, query heads hq0 .. hq0 + n_heads - 1.
 struct alignas(16) CombineDesc {
   int32_t row0;
   int32_t n_rows;
@@ -121,6 +144,7 @@ constexpr int kMaxSplitSlots = 4096;
 struct PlanDev {
   const GatherDesc* gather;
   const RowDesc* rows;
+  const AttnRow* attn_rows;   // the rows in item order (row-block bf16 kernel)
   const RetainDesc* retain;
   const AttnItem* items;
   const AttnItem* items_part[2];
@@ -158,12 +182,15 @@ struct tsr_plan {
   int32_t n_combine;
   int32_t n_combine_part[2];
   int32_t n_split_slots;
+  int32_t n_split_items;    // items whose key range was split
   size_t off_combine, off_split_o, off_split_lse;
   size_t image_bytes;       // bytes of the image uploaded (the split buffer follows)
   int32_t n_gpages, n_apages, n_rpages;   // e4m3 plans only
   std::vector<int32_t> row_pos, row_req, row_lo;
   std::vector<char> image;  // host copy of the device image
   size_t off_gather, off_rows, off_retain, off_items, off_bt, ws_bytes;
+  size_t off_attn_rows;
+  bool rows_grouped;          // attn_rows groups rows by first visible key
   size_t off_items_part[2];
   size_t off_vbt;
   bool alias_v;               // V of whole gathered pages read from the pool

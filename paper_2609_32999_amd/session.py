@@ -109,7 +109,8 @@ class Session:
         `split_tiles` the key-range split of long attention items (0
         automatic, > 0 the most 32-key tiles an item keeps, -1 never),
         `attn_kernel` the bf16 attention kernel (0 automatic, 1 pipelined,
-        2 row-block)."""
+        2 row-block under its rule, 3 / 4 row-block with three / one row
+        blocks)."""
         batch = B.RequestBatch(requests)
         ws_bytes = B.tsr_plan_workspace_size(self.model, batch, self.n_pool_pages,
                                              self.n_req_pages, alias_v, alias_k, split_tiles,

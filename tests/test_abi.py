@@ -63,14 +63,18 @@ def test_host_plan_matches_oracle_sets(name):
     assert plan.num_attn_items % 8 == 0
 
 
-def _items_per_kv_head(wl, rows_per_item):
+def _items_per_kv_head(wl, rows_per_item, grouped=False):
     """Attention items of each KV head (before launch padding) when runs of
     rows with the same first visible key are cut into items of
     rows_per_item rows, and the share of (32-row block x 32-key tile) slots
-    of those items that hold keys the block's rows need."""
+    of those items that hold keys the block's rows need.  grouped: each
+    request's rows first stably sorted by first visible key."""
     n = need = slots = 0
     for req in wl.requests:
         pos, lo = L.compute_positions(req), L.row_kv_lo(req)
+        if grouped:
+            o = np.argsort(lo, kind="stable")
+            pos, lo = pos[o], lo[o]
         a0 = 0
         while a0 < len(pos):
             a1 = a0 + 1
@@ -90,24 +94,28 @@ def _items_per_kv_head(wl, rows_per_item):
                                         ("agent8b", "local"), ("long70b", "global"),
                                         ("fp8rag", "global"), ("small_f32", "global")])
 def test_attention_row_blocks(name, scope):
-    """Rows per attention item.  bf16 and e4m3 KV: three 32-row blocks
-    unless fewer than 80 % of the items' block x tile slots would hold
-    work, then one; fp32: one."""
+    """Rows per attention item.  bf16 KV: three 32-row blocks over rows
+    grouped by first visible key unless fewer than 60 % of the items' block x
+    tile slots would hold work or there would be fewer than 256 items, then
+    one; e4m3 KV: three over the computed order under an 80 % rule; fp32:
+    one."""
     cfg = workloads.get_config(name)
     if scope != "global":
         cfg = cfg.with_(miss_scope=scope)
     wl = workloads.make_workload(cfg)
     m = wl.model
     n1, _ = _items_per_kv_head(wl, 32)
-    n3, use3 = _items_per_kv_head(wl, 96)
     bf16_act = m.act_dtype == "bf16"
-    if bf16_act and m.kv_dtype in ("bf16", "e4m3") and use3 >= 0.8:
-        rows, n = 96, n3
-    else:
-        rows, n = 32, n1
+    n3, use3 = _items_per_kv_head(wl, 96, grouped=m.kv_dtype == "bf16")
     groups = (m.n_q_heads // m.n_kv_heads) // 4 if bf16_act and \
         m.n_q_heads // m.n_kv_heads > 4 else 1
     per = m.n_kv_heads * groups
+    bar = 0.6 if m.kv_dtype == "bf16" else 0.8
+    enough = m.kv_dtype != "bf16" or n3 * per >= 256
+    if bf16_act and m.kv_dtype in ("bf16", "e4m3") and use3 >= bar and enough:
+        rows, n = 96, n3
+    else:
+        rows, n = 32, n1
     plan = _plan(wl)
     # launch padding only adds items: multi-block items give fewer items than
     # one-block items would need, one row block at least that many
@@ -116,7 +124,8 @@ def test_attention_row_blocks(name, scope):
     else:
         assert plan.num_attn_items >= n1 * per, (plan.num_attn_items, n1, n3, use3)
     assert plan.attn_rows_per_item == rows
-    expect = {("rag8b", "global"): 96, ("long70b", "global"): 96, ("fp8rag", "global"): 96}
+    expect = {("rag8b", "global"): 96, ("long70b", "global"): 96, ("fp8rag", "global"): 96,
+              ("rag8b", "local"): 96, ("agent8b", "local"): 96}
     assert rows == expect.get((name, scope), 32)
 
 
@@ -124,20 +133,24 @@ def test_attention_row_blocks(name, scope):
 def test_attention_kernel_option(name):
     """attn_kernel: 1 asks for the pipelined kernel (64-row items, refused
     where it does not apply: K rotated on load), 2 for the row-block
-    kernel, 0 (automatic) for the row-block kernel, anything else is an
-    invalid argument."""
+    kernel under its rule (as 0), 3 / 4 for it with three / one row blocks,
+    anything else is an invalid argument."""
     wl = workloads.generate(name)
     mk = lambda **kw: P.tsr_plan_create(_model(wl), P.RequestBatch(wl.requests),
                                         wl.n_pool_pages, wl.n_req_pages, **kw)
     assert mk(attn_kernel=1).attn_rows_per_item == 64
     assert mk(attn_kernel=2).attn_rows_per_item in (32, 96)
     assert mk().attn_rows_per_item == mk(attn_kernel=2).attn_rows_per_item
+    assert mk(attn_kernel=3).attn_rows_per_item == 96
+    assert mk(attn_kernel=4).attn_rows_per_item == 32
+    assert mk(attn_kernel=3, alias_k=True).attn_rows_per_item == 96
     with pytest.raises(P.TsrError) as e:
         mk(attn_kernel=1, alias_k=True)
     assert e.value.status == P.TSR_ERR_UNSUPPORTED
-    with pytest.raises(P.TsrError) as e:
-        mk(attn_kernel=3)
-    assert e.value.status == P.TSR_ERR_INVALID_ARG
+    for bad in (-1, 5):
+        with pytest.raises(P.TsrError) as e:
+            mk(attn_kernel=bad)
+        assert e.value.status == P.TSR_ERR_INVALID_ARG
 
 
 def _tiny_req(**over):
@@ -435,15 +448,20 @@ def test_split_ignored_outside_bf16(name):
 
 def test_split_automatic_threshold():
     """Automatic splitting caps items at the launch's mean key tiles per
-    compute unit: the RAG batch under the LOCAL scope (its longest items,
-    the suffix rows, hold 163 tiles against a mean of 288 per unit) is not
-    split; one request of it alone is (its suffix rows then far exceed the
-    mean); under the GLOBAL scope items hold three row blocks and never
-    are."""
+    compute unit.  The RAG batch under the LOCAL scope takes three-row-block
+    items of grouped rows (1,344 items, 31,680 tiles, 124 per unit); its 64
+    longest, the rows that see the whole prompt (up to 163 tiles), are
+    split.  With one row block per item (attn_kernel 4: 3,664 items, a mean
+    of 288 tiles per unit) none is; one request alone is (its suffix rows
+    then far exceed the mean).  Under the GLOBAL scope items hold three row
+    blocks and none exceeds the mean."""
     wl, (local,), _ = _split_plans("rag8b", "local", 0)
-    assert local.attn_rows_per_item == 32 and local.num_attn_splits == 0
-    one = P.tsr_plan_create(_model(wl), P.RequestBatch(wl.requests[:1]), wl.n_pool_pages,
-                            wl.n_req_pages)
+    assert local.attn_rows_per_item == 96 and local.num_attn_splits == 64
+    mk = lambda reqs: P.tsr_plan_create(_model(wl), P.RequestBatch(reqs), wl.n_pool_pages,
+                                        wl.n_req_pages, attn_kernel=4)
+    one_rb = mk(wl.requests)
+    assert one_rb.attn_rows_per_item == 32 and one_rb.num_attn_splits == 0
+    one = mk(wl.requests[:1])
     assert one.attn_rows_per_item == 32 and one.num_attn_splits > 0
     _, (glob,), _ = _split_plans("rag8b", "global", 0)
     assert glob.attn_rows_per_item == 96 and glob.num_attn_splits == 0

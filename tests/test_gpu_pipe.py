@@ -1,10 +1,12 @@
-"""GPU parity of the pipelined bf16 attention kernel (attn_kernel = 1: items
-of two 32-row blocks, eight waves, the next tile's QK^T under this tile's
-softmax) against the oracle, on every request and query head: GQA groups of
+"""GPU parity of each bf16 attention kernel shape against the oracle, on
+every request and query head: the pipelined kernel (attn_kernel 1: items of
+two 32-row blocks, eight waves, the next tile's QK^T under this tile's
+softmax) and the row-block kernel with three row blocks over rows grouped
+by first visible key (3) and with one row block (4).  Cases: GQA groups of
 1, 2, 4 and 8, pages of 32 keys, the LOCAL scope (a first visible key inside
-a tile), rows past an item's last, no recompute window or no text, all hits,
-all misses, duplicate units and V aliasing.  The row-block kernel
-(attn_kernel = 2) runs the same cases as a second witness."""
+a tile; grouped rows out of computed order), rows past an item's last, no
+recompute window or no text, all hits, all misses, duplicate units and V
+aliasing."""
 import numpy as np
 import pytest
 import torch
@@ -61,13 +63,12 @@ CASES = ["small_bf16", "g1", "g2", "g8", "page32", "local", "local_g8", "all_hit
          "all_miss", "dup_units", "long_rows"]
 
 
-@pytest.mark.parametrize("kernel", [1, 2])
+@pytest.mark.parametrize("kernel", [1, 3, 4])
 @pytest.mark.parametrize("name", CASES)
 def test_attention_kernel_against_oracle(name, kernel):
     wl = workloads.make_workload(_case(name))
     run = GpuRun(wl, attn_kernel=kernel)
-    if kernel == 1:
-        assert run.plan.attn_rows_per_item == 64
+    assert run.plan.attn_rows_per_item == {1: 64, 3: 96, 4: 32}[kernel]
     assert run.pool_after_compose_ok and run.pool_after_attn_ok, "pool modified"
     for r in range(len(wl.requests)):
         check_request(run, r)

@@ -26,8 +26,9 @@ def _local(name, **model_kw):
     return workloads.make_workload(cfg)
 
 
-def _check_all(run):
-    assert run.plan.num_attn_splits > 0, "no item was split"
+def _check_all(run, expect_split=True):
+    if expect_split:
+        assert run.plan.num_attn_splits > 0, "no item was split"
     assert run.pool_after_compose_ok and run.pool_after_attn_ok, "pool modified"
     for r in range(len(run.wl.requests)):
         check_request(run, r)
@@ -35,13 +36,21 @@ def _check_all(run):
     check_retained(run)
 
 
+@pytest.mark.parametrize("kernel", [4, 3])
 @pytest.mark.parametrize("name,split", [("small_bf16", 1), ("small_bf16", 2),
                                         ("small_bf16", 5), ("small_bf16_g8", 2)])
-def test_split_local_matches_oracle(name, split):
+def test_split_local_matches_oracle(name, split, kernel):
     """Every row of every request against the oracle with items split every
     `split` key tiles (one-tile ranges included; the first range holds the
-    unit's first key off the tile grid, the last the causal diagonal)."""
-    _check_all(GpuRun(_local(name), split_tiles=split))
+    unit's first key off the tile grid, the last the causal diagonal), for
+    items of one row block (attn_kernel 4) and of three row blocks over rows
+    grouped by first visible key (3: a slot per row block and range)."""
+    run = GpuRun(_local(name), split_tiles=split, attn_kernel=kernel)
+    assert run.plan.attn_rows_per_item == (96 if kernel == 3 else 32)
+    # range boundaries stay at or below an item's smallest position: the
+    # small batch's grouped three-block items reach at most 4 tiles past it,
+    # so 5-tile ranges split none of them
+    _check_all(run, expect_split=not (kernel == 3 and split == 5))
 
 
 @pytest.mark.parametrize("G", [1, 2])
@@ -58,16 +67,17 @@ def _attn(sess, plan, q, part=P.TSR_ATTN_ALL, out=None, lse=None):
     return out, lse
 
 
-def test_split_against_unsplit_and_parts():
+@pytest.mark.parametrize("kernel", [4, 3])
+def test_split_against_unsplit_and_parts(kernel):
     """The same batch planned without splitting and with two-tile ranges:
     outputs agree to bf16 rounding and lse to fp32 rounding (the merge sums
     the ranges in fp32); the two attention parts together reproduce the
     split plan's full launch bit for bit."""
     wl = _local("small_bf16")
-    run = GpuRun(wl, split_tiles=-1)
+    run = GpuRun(wl, split_tiles=-1, attn_kernel=kernel)
     s = run.sess
     assert run.plan.num_attn_splits == 0
-    plan = s.plan(wl.requests, split_tiles=2)
+    plan = s.plan(wl.requests, split_tiles=2, attn_kernel=kernel)
     assert plan.num_attn_splits > 0
     out1, lse1 = _attn(s, plan, run.q)
     torch.cuda.synchronize()
@@ -98,3 +108,18 @@ def test_split_automatic_single_request_local():
     assert run.plan.attn_rows_per_item == 32 and run.plan.num_attn_splits > 0
     check_request(run, 0)
     check_request_sentinels(run, 0)
+
+
+@pytest.mark.slow
+def test_grouped_split_full_local_batch():
+    """The full RAG batch under the LOCAL scope with the automatic choices:
+    three-row-block items over rows grouped by first visible key, the
+    longest split by key range.  The first and last requests against the
+    oracle on every KV head."""
+    wl = _local("rag8b")
+    run = GpuRun(wl)
+    assert run.plan.attn_rows_per_item == 96 and run.plan.num_attn_splits > 0
+    assert run.pool_after_compose_ok and run.pool_after_attn_ok, "pool modified"
+    for r in (0, len(wl.requests) - 1):
+        check_request(run, r)
+        check_request_sentinels(run, r)
