@@ -560,9 +560,10 @@ def main():
                          "rotated on load, both)")
     ap.add_argument("--no-host-tier", dest="host_tier", action="store_false",
                     help="skip timing compose and retain against a pool in pinned host memory")
-    ap.add_argument("--attn-kernel", type=int, default=0, choices=[0, 1, 2],
+    ap.add_argument("--attn-kernel", type=int, default=0, choices=[0, 1, 2, 3, 4],
                     help="bf16 attention kernel of the main plan: 0 automatic, 1 the "
-                         "pipelined kernel, 2 the row-block kernel")
+                         "pipelined kernel, 2 the row-block kernel under its rule, "
+                         "3 / 4 the row-block kernel with three / one row blocks")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="run one launch of libtsr's plain copy kernel of this size "
                          "first (to scale HBM byte counters against a kernel of known "

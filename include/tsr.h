@@ -221,8 +221,8 @@ tsr_status tsr_plan_create(const tsr_model* model, const tsr_request* reqs,
  *             With alias_v too, such pages are not touched by compose at
  *             all.  The pool pages must stay unchanged until attention
  *             completes.  bf16 pools only (else UNSUPPORTED).
- *   split_tiles  key-range splitting of long attention items (bf16 plans
- *             whose items hold one 32-row block; other plans ignore it).
+ *   split_tiles  key-range splitting of long attention items (plans of
+ *             the bf16 row-block kernel; other plans ignore it).
  *             An item whose keys span more than S tiles of 32 keys runs as
  *             ceil(tiles / S) items over consecutive key ranges, each
  *             writing its rows' normalized output and log-sum-exp in fp32
@@ -232,10 +232,11 @@ tsr_status tsr_plan_create(const tsr_model* model, const tsr_request* reqs,
  *             launch lasts at least as long as its longest item: under
  *             TSR_SCOPE_LOCAL the rows after the units attend to the whole
  *             prompt while most rows attend within a short unit.
- *               0   automatic: S = the launch's mean key tiles per compute
- *                   unit (256 units, 32 tiles at least), so only items
- *                   that would outlast the rest of the launch are split;
- *                   never for tsr_plan_create_static;
+ *               0   automatic: for items of one row block, S = the
+ *                   launch's mean key tiles per compute unit (256 units,
+ *                   32 tiles at least), so only items that would outlast
+ *                   the rest of the launch are split; items of three row
+ *                   blocks are not split; never for tsr_plan_create_static;
  *               >0  S = split_tiles;
  *               -1  never split.
  *             A plan with split items writes that buffer on every

@@ -490,8 +490,14 @@ tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
   // item's ranges read no gathered key either).
   std::vector<CombineDesc> combine[2];
   int32_t n_slots = 0, n_split_items = 0;
+  // The automatic threshold (split_tiles == 0) applies to one-row-block
+  // plans only: on the LOCAL-scope RAG batch at three row blocks it split 64
+  // items and the launch plus merge took 4 % longer (one workgroup per
+  // compute unit there, so an item's tail is shared by fewer waiting
+  // items); split_tiles > 0 splits either.
   const int rb_split = p->row_blocks;
-  if (split_tiles >= 0 && (rb_split == 1 || rb_split == kMaxRowBlocks) &&
+  if ((split_tiles > 0 || (split_tiles == 0 && rb_split == 1)) &&
+      (rb_split == 1 || rb_split == kMaxRowBlocks) &&
       m.act_dtype == TSR_BF16 && m.kv_dtype == TSR_BF16 && !items.empty()) {
     auto tiles_of = [](const AttnItem& a) -> int64_t {
       return (a.kv_len + kMfmaKeys - 1) / kMfmaKeys - a.kv_lo / kMfmaKeys;

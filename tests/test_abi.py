@@ -447,16 +447,18 @@ def test_split_ignored_outside_bf16(name):
 
 
 def test_split_automatic_threshold():
-    """Automatic splitting caps items at the launch's mean key tiles per
-    compute unit.  The RAG batch under the LOCAL scope takes three-row-block
-    items of grouped rows (1,344 items, 31,680 tiles, 124 per unit); its 64
-    longest, the rows that see the whole prompt (up to 163 tiles), are
-    split.  With one row block per item (attn_kernel 4: 3,664 items, a mean
-    of 288 tiles per unit) none is; one request alone is (its suffix rows
-    then far exceed the mean).  Under the GLOBAL scope items hold three row
-    blocks and none exceeds the mean."""
-    wl, (local,), _ = _split_plans("rag8b", "local", 0)
-    assert local.attn_rows_per_item == 96 and local.num_attn_splits == 64
+    """Automatic splitting caps one-row-block items at the launch's mean key
+    tiles per compute unit.  With one row block per item (attn_kernel 4:
+    3,664 items, a mean of 288 tiles per unit) the RAG batch under the
+    LOCAL scope splits none; one request alone splits (its suffix rows then
+    far exceed the mean).  Three-row-block plans are not split
+    automatically: the RAG LOCAL batch's grouped items (1,344 items, 31,680
+    tiles, 124 per unit) hold 64 longer than the mean, and splitting them
+    measured slower; an explicit threshold still splits them.  Under the
+    GLOBAL scope none exceeds the mean either way."""
+    wl, (local, forced), _ = _split_plans("rag8b", "local", 0, 124)
+    assert local.attn_rows_per_item == 96 and local.num_attn_splits == 0
+    assert forced.attn_rows_per_item == 96 and forced.num_attn_splits == 64
     mk = lambda reqs: P.tsr_plan_create(_model(wl), P.RequestBatch(reqs), wl.n_pool_pages,
                                         wl.n_req_pages, attn_kernel=4)
     one_rb = mk(wl.requests)

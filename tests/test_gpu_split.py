@@ -112,12 +112,13 @@ def test_split_automatic_single_request_local():
 
 @pytest.mark.slow
 def test_grouped_split_full_local_batch():
-    """The full RAG batch under the LOCAL scope with the automatic choices:
-    three-row-block items over rows grouped by first visible key, the
-    longest split by key range.  The first and last requests against the
-    oracle on every KV head."""
+    """The full RAG batch under the LOCAL scope: three-row-block items over
+    rows grouped by first visible key (the automatic choice), the longest
+    split by key range at 124 tiles (the launch's mean per compute unit; the
+    automatic threshold leaves three-row-block items whole).  The first and
+    last requests against the oracle on every KV head."""
     wl = _local("rag8b")
-    run = GpuRun(wl)
+    run = GpuRun(wl, split_tiles=124)
     assert run.plan.attn_rows_per_item == 96 and run.plan.num_attn_splits > 0
     assert run.pool_after_compose_ok and run.pool_after_attn_ok, "pool modified"
     for r in (0, len(wl.requests) - 1):
