@@ -48,6 +48,7 @@ constexpr int kVStr = kKT + 8;         // fp16 elements per V^T row in LDS
 constexpr int kKBytes = kKT * kKStr;
 constexpr int kVElems = kD * kVStr;
 constexpr float kLazy = 8.0f;          // lazy-rescale threshold (log2 units)
+constexpr float kLazySum = 256.0f;     // 2^kLazy
 
 __device__ __forceinline__ int page_scale_exp(float amax) {
   if (!(amax > 0.0f)) return 0;
@@ -272,16 +273,30 @@ __global__ __launch_bounds__(256 * R, 3) void attn_fp8_kernel(
               a, qf[i][kst], s[i][kb], 0, 0, 0, 127, 0, 127);
       }
     }
-    // page of S register r: r/8 within the tile; its
-    // factor f (Q scale x K page scale x softmax scale x log2 e) is > 0, so
-    // each page's row max is f times the max of its raw scores, and P =
-    // exp2(f s - m) is one fma and one exp2 per score
-    f16x8 pf[HPW][2];
+    // page of S register r: r/8 within the tile; its factor f (Q scale x K
+    // page scale x softmax scale x log2 e) is > 0, so P = exp2(f s - m) is
+    // one fma and one exp2 per score and each page's row max is f times the
+    // max of its raw scores.
+    // Lazy rescale on the tile's probability sum (as in attn.hip): P is
+    // taken against the running max m; while a lane's sum stays <= 2^kLazy
+    // (every P is then exact-range for fp16) no max is taken.  Otherwise
+    // (or while m is still -inf) the scores are computed again from the
+    // tile in LDS, m moves to the row max, O and l are rescaled and P is
+    // recomputed.
+    auto scores = [&](int i) __attribute__((always_inline)) {
 #pragma unroll
-    for (int i = 0; i < HPW; ++i) {
-      float f[2];
+      for (int r = 0; r < 16; ++r) s[i][0][r] = 0.0f;
 #pragma unroll
-      for (int b = 0; b < 2; ++b) f[b] = qs[i] * kscl[j & 1][b] * scale_log2e;
+      for (int kst = 0; kst < 2; ++kst) {
+        const uint8_t* kp = ks + lrow * kKStr + 64 * kst + 32 * lh;
+        union { uint4 u[2]; i32x8 v; } x;
+        x.u[0] = *reinterpret_cast<const uint4*>(kp);
+        x.u[1] = *reinterpret_cast<const uint4*>(kp + 16);
+        s[i][0] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
+            x.v, qf[i][kst], s[i][0], 0, 0, 0, 127, 0, 127);
+      }
+    };
+    auto mask = [&](int i) __attribute__((always_inline)) {
       if constexpr (MASK != 0) {
         // score r holds key j kKT + 8 (r / 4) + 4 lh + r % 4: compare its
         // in-tile offset with the row's bounds moved to the same origin
@@ -294,29 +309,14 @@ __global__ __launch_bounds__(256 * R, 3) void attn_fp8_kernel(
           s[i][0][r] = out ? -INFINITY : s[i][0][r];
         }
       }
-      float mb[2];
+    };
+    f16x8 pf[HPW][2];
 #pragma unroll
-      for (int b = 0; b < 2; ++b) {
-        const int r0 = 8 * b;
-        float x = s[i][0][r0];
+    for (int i = 0; i < HPW; ++i) {
+      float f[2];
 #pragma unroll
-        for (int r = 1; r < 8; ++r) x = fmaxf(x, s[i][0][r0 + r]);
-        mb[b] = x * f[b];
-      }
-      // each half-wave holds half of every row's keys: the halves exchange
-      // their maxima only on the rare rescale path (scores are in log2 units
-      // here; see attn.hip for the lazy rescale)
-      const float mt = fmaxf(mb[0], mb[1]);
-      if (__builtin_amdgcn_ballot_w64(mt > m[i] + kLazy)) {
-        const float mn = fmaxf(m[i], fmaxf(mt, __shfl_xor(mt, 32)));
-        const float alpha = __builtin_amdgcn_exp2f(m[i] - mn);
-        m[i] = mn;
-        l[i] *= alpha;
-#pragma unroll
-        for (int db = 0; db < 4; ++db)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) o[i][db][r] *= alpha;
-      }
+      for (int b = 0; b < 2; ++b) f[b] = qs[i] * kscl[j & 1][b] * scale_log2e;
+      mask(i);
       // row sum in fp32 as four independent chains of plain adds; a row with
       // no visible key yet keeps m at -inf and is exponentiated against 0
       const float mi = m[i] == -INFINITY ? 0.0f : m[i];
@@ -326,6 +326,37 @@ __global__ __launch_bounds__(256 * R, 3) void attn_fp8_kernel(
         const float p = __builtin_amdgcn_exp2f(fmaf(s[i][0][r], f[r >> 3], -mi));
         s[i][0][r] = p;
         ls[r & 3] += p;
+      }
+      const float lt = (ls[0] + ls[1]) + (ls[2] + ls[3]);
+      if (__builtin_amdgcn_ballot_w64(!(lt <= kLazySum) || m[i] == -INFINITY)) {
+        scores(i);
+        mask(i);
+        float mb[2];
+#pragma unroll
+        for (int b = 0; b < 2; ++b) {
+          float x = s[i][0][8 * b];
+#pragma unroll
+          for (int r = 1; r < 8; ++r) x = fmaxf(x, s[i][0][8 * b + r]);
+          mb[b] = x * f[b];
+        }
+        const float mt = fmaxf(mb[0], mb[1]);
+        const float mn = fmaxf(m[i], fmaxf(mt, __shfl_xor(mt, 32)));
+        const float alpha = mn == -INFINITY ? 1.0f : __builtin_amdgcn_exp2f(m[i] - mn);
+        m[i] = mn;
+        l[i] *= alpha;
+#pragma unroll
+        for (int db = 0; db < 4; ++db)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) o[i][db][r] *= alpha;
+        const float mi2 = m[i] == -INFINITY ? 0.0f : m[i];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) ls[r] = 0.0f;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const float p = __builtin_amdgcn_exp2f(fmaf(s[i][0][r], f[r >> 3], -mi2));
+          s[i][0][r] = p;
+          ls[r & 3] += p;
+        }
       }
       l[i] += (ls[0] + ls[1]) + (ls[2] + ls[3]);
 #pragma unroll
