@@ -243,7 +243,8 @@ tsr_status tsr_plan_create(const tsr_model* model, const tsr_request* reqs,
  *             attention call: calls that use one plan on streams that
  *             run concurrently race there.
  *   attn_kernel  which bf16 attention kernel the plan schedules for
- *             (plans with bf16 activations and bf16 KV; others ignore it):
+ *             (plans with bf16 activations and bf16 KV; with e4m3 KV only
+ *             3 and 4 apply, as noted below; other plans ignore it):
  *               0   automatic: the row-block kernel's rule (2), the faster
  *                   choice on every batch measured;
  *               1   the pipelined kernel: items of up to two 32-row blocks,
@@ -257,7 +258,10 @@ tsr_status tsr_plan_create(const tsr_model* model, const tsr_request* reqs,
  *                   slots hold work and there are at least 256 of them
  *                   (one per compute unit); else of one row block;
  *               3   the row-block kernel, three row blocks;
- *               4   the row-block kernel, one row block.
+ *               4   the row-block kernel, one row block;
+ *             3 and 4 also fix the row blocks of the e4m3 kernel (plans
+ *             with bf16 activations and e4m3 KV), which otherwise follows
+ *             the rule of 2.
  *             The row-block kernel is the only one for alias_k plans and
  *             for the key-range split.
  *   reserved  must be zero. */

@@ -66,7 +66,7 @@ __global__ __launch_bounds__(256 * R, 3) void attn_fp8_kernel(
     const uint16_t* __restrict__ q, const uint8_t* __restrict__ kc,
     const uint8_t* __restrict__ vc, const float* __restrict__ scales,
     const AttnItem* __restrict__ items, const int32_t* __restrict__ bts,
-    const RowDesc* __restrict__ rows, const float* __restrict__ rope_cos,
+    const AttnRow* __restrict__ arows, const float* __restrict__ rope_cos,
     const float* __restrict__ rope_sin, uint16_t* __restrict__ out,
     float* __restrict__ lse, int n_q_heads, int n_kv_heads, int log2_page,
     float scale_log2e) {
@@ -94,11 +94,15 @@ __global__ __launch_bounds__(256 * R, 3) void attn_fp8_kernel(
   const int page_mask = (1 << log2_page) - 1;
   const int32_t* bt = bts + it.bt_off;
   const int rbase = 32 * rb;
-  const int row = it.row0 + min(rbase + lrow, it.n_rows - 1);
-  const int pos = rows[row].pos;
+  // item rows are entries of arows: the computed row (q, out, lse) and
+  // its position (with three row blocks, each request's rows grouped by
+  // first visible key)
+  const AttnRow ar = arows[it.row0 + min(rbase + lrow, it.n_rows - 1)];
+  const int row = ar.row;
+  const int pos = ar.pos;
   {
     const int t = tid & 255, lr = t >> 3, c8 = 8 * (t & 7);
-    const int ppos = rows[it.row0 + min(rbase + lr, it.n_rows - 1)].pos;
+    const int ppos = arows[it.row0 + min(rbase + lr, it.n_rows - 1)].pos;
     float c[8], sn[8];
     load8(rope_cos + (int64_t)ppos * (kD / 2) + c8, c);
     load8(rope_sin + (int64_t)ppos * (kD / 2) + c8, sn);
@@ -472,7 +476,7 @@ hipError_t launch_attn_e4m3(const tsr_plan* p, const AttnItem* items, int32_t n_
   hipLaunchKernelGGL((attn_fp8_kernel<GG, RB>), dim3(n_items), dim3(256 * (RB)), 0, s, \
                      static_cast<const uint16_t*>(q), static_cast<const uint8_t*>(req_k), \
                      static_cast<const uint8_t*>(req_v), req_scale, items,            \
-                     p->dev.block_tables, p->dev.rows, p->dev.rope_cos,               \
+                     p->dev.block_tables, p->dev.attn_rows, p->dev.rope_cos,          \
                      p->dev.rope_sin, static_cast<uint16_t*>(out), lse, m.n_q_heads,  \
                      m.n_kv_heads, lp, sl2e)
   switch (G) {

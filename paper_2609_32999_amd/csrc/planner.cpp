@@ -439,14 +439,15 @@ tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
   // blocks idle, or the batch has fewer such items than the GPU has compute
   // units (one three-row-block workgroup fills a unit; one-row-block
   // workgroups run three to a unit); the fp32 kernel takes one row block.
-  // The bf16 row-block kernel cuts its three-row-block items from rows
-  // grouped by first visible key (AttnRow order); one-row-block plans keep
-  // the computed order.
-  // attn_kernel (bf16 KV only): 1 the pipelined kernel (attn_pipe.hip, two
+  // Both kernels cut their three-row-block items from rows grouped by first
+  // visible key (AttnRow order); one-row-block plans keep the computed
+  // order.
+  // attn_kernel (1 and 2 for bf16 KV only): 1 the pipelined kernel (attn_pipe.hip, two
   // row blocks per item; it cannot rotate K on load and its page-id table
   // bounds an item's keys; measured slower than the row-block kernel on the
   // RAG batches), 2 the row-block kernel under the rule above (as 0),
-  // 3 / 4 the row-block kernel with three / one row blocks.
+  // 3 / 4 the row-block kernel (or the e4m3 kernel) with three / one row
+  // blocks.
   p->row_blocks = 1;
   const bool bf16_kv = m.act_dtype == TSR_BF16 && m.kv_dtype == TSR_BF16;
   auto split_threshold = [&](int64_t total_tiles) -> int64_t {
@@ -463,14 +464,13 @@ tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
                   alias_k ? "the pipelined attention kernel does not rotate K on load"
                           : "an attention item spans more keys than the pipelined kernel takes");
     p->row_blocks = kPipeRowBlocks;
-  } else if (bf16_kv && attn_kernel == 3) {
+  } else if (mfma && attn_kernel == 3) {
     build_items(kMaxRowBlocks, true);
     p->row_blocks = kMaxRowBlocks;
-  } else if (bf16_kv && attn_kernel == 4) {
+  } else if (mfma && attn_kernel == 4) {
     build_items(1);
-  } else if (mfma && build_items(kMaxRowBlocks, bf16_kv) >=
-                         (bf16_kv ? kMinGroupedRowBlockUse : kMinRowBlockUse) &&
-             (!bf16_kv || (int64_t)items.size() >= kNumCus)) {
+  } else if (mfma && build_items(kMaxRowBlocks, true) >= kMinGroupedRowBlockUse &&
+             (int64_t)items.size() >= kNumCus) {
     p->row_blocks = kMaxRowBlocks;
   } else {
     build_items(1);

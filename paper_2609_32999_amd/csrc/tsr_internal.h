@@ -18,15 +18,14 @@ namespace tsr {
 // Rows of one attention row block: consecutive rows of one request (in the
 // computed order, or for the three-row-block bf16 kernel in AttnRow order).
 constexpr int kTileRows = 32;
-// Row blocks per bf16 attention item (one workgroup of 4 waves per row
-// block), used when at least kMinRowBlockUse of the item's row-block x key
-// tile slots hold work.
+// Row blocks per attention item of the MFMA kernels (bf16 and e4m3 KV; one
+// workgroup of 4 waves per row block), used when at least
+// kMinGroupedRowBlockUse of the items' row-block x key tile slots hold work,
+// over rows grouped by first visible key (AttnRow order).  Measured on the
+// LOCAL-scope RAG and agent batches (slot use 0.70 and 0.78): three row
+// blocks 13 % and 23 % faster than one; at 0.62 (the RAG batch without
+// grouping) the two were level.
 constexpr int kMaxRowBlocks = 3;
-constexpr double kMinRowBlockUse = 0.8;
-// The bf16 row-block kernel's threshold, over rows grouped by first visible
-// key (AttnRow order).  Measured on the LOCAL-scope RAG and agent batches
-// (slot use 0.70 and 0.78): three row blocks 13 % and 23 % faster than one;
-// at 0.62 (the RAG batch without grouping) the two were level.
 constexpr double kMinGroupedRowBlockUse = 0.6;
 // Compute units of the GPU (MI355X).
 constexpr int kNumCus = 256;

@@ -94,11 +94,10 @@ def _items_per_kv_head(wl, rows_per_item, grouped=False):
                                         ("agent8b", "local"), ("long70b", "global"),
                                         ("fp8rag", "global"), ("small_f32", "global")])
 def test_attention_row_blocks(name, scope):
-    """Rows per attention item.  bf16 KV: three 32-row blocks over rows
-    grouped by first visible key unless fewer than 60 % of the items' block x
-    tile slots would hold work or there would be fewer than 256 items, then
-    one; e4m3 KV: three over the computed order under an 80 % rule; fp32:
-    one."""
+    """Rows per attention item.  bf16 and e4m3 KV: three 32-row blocks over
+    rows grouped by first visible key unless fewer than 60 % of the items'
+    block x tile slots would hold work or there would be fewer than 256
+    items, then one; fp32: one."""
     cfg = workloads.get_config(name)
     if scope != "global":
         cfg = cfg.with_(miss_scope=scope)
@@ -106,13 +105,11 @@ def test_attention_row_blocks(name, scope):
     m = wl.model
     n1, _ = _items_per_kv_head(wl, 32)
     bf16_act = m.act_dtype == "bf16"
-    n3, use3 = _items_per_kv_head(wl, 96, grouped=m.kv_dtype == "bf16")
+    n3, use3 = _items_per_kv_head(wl, 96, grouped=True)
     groups = (m.n_q_heads // m.n_kv_heads) // 4 if bf16_act and \
         m.n_q_heads // m.n_kv_heads > 4 else 1
     per = m.n_kv_heads * groups
-    bar = 0.6 if m.kv_dtype == "bf16" else 0.8
-    enough = m.kv_dtype != "bf16" or n3 * per >= 256
-    if bf16_act and m.kv_dtype in ("bf16", "e4m3") and use3 >= bar and enough:
+    if bf16_act and m.kv_dtype in ("bf16", "e4m3") and use3 >= 0.6 and n3 * per >= 256:
         rows, n = 96, n3
     else:
         rows, n = 32, n1

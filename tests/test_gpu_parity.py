@@ -248,7 +248,21 @@ def test_local_miss_scope_small_groups(G):
 
 
 @pytest.mark.slow
-@pytest.mark.parametrize("name", ["rag8b", "agent8b"])
+@pytest.mark.parametrize("kernel", [3, 4])
+@pytest.mark.parametrize("name", ["small_fp8", "small_bf16"])
+def test_local_row_block_shapes(name, kernel):
+    """Under the LOCAL scope, items of three row blocks cut from rows grouped
+    by first visible key (attn_kernel 3: out of computed order) and of one
+    row block (4), for bf16 and e4m3 KV, on every request and head."""
+    wl = workloads.make_workload(workloads.get_config(name).with_(miss_scope="local"))
+    run = GpuRun(wl, attn_kernel=kernel)
+    assert run.plan.attn_rows_per_item == (96 if kernel == 3 else 32)
+    for r in range(len(wl.requests)):
+        check_request(run, r)
+    check_retained(run)
+
+
+@pytest.mark.parametrize("name", ["rag8b", "agent8b", "fp8rag"])
 def test_local_miss_scope_large(name):
     """Full-size batches under the LOCAL scope; attention checked on one
     sampled KV head of sampled requests."""
