@@ -218,10 +218,18 @@ __global__ __launch_bounds__(256 * R, 3) void attn_mfma_kernel(
 
   const int rbase = 32 * rb;
   // item rows are entries of arows: the computed row (q, out, lse) and
-  // its position
-  const AttnRow ar = arows[it.row0 + min(rbase + lrow, it.n_rows - 1)];
-  const int row = ar.row;
-  const int pos = ar.pos;
+  // its position; items of consecutive computed rows at consecutive
+  // positions carry their first row (crow0) and skip that read
+  const int rr = min(rbase + lrow, it.n_rows - 1);
+  int row, pos;
+  if (it.crow0 >= 0) {
+    row = it.crow0 + rr;
+    pos = it.min_pos + rr;
+  } else {
+    const AttnRow ar = arows[it.row0 + rr];
+    row = ar.row;
+    pos = ar.pos;
+  }
   const int pos_l = pos - 4 * lh;   // position less the lane's key offset in a tile
   // key tiles this wave's rows need: up to their largest position
   int my_ntiles = 0;
@@ -503,7 +511,9 @@ __global__ __launch_bounds__(256 * R, 3) void attn_mfma_kernel(
   const int j0 = it.kv_lo / kKT;
   const int jlo = min(ntiles, (it.kv_lo + kKT - 1) / kKT);   // first tile without keys < kv_lo
   const int nfull = min(ntiles, (it.min_pos + 1) / kKT);      // tiles ending at or before min_pos
-  int pid = fetch_pages(j0);   // ids of the next tile to load (staging waves)
+  // ids of the next tile to load (staging waves; the first tile's come
+  // with the item)
+  int pid = (lane & 1) ? it.pg[1] : it.pg[0];
   // One tile j: issue the next tile's loads into the other buffers, compute
   // this one, stage the next V^T, wait for this wave's direct K loads, then
   // the workgroup barrier.
@@ -546,7 +556,8 @@ __global__ __launch_bounds__(256 * R, 3) void attn_mfma_kernel(
   // and every wave loads its raw queries; the rotation follows the barrier.
   {
     const int t = tid & 255, lr = t >> 3, c8 = 8 * (t & 7);
-    const int ppos = arows[it.row0 + min(rbase + lr, it.n_rows - 1)].pos;
+    const int pr = min(rbase + lr, it.n_rows - 1);
+    const int ppos = it.crow0 >= 0 ? it.min_pos + pr : arows[it.row0 + pr].pos;
     float c[8], sn[8];
     load8(rope_cos + (int64_t)ppos * (kD / 2) + c8, c);
     load8(rope_sin + (int64_t)ppos * (kD / 2) + c8, sn);

@@ -408,6 +408,9 @@ tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
         for (int32_t t0 = a0; t0 < a1; t0 += tile_rows) {
           const int32_t n = std::min(tile_rows, a1 - t0);
           const int32_t lo = pos_at(t0), hi = pos_at(t0 + n - 1);
+          int32_t crow0 = ord[t0];
+          for (int32_t i = 1; i < n && crow0 >= 0; ++i)
+            if (ord[t0 + i] != ord[t0] + i || pos_at(t0 + i) != lo + i) crow0 = -1;
           max_kv = std::max(max_kv, hi + 1);
           const int32_t t_lo = kv_lo / kMfmaKeys;
           max_blocks = std::max<int64_t>(max_blocks, 2 * ((int64_t)hi / kMfmaKeys + 1 - t_lo));
@@ -424,7 +427,8 @@ tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
             if (iv.first < khi && iv.second > klo) part = 1;
           for (int g = 0; g < Hkv; ++g)
             for (int hs = 0; hs < hsplit; ++hs) {
-              AttnItem a{t0, n, hi + 1, lo, g, bt_off[r], bt_len[r], 4 * hs, kv_lo, -1, 0, 0};
+              AttnItem a{t0, n, hi + 1, lo, g, bt_off[r], bt_len[r], 4 * hs, kv_lo, -1, 0,
+                         crow0, {0, 0}, {0, 0, 0}};
               items.push_back({a, (int64_t)(hi + 1 - kv_lo), r * Hkv + g, part});
             }
         }
@@ -595,11 +599,23 @@ tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
     for (size_t i = 0; i < per_bin; ++i)
       for (int b = 0; b < kNumXcd; ++b)
         order.push_back(i < bins[b].size() ? bins[b][i]
-                                           : AttnItem{0, 0, 0, 0, 0, 0, 0, 0, 0, -1, 0, 0});
+                                           : AttnItem{0, 0, 0, 0, 0, 0, 0, 0, 0, -1, 0, -1,
+                                                      {0, 0}, {0, 0, 0}});
     return order;
   };
-  const std::vector<AttnItem> order = schedule(-1);
-  const std::vector<AttnItem> order_part[2] = {schedule(0), schedule(1)};
+  std::vector<AttnItem> order = schedule(-1);
+  std::vector<AttnItem> order_part[2] = {schedule(0), schedule(1)};
+  // first key tile's page ids, from the block table the kernels read for K
+  {
+    const std::vector<int32_t>& kt = alias_k ? kbts : bts;
+    for (std::vector<AttnItem>* list : {&order, &order_part[0], &order_part[1]})
+      for (AttnItem& a : *list) {
+        if (a.n_rows == 0) continue;
+        const int32_t key0 = a.kv_lo / kMfmaKeys * kMfmaKeys;
+        for (int b = 0; b < 2; ++b)
+          a.pg[b] = kt[a.bt_off + std::min((key0 + 16 * b) / B, a.n_pages - 1)];
+      }
+  }
 
   p->T = (int32_t)rows.size();
   p->n_gather = (int32_t)gather.size();

@@ -109,7 +109,15 @@ struct alignas(16) AttnItem {
   // in consecutive slots)
   int32_t part_slot;
   int32_t n_parts;
-  int32_t pad;
+  // the computed row of the item's first row when its rows are consecutive
+  // computed rows at consecutive positions (then row i is crow0 + i at
+  // position min_pos + i), else -1; and the K block-table entries of the
+  // first key tile's two 16-key blocks: a workgroup can then load its
+  // queries and first tile without reading the row table or the block
+  // table first
+  int32_t crow0;
+  int32_t pg[2];
+  int32_t pad[3];
 };
 
 // A row block of a split item: its rows were computed over n_slots
