@@ -278,11 +278,11 @@ __global__ __launch_bounds__(256 * R, 3) void attn_mfma_kernel(
   const int voff = (2 * kp - 16 * vb) * kD + vc8;
   const int vk = 2 * kp - 16 * vb;         // key within its block
   const int vcol = 16 * vb + ((vk >> 2) & 1) * 8 + ((vk >> 3) & 1) * 4 + (vk & 3);
-  // Page ids of a tile's two 16-key blocks: lane q (mod 2) loads block q's
-  // id with a vector load one tile before the tile's loads need it, and
-  // readlane moves the ids to scalar registers.
-  auto fetch_pages = [&](int j) -> int {
-    return bt[min((j * kKT + 16 * (lane & 1)) >> log2_page, it.n_pages - 1)];
+  // Page ids of a tile's two 16-key blocks: uniform, so scalar loads, one
+  // tile before the tile's loads need them.
+  auto fetch_pages = [&](int j, int& q0, int& q1) __attribute__((always_inline)) {
+    q0 = bt[min((j * kKT) >> log2_page, it.n_pages - 1)];
+    q1 = bt[min((j * kKT + 16) >> log2_page, it.n_pages - 1)];
   };
   auto block_base = [&](int page, int kq) -> int64_t {
     return ((((int64_t)page * n_kv_heads + g) << log2_page) + (kq & page_mask)) * kD;
@@ -294,9 +294,8 @@ __global__ __launch_bounds__(256 * R, 3) void attn_mfma_kernel(
   const int kk = tid & 31, kch = (tid >> 5) & 7;
   uint4 kraw[2];
   bool krot = false, kreg = false;
-  auto load_tile = [&](int j, int pid, uint8_t* kt) __attribute__((always_inline)) {
+  auto load_tile = [&](int j, int p0, int p1, uint8_t* kt) __attribute__((always_inline)) {
     const int key0 = j * kKT;
-    const int p0 = __builtin_amdgcn_readlane(pid, 0), p1 = __builtin_amdgcn_readlane(pid, 1);
     const int64_t b0 = block_base(p0 & ~kPoolPageFlag, key0);
     const int64_t b1 = block_base(p1 & ~kPoolPageFlag, key0 + 16);
     int64_t vbase = vb ? b1 : b0;
@@ -511,9 +510,9 @@ __global__ __launch_bounds__(256 * R, 3) void attn_mfma_kernel(
   const int j0 = it.kv_lo / kKT;
   const int jlo = min(ntiles, (it.kv_lo + kKT - 1) / kKT);   // first tile without keys < kv_lo
   const int nfull = min(ntiles, (it.min_pos + 1) / kKT);      // tiles ending at or before min_pos
-  // ids of the next tile to load (staging waves; the first tile's come
-  // with the item)
-  int pid = (lane & 1) ? it.pg[1] : it.pg[0];
+  // page ids of the next tile to load (staging waves; the first tile's
+  // come with the item)
+  int pp0 = it.pg[0], pp1 = it.pg[1];
   // One tile j: issue the next tile's loads into the other buffers, compute
   // this one, stage the next V^T, wait for this wave's direct K loads, then
   // the workgroup barrier.
@@ -524,8 +523,8 @@ __global__ __launch_bounds__(256 * R, 3) void attn_mfma_kernel(
     for (int j = ja; j < jb; ++j) {
       const bool more = j + 1 < ntiles;
       if (more) {
-        load_tile(j + 1, pid, kl[(j + 1) & 1]);
-        pid = fetch_pages(j + 2);
+        load_tile(j + 1, pp0, pp1, kl[(j + 1) & 1]);
+        fetch_pages(j + 2, pp0, pp1);
       }
       if (!SKIP || j < my_ntiles) tile(j, mask_tag, kl[j & 1], vl[j & 1]);
       if (more) {
@@ -548,8 +547,8 @@ __global__ __launch_bounds__(256 * R, 3) void attn_mfma_kernel(
     }
   };
   if (stager) {
-    load_tile(j0, pid, kl[j0 & 1]);
-    pid = fetch_pages(j0 + 1);
+    load_tile(j0, pp0, pp1, kl[j0 & 1]);
+    fetch_pages(j0 + 1, pp0, pp1);
   }
   // While the first tile is in flight: each row block's cos/sin rows go to
   // LDS (thread t of the block loads 8 dims of cos and sin of row t / 8)
