@@ -476,7 +476,10 @@ def local_leg(torch, sess, wl, qs, ks, vs, out, lse, L, steps, warmup):
            "kernel_us": {"assembly": dist(asm), "attention": d_att},
            "roofline": {"bound": "mfma", "achieved": tf, "peak": peak, "unit": "TFLOP/s",
                         "frac": tf / peak, "kernel": attention_kernel_name(plan, m),
-                        "flops_per_launch": flops}}
+                        "flops_per_launch": flops,
+                        # profiles/local_kernels.md is this leg's counter profile
+                        "traffic": (profiled_traffic("local", attention_kernel_name(plan, m))
+                                    if wl.name == "rag8b" else None)}}
     log(f"[bench] local scope: {res}")
     return res
 
