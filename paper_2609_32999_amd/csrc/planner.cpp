@@ -363,7 +363,8 @@ tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
     return fail(TSR_ERR_OUT_OF_RANGE, "batch too large");
   }
 
-  // attention items: up to rb * kTileRows consecutive rows x KV heads
+  // attention items: up to rb * kTileRows consecutive rows (in item row
+  // order) x KV heads
   // The MFMA kernels give each of their 4 waves per row block one query
   // head; a larger GQA group is split over several items that read the same
   // K/V tiles (adjacent in the launch order, so the repeat reads hit L2).
@@ -446,12 +447,12 @@ tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
   // Both kernels cut their three-row-block items from rows grouped by first
   // visible key (AttnRow order); one-row-block plans keep the computed
   // order.
-  // attn_kernel (1 and 2 for bf16 KV only): 1 the pipelined kernel (attn_pipe.hip, two
-  // row blocks per item; it cannot rotate K on load and its page-id table
-  // bounds an item's keys; measured slower than the row-block kernel on the
-  // RAG batches), 2 the row-block kernel under the rule above (as 0),
-  // 3 / 4 the row-block kernel (or the e4m3 kernel) with three / one row
-  // blocks.
+  // attn_kernel (1 and 2 for bf16 KV only): 1 the pipelined kernel
+  // (attn_pipe.hip, two row blocks per item; it cannot rotate K on load and
+  // its page-id table bounds an item's keys; measured slower than the
+  // row-block kernel on the RAG batches), 2 the row-block kernel under the
+  // rule above (as 0), 3 / 4 the row-block kernel (or the e4m3 kernel) with
+  // three / one row blocks.
   p->row_blocks = 1;
   const bool bf16_kv = m.act_dtype == TSR_BF16 && m.kv_dtype == TSR_BF16;
   auto split_threshold = [&](int64_t total_tiles) -> int64_t {
