@@ -591,8 +591,30 @@ tsr_status build_plan(const tsr_model* model, const tsr_request* reqs,
       bin_load[best] += gcost[g];
     }
     std::vector<std::vector<AttnItem>> bins(kNumXcd);
+    std::vector<const Item*> sel;
     for (const Item& x : items)
-      if (part < 0 || x.part == part) bins[gbin[x.group]].push_back(x.it);
+      if (part < 0 || x.part == part) sel.push_back(&x);
+    int n_groups = 0;
+    for (int64_t c : gcost) n_groups += c > 0;
+    if (n_groups >= kGroupMajorMinGroups * kNumXcd && !sel.empty()) {
+      // many (request, KV head) groups per bin: within each third of the
+      // cost range (longest third first) issue a bin's items group by
+      // group, so the compute units of an XCD work on few groups at a time
+      // and their K/V stays in the caches; the cost thirds keep the longest
+      // items first
+      std::vector<int> grank(gcost.size());
+      for (size_t i = 0; i < gorder.size(); ++i) grank[gorder[i]] = (int)i;
+      std::vector<int64_t> cs;
+      for (const Item* x : sel) cs.push_back(x->cost);
+      std::sort(cs.begin(), cs.end());
+      const int64_t c1 = cs[cs.size() * 2 / 3], c2 = cs[cs.size() / 3];
+      auto tier = [&](int64_t c) { return c >= c1 ? 0 : (c >= c2 ? 1 : 2); };
+      std::stable_sort(sel.begin(), sel.end(), [&](const Item* a, const Item* b) {
+        const int ta = tier(a->cost), tb = tier(b->cost);
+        return ta != tb ? ta < tb : grank[a->group] < grank[b->group];
+      });
+    }
+    for (const Item* x : sel) bins[gbin[x->group]].push_back(x->it);
     size_t per_bin = 0;
     for (auto& b : bins) per_bin = std::max(per_bin, b.size());
     std::vector<AttnItem> order;
