@@ -575,7 +575,8 @@ def main():
     args.legs = [x for x in args.legs.split(",") if x]
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the path "
-              "shards by request or KV head with no exchange, see DESIGN.md", file=sys.stderr)
+              "shards by request or by KV head with no exchange between GPUs, so one GPU's "
+              "share is the same kernels on its requests or heads", file=sys.stderr)
         sys.exit(2)
 
     import torch
